@@ -1,0 +1,249 @@
+/*
+ * swiftcache.h — C ABI of the MI355X layer-wise prefix-KV reload and prefill
+ * attention library (libswiftcache.so, gfx950).
+ *
+ * The library implements the per-layer hot path of a layer stream cache
+ * (paper §3.2 "Layer Stream Cache"): a conversation's cached prefix KV lives
+ * in a donor pool in block-major layout (§3.4); before each layer's attention
+ * the layer's prefix blocks are loaded through a block table into a local
+ * buffer that holds only the active layer (§3.2, §3.3 "KV Load"); the new
+ * turn's K/V are written into that buffer; causal GQA prefill attention runs
+ * over prefix + new tokens (§2.2); the new turn's K/V are written back to
+ * donor blocks (§3.3 "KV Store").
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Element type of every KV, q and output tensor: bf16 (raw 16-bit).
+ *  - Device pointers are HIP device addresses on the pool's device.  Host
+ *    arrays (block tables, lengths) are read synchronously during the call
+ *    and may be freed when it returns.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *    device work is enqueued asynchronously on it; no call synchronises the
+ *    caller's stream.  Caller-owned buffers must stay alive until that work
+ *    has completed.
+ *  - Errors: argument, shape and range errors are detected before any work
+ *    is enqueued and return a negative sc_status; sc_last_error() then gives
+ *    a message (thread-local, valid until the next call on the thread).
+ *    A failed kernel launch returns SC_ERR_HIP.  Faults during asynchronous
+ *    execution surface at the caller's next synchronisation.
+ *  - Packed varlen layout: sequence b of a batch owns query rows
+ *    [cu_q[b], cu_q[b] + N_b) of q/out/k_new/v_new and active-buffer rows
+ *    [cu_k[b], cu_k[b] + P_b + N_b), prefix first, where
+ *    cu_q = exclusive prefix sum of N_b and cu_k = exclusive prefix sum of
+ *    P_b + N_b.
+ *  - Thread safety: distinct objects may be used from distinct threads.
+ *    Calls that enqueue work on the same stream are ordered by the stream.
+ */
+#ifndef SWIFTCACHE_H
+#define SWIFTCACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SC_OK = 0,
+  SC_ERR_INVALID = -1,      /* null pointer, bad enum/flag, malformed table  */
+  SC_ERR_OOM = -2,          /* device or pinned host allocation failed       */
+  SC_ERR_HIP = -3,          /* a HIP runtime call or kernel launch failed    */
+  SC_ERR_RANGE = -4,        /* index or size outside the object's bounds     */
+  SC_ERR_UNSUPPORTED = -5   /* shape the kernels are not built for           */
+} sc_status;
+
+typedef struct sc_pool sc_pool;     /* opaque, library-owned */
+typedef struct sc_table sc_table;   /* opaque, library-owned */
+
+/*
+ * Donor pool description.  Eq. 1 (§3.2) gives the bytes of one block of one
+ * layer: slice_bytes = 2 * block_size * n_kv_heads * head_dim * 2 (bf16).
+ * Block-major layout (§3.4), with Eq. 1's K/V factor made explicit and the
+ * K half first:
+ *     pool[n_blocks][n_layers][2][block_size][n_kv_heads][head_dim]
+ * so one block occupies block_bytes = n_layers * slice_bytes contiguous
+ * bytes, and its layer-l slice starts at l * slice_bytes.
+ *
+ * Block ids [0, n_device_blocks) address the HBM tier (a device allocation
+ * standing in for a co-located model's idle KV memory); ids
+ * [n_device_blocks, n_device_blocks + n_host_blocks) address the host-pinned
+ * tier, whose block k is id n_device_blocks + k.
+ *
+ * device_base / host_base: when non-NULL the pool indexes caller-owned
+ * memory of at least n_device_blocks * block_bytes (device memory on
+ * `device`) and n_host_blocks * block_bytes (pinned host memory from
+ * hipHostMalloc, mapped for device access) bytes, and never frees it.  When
+ * NULL the library allocates the tier (hipMalloc / hipHostMalloc) and frees
+ * it in sc_pool_destroy.
+ */
+typedef struct {
+  int32_t n_layers;
+  int32_t n_kv_heads;
+  int32_t head_dim;          /* 64 or 128 */
+  int32_t block_size;        /* tokens per block, 1..256 */
+  int64_t n_device_blocks;
+  int64_t n_host_blocks;
+  int32_t device;            /* HIP device ordinal */
+  int32_t reserved;          /* must be 0 */
+  void *device_base;         /* optional caller-owned HBM tier */
+  void *host_base;           /* optional caller-owned pinned host tier */
+} sc_pool_desc;
+
+typedef struct {
+  void *device_base;         /* HBM tier base (device address) */
+  void *host_base;           /* pinned host tier base (host address), or NULL */
+  size_t slice_bytes;        /* Eq. 1: bytes of one block of one layer */
+  size_t block_bytes;        /* n_layers * slice_bytes */
+  size_t row_bytes;          /* one token of one layer, K or V: n_kv_heads*head_dim*2 */
+  int64_t n_device_blocks;
+  int64_t n_host_blocks;
+} sc_pool_layout;
+
+/* Active-layer buffer (the layer stream cache slot, §3.2): caller-owned
+ * device arrays K and V, each [capacity_tokens][n_kv_heads][head_dim] bf16. */
+typedef struct {
+  void *k;
+  void *v;
+  int64_t capacity_tokens;
+} sc_active;
+
+/* Create a pool (see sc_pool_desc).  Errors: SC_ERR_INVALID for a null
+ * argument, non-positive sizes or reserved != 0; SC_ERR_UNSUPPORTED for a
+ * head_dim other than 64/128; SC_ERR_OOM when an allocation fails. */
+sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out);
+
+/* Free a pool and any tiers it allocated.  Call only after every stream that
+ * used it has drained.  NULL is ignored. */
+void sc_pool_destroy(sc_pool *pool);
+
+/* Bases and strides of the pool (for filling or reading it). */
+sc_status sc_pool_layout_get(const sc_pool *pool, sc_pool_layout *out);
+
+/*
+ * Block table of a batch of conversations: the master's replica of the donor
+ * block table (§3.5).  Host arrays, copied during the call:
+ *   prefix_len[batch]  P_b >= 0 cached tokens;   new_len[batch]  N_b >= 0;
+ *   cu_blocks[batch+1] offsets into block_ids; sequence b owns exactly
+ *                      ceil((P_b + N_b) / block_size) entries, in token
+ *                      order: logical token t lives in block
+ *                      block_ids[cu_blocks[b] + t / block_size], row
+ *                      t % block_size.  The new turn continues the last,
+ *                      possibly partial, prefix block.
+ *   block_ids[...]     pool block ids, each in range and used at most once
+ *                      within the table.
+ * The table copies its index arrays to the device with hipMemcpyAsync on
+ * `stream` (work issued on other streams must be ordered after it).
+ * Errors: SC_ERR_INVALID (null pointer, batch <= 0, negative length, wrong
+ * entry count, duplicate id), SC_ERR_RANGE (id outside the pool).
+ */
+sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids,
+                          const int32_t *cu_blocks, const int32_t *prefix_len,
+                          const int32_t *new_len, void *stream, sc_table **out);
+void sc_table_destroy(sc_table *table);
+
+/* Totals of a table: sum N_b (query rows) and sum (P_b + N_b) (active rows). */
+sc_status sc_table_totals(const sc_table *table, int64_t *total_q, int64_t *total_kv);
+
+/*
+ * KV Load of one layer (§3.2, §3.3): for every sequence b and prefix token
+ * t < P_b, copy K and V of token t of layer `layer` from its pool block to
+ * rows cu_k[b] + t of dst->k and dst->v.  Token-exact: a partial last prefix
+ * block copies P_b mod block_size rows; rows of new tokens are not written.
+ * Host-tier blocks are read by the kernel over the host link (zero-copy).
+ * The pool is only read.
+ * Errors: SC_ERR_INVALID (null), SC_ERR_RANGE (layer outside [0, n_layers)
+ * or sum(P+N) > dst->capacity_tokens).
+ */
+sc_status sc_fetch_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
+                            const sc_active *dst, void *stream);
+
+/*
+ * Append the new turn (§3.2: new entries are written into the active
+ * buffer): rows cu_q[b] + i of k_new / v_new ([sum N][n_kv_heads][head_dim]
+ * bf16, device) go to rows cu_k[b] + P_b + i of dst->k / dst->v.
+ * Errors: as sc_fetch_layer_kv.
+ */
+sc_status sc_append_new_kv(sc_pool *pool, const sc_table *table, const void *k_new,
+                           const void *v_new, const sc_active *dst, void *stream);
+
+/*
+ * Causal GQA prefill attention of one sequence (§2.2; GQA as in §5):
+ *   out[i][h][:] = sum_{j <= P + i} softmax_j(scale * q[i][h] . k[j][g]) v[j][g]
+ *   with g = h / (n_q_heads / n_kv_heads), for i < new_len, h < n_q_heads.
+ * q, out: [new_len][n_q_heads][head_dim] bf16; k_active, v_active:
+ * [prefix_len + new_len][n_kv_heads][head_dim] bf16 (the prefix rows then
+ * the new rows).  scale <= 0 selects 1/sqrt(head_dim).  lse (nullable):
+ * float [n_q_heads][new_len], the natural-log log-sum-exp of each row's
+ * scaled scores.  Arithmetic: bf16 MFMA products, fp32 accumulation and
+ * softmax, probabilities rounded to bf16 for the PV product, output rounded
+ * to nearest even.  The library may use a device workspace of its own for
+ * split-key partials (one per device and stream, grown on demand).
+ * Errors: SC_ERR_INVALID (null, negative length, n_q_heads not a multiple
+ * of n_kv_heads), SC_ERR_UNSUPPORTED (head_dim not 64/128, group > 16).
+ * new_len == 0 is a no-op.
+ */
+sc_status sc_prefill_attn(const void *q, const void *k_active, const void *v_active,
+                          int32_t prefix_len, int32_t new_len, int32_t n_q_heads,
+                          int32_t n_kv_heads, int32_t head_dim, float scale, void *out,
+                          float *lse, void *stream);
+
+/* The same attention for every sequence of a table (packed varlen layout):
+ * q, out [sum N][n_q_heads][head_dim]; kv = the active buffer filled by
+ * sc_fetch_layer_kv + sc_append_new_kv; lse (nullable) [n_q_heads][sum N]. */
+sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, const void *q,
+                                 const sc_active *kv, int32_t n_q_heads, float scale,
+                                 void *out, float *lse, void *stream);
+
+/*
+ * KV Store of one layer (§3.3): write row cu_q[b] + i of k_new / v_new to
+ * logical position P_b + i of sequence b's block table, layer `layer`.
+ * Only those rows of the pool change.  Host-tier blocks are written over the
+ * host link.
+ * Errors: SC_ERR_INVALID (null), SC_ERR_RANGE (layer out of range).
+ */
+sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
+                            const void *k_new, const void *v_new, void *stream);
+
+/*
+ * The whole layer stack with layer-wise pipelining (§3.3).  Per layer l, slot
+ * s = l % 2 of `slots`:
+ *   copy stream:    wait until attention(l-2) released slot s; fetch(l) and
+ *                   append(l) into slot s; mark slot s ready; store(l).
+ *   compute stream: wait for slot s; attention(l) into out_per_layer[l];
+ *                   release slot s.
+ * so the fetch of layer l+1 runs while layer l's attention runs.  Two slots
+ * are needed because this path has no FFN to hide the load behind (the
+ * paper loads layer i while the FFN of layer i-1 runs).  On return all work
+ * is enqueued and the compute stream is ordered after every store.
+ * Arrays of per-layer device pointers (host arrays of length n_layers):
+ *   q_per_layer, knew_per_layer, vnew_per_layer, out_per_layer.
+ * flags: SC_STACK_OVERLAP (two streams, two slots), SC_STACK_SERIAL
+ * (everything on `compute`, slot 0 only), SC_STACK_ATTN_ONLY (attention
+ * only, over whatever the slots hold: the reference point for the overlap
+ * overhead), optionally | SC_STACK_NO_STORE.  `copy` may be NULL unless
+ * SC_STACK_OVERLAP is set.
+ */
+enum {
+  SC_STACK_OVERLAP = 0,
+  SC_STACK_SERIAL = 1,
+  SC_STACK_ATTN_ONLY = 2,
+  SC_STACK_MODE_MASK = 3,
+  SC_STACK_NO_STORE = 4
+};
+sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers,
+                           const void *const *q_per_layer, const void *const *knew_per_layer,
+                           const void *const *vnew_per_layer, void *const *out_per_layer,
+                           const sc_active *slots /* [2] */, int32_t n_q_heads, float scale,
+                           uint32_t flags, void *compute_stream, void *copy_stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *sc_last_error(void);
+
+/* Library version string. */
+const char *sc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SWIFTCACHE_H */

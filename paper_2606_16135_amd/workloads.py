@@ -1,0 +1,266 @@
+"""Seeded synthetic inputs for the layer-wise prefix-KV reload + prefill path.
+
+This module only draws inputs: block placements, sequence lengths, pool
+contents and per-layer q / k_new / v_new.  It holds none of the method's
+arithmetic (no gather, no attention) and is the one module both the HIP path
+and the oracle consume.
+
+The paper evaluates on multi-turn conversation datasets that are not
+available here; the workloads below are synthetic stand-ins with the shapes
+and length distributions of those conversations: a long cached history
+(prefix) plus a short new turn, KV blocks of 16 tokens scattered over a donor
+pool in block-major layout.
+
+Values are N(0, 1) draws rounded to bf16 (round to nearest even) and kept as
+raw 16-bit patterns.  Pool blocks that no table references are filled with
+the bf16 quiet-NaN pattern 0x7FC0, so any stray read poisons attention.
+"""
+
+import dataclasses
+import math
+
+import numpy as np
+
+BF16_NAN_SENTINEL = 0x7FC0
+SEED_BASE = 26061613500
+
+
+@dataclasses.dataclass
+class Workload:
+    name: str
+    n_layers: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    block_size: int
+    prefix_len: np.ndarray          # int32 [batch]
+    new_len: np.ndarray             # int32 [batch]
+    n_device_blocks: int
+    n_host_blocks: int
+    block_ids: np.ndarray           # int32 [sum ceil((P+N)/B)]
+    cu_blocks: np.ndarray           # int32 [batch + 1]
+    seed: int
+    description: str = ""
+
+    @property
+    def batch(self):
+        return len(self.prefix_len)
+
+    @property
+    def n_blocks(self):
+        return self.n_device_blocks + self.n_host_blocks
+
+    @property
+    def total_q(self):
+        return int(np.sum(self.new_len))
+
+    @property
+    def total_kv(self):
+        return int(np.sum(self.prefix_len) + np.sum(self.new_len))
+
+    @property
+    def row_elems(self):
+        """Elements of one token of one layer for K (or V)."""
+        return self.n_kv_heads * self.head_dim
+
+    @property
+    def block_elems(self):
+        """Elements of one pool block (all layers, K and V)."""
+        return self.n_layers * 2 * self.block_size * self.row_elems
+
+    def pool_shape(self):
+        return (self.n_blocks, self.n_layers, 2, self.block_size,
+                self.n_kv_heads, self.head_dim)
+
+    def seed_for(self, tag):
+        """Sub-seed for one named stream of random numbers."""
+        ss = np.random.SeedSequence([self.seed, _tag_int(tag)])
+        return int(ss.generate_state(1, dtype=np.uint64)[0] >> 1)
+
+
+def _tag_int(tag):
+    h = 1469598103934665603
+    for ch in str(tag).encode():
+        h = ((h ^ ch) * 1099511628211) % (1 << 63)
+    return h
+
+
+def _blocks_for(p, n, bs):
+    return (int(p) + int(n) + bs - 1) // bs
+
+
+def _place(rng, total_blocks, needed):
+    """Seeded random placement: ``needed`` distinct pool block ids."""
+    return rng.permutation(total_blocks)[:needed].astype(np.int32)
+
+
+def make_workload(name, n_layers, n_q_heads, n_kv_heads, head_dim, prefix_len,
+                  new_len, seed, block_size=16, pool_factor=4, host_fraction=0.0,
+                  description=""):
+    """Build a workload with a seeded block placement.
+
+    The pool holds ``pool_factor`` times the blocks the batch needs; a
+    fraction ``host_fraction`` of the pool slots is the host-pinned tier (its
+    ids follow the device tier's).  Table entries are drawn without
+    replacement from all slots, so about ``host_fraction`` of the blocks of
+    each sequence land on the host tier."""
+    prefix_len = np.asarray(prefix_len, dtype=np.int32)
+    new_len = np.asarray(new_len, dtype=np.int32)
+    per_seq = np.array([_blocks_for(p, n, block_size) for p, n in zip(prefix_len, new_len)],
+                       dtype=np.int64)
+    needed = int(per_seq.sum())
+    total = max(needed, int(round(pool_factor * needed)))
+    n_host = int(round(host_fraction * total))
+    n_dev = total - n_host
+    rng = np.random.default_rng(np.random.SeedSequence([seed, _tag_int("placement")]))
+    ids = _place(rng, total, needed)
+    cu = np.concatenate([[0], np.cumsum(per_seq)]).astype(np.int32)
+    return Workload(name=name, n_layers=n_layers, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
+                    head_dim=head_dim, block_size=block_size, prefix_len=prefix_len,
+                    new_len=new_len, n_device_blocks=n_dev, n_host_blocks=n_host,
+                    block_ids=ids, cu_blocks=cu, seed=seed, description=description)
+
+
+def config(index, seed=None):
+    """The five benchmark shapes, numbered 1..5.
+
+    1 tiny: 1 layer, 8/8 heads, D=64, prefix 256 (16 blocks) + new 64, pool of
+      64 blocks, placement = a seeded permutation of the pool.
+    2 Llama-3-8B shape: 32 layers, 32 q / 8 KV heads, D=128, prefix 8192, new
+      512, donor pool 4x what is needed.
+    3 the 8B shape with 16 conversations: prefix ~ lognormal(ln 4096, 0.8)
+      clipped to [512, 32768] and floored; new-turn length uniform integer in
+      [64, 1024]; ragged tables.
+    4 Qwen-14B shape: 48 layers, 40 q / 8 KV heads, D=128, prefix 32768, new
+      1024, pool 4x.
+    5 long context, 8B shape: prefix 131072, new 2048; pool 2x what is needed,
+      half of it on the host-pinned tier.
+    """
+    if seed is None:
+        seed = SEED_BASE + index
+    if index == 1:
+        p, n = [256], [64]
+        wl = make_workload("tiny-L1-H8-D64-P256-N64", 1, 8, 8, 64, p, n, seed,
+                           pool_factor=64 / 20, description="1 layer, 8/8 heads, D=64, P=256, N=64")
+        assert wl.n_blocks == 64
+        return wl
+    if index == 2:
+        return make_workload("llama3-8b-P8192-N512", 32, 32, 8, 128, [8192], [512], seed,
+                             description="32 layers, 32q/8kv heads, D=128, P=8192, N=512, batch 1")
+    if index == 3:
+        rng = np.random.default_rng(np.random.SeedSequence([seed, _tag_int("lengths")]))
+        p = np.floor(np.clip(rng.lognormal(math.log(4096.0), 0.8, size=16), 512, 32768))
+        n = rng.integers(64, 1024, size=16, endpoint=True)
+        return make_workload("llama3-8b-batch16-varlen", 32, 32, 8, 128, p.astype(np.int32),
+                             n.astype(np.int32), seed,
+                             description="32 layers, 32q/8kv, D=128, 16 conversations, "
+                                         "P~lognormal(ln4096,0.8) in [512,32768], N~U[64,1024]")
+    if index == 4:
+        return make_workload("qwen-14b-P32768-N1024", 48, 40, 8, 128, [32768], [1024], seed,
+                             description="48 layers, 40q/8kv heads, D=128, P=32768, N=1024")
+    if index == 5:
+        return make_workload("llama3-8b-P131072-N2048-hosttier", 32, 32, 8, 128, [131072], [2048],
+                             seed, pool_factor=2, host_fraction=0.5,
+                             description="32 layers, 32q/8kv, D=128, P=131072, N=2048, "
+                                         "pool 2x, half host-pinned")
+    raise ValueError(f"unknown config {index}")
+
+
+def small_workload(seed, prefix_len, new_len, n_layers=2, n_q_heads=8, n_kv_heads=2,
+                   head_dim=64, block_size=16, pool_factor=2.0, host_fraction=0.0):
+    """A custom small workload for parity edge cases."""
+    return make_workload(f"small-{seed}", n_layers, n_q_heads, n_kv_heads, head_dim,
+                         prefix_len, new_len, seed, block_size=block_size,
+                         pool_factor=pool_factor, host_fraction=host_fraction)
+
+
+# ----------------------------------------------------------------------------
+# numpy generation (small shapes; CPU tests and parity cases)
+# ----------------------------------------------------------------------------
+
+def f32_to_bf16_bits(x):
+    """Round float32 to bf16 (nearest even) and return the 16-bit patterns.
+    Inputs here are finite normal draws."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def normal_bf16(rng, shape, scale=1.0):
+    return f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32) * np.float32(scale))
+
+
+def pool_numpy(wl):
+    """Pool contents as uint16 of shape ``wl.pool_shape()``: N(0,1) bf16 in
+    every referenced block, the NaN sentinel in every other block."""
+    rng = np.random.default_rng(wl.seed_for("pool"))
+    pool = np.full(wl.pool_shape(), BF16_NAN_SENTINEL, dtype=np.uint16)
+    used = np.unique(wl.block_ids)
+    pool[used] = normal_bf16(rng, (len(used),) + wl.pool_shape()[1:])
+    return pool
+
+
+def layer_inputs_numpy(wl, layer, q_scale=1.0):
+    """q[sum N][H_q][D], k_new and v_new[sum N][H_kv][D] of one layer as
+    uint16 bf16 patterns.  ``q_scale`` > 1 makes the softmax peaky."""
+    rng = np.random.default_rng(wl.seed_for(f"layer{layer}"))
+    t = wl.total_q
+    q = normal_bf16(rng, (t, wl.n_q_heads, wl.head_dim), q_scale)
+    k = normal_bf16(rng, (t, wl.n_kv_heads, wl.head_dim))
+    v = normal_bf16(rng, (t, wl.n_kv_heads, wl.head_dim))
+    return q, k, v
+
+
+# ----------------------------------------------------------------------------
+# torch generation on the device (large shapes).  torch is imported lazily so
+# that CPU-only users of this module do not need it.
+# ----------------------------------------------------------------------------
+
+def _torch_gen(wl, tag, device):
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(wl.seed_for(tag))
+    return g
+
+
+def fill_pool_torch(wl, dev_pool, host_pool=None, chunk_blocks=256):
+    """Fill a device pool tensor (and the host-tier tensor, if any) in place.
+
+    ``dev_pool`` is a bf16 tensor of ``n_device_blocks * block_elems``
+    elements; ``host_pool`` is a pinned CPU tensor for the host tier.
+    Referenced blocks get N(0,1) bf16 values, all others the NaN sentinel.
+    Values are drawn on the device in chunks of blocks."""
+    import torch
+    device = dev_pool.device
+    used = np.zeros(wl.n_blocks, dtype=bool)
+    used[wl.block_ids] = True
+    be = wl.block_elems
+    gen = _torch_gen(wl, "pool-device", device)
+    dv = dev_pool.view(torch.int16).view(wl.n_device_blocks, be)
+    dv.fill_(BF16_NAN_SENTINEL)
+    dev_used = np.nonzero(used[:wl.n_device_blocks])[0]
+    for i in range(0, len(dev_used), chunk_blocks):
+        idx = torch.from_numpy(dev_used[i:i + chunk_blocks]).to(device)
+        vals = torch.randn((len(idx), be), generator=gen, device=device, dtype=torch.float32)
+        dv.index_copy_(0, idx, vals.to(torch.bfloat16).view(torch.int16))
+    if wl.n_host_blocks:
+        assert host_pool is not None
+        hv = host_pool.view(torch.int16).view(wl.n_host_blocks, be)
+        hv.fill_(BF16_NAN_SENTINEL)
+        host_used = np.nonzero(used[wl.n_device_blocks:])[0]
+        genh = _torch_gen(wl, "pool-host", device)
+        for i in range(0, len(host_used), chunk_blocks):
+            sel = host_used[i:i + chunk_blocks]
+            vals = torch.randn((len(sel), be), generator=genh, device=device, dtype=torch.float32)
+            hv[torch.from_numpy(sel)] = vals.to(torch.bfloat16).view(torch.int16).cpu()
+
+
+def layer_inputs_torch(wl, layer, device, q_scale=1.0):
+    """Device bf16 tensors q[sum N][H_q][D], k_new, v_new[sum N][H_kv][D]."""
+    import torch
+    g = _torch_gen(wl, f"layer{layer}", device)
+    t = wl.total_q
+    q = (torch.randn((t, wl.n_q_heads, wl.head_dim), generator=g, device=device) * q_scale)
+    k = torch.randn((t, wl.n_kv_heads, wl.head_dim), generator=g, device=device)
+    v = torch.randn((t, wl.n_kv_heads, wl.head_dim), generator=g, device=device)
+    return q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
