@@ -1,0 +1,201 @@
+"""Benchmark of the layer-wise prefix-KV reload + prefill attention path on one GPU.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+
+A step is one pass of the whole path over one batch: for every layer of the
+stack, fetch the layer's prefix KV from the donor pool through the block
+table, append the new turn, run causal GQA prefill attention over prefix +
+new tokens, and store the new turn back to the pool, with the fetch of layer
+l+1 overlapped with the attention of layer l on a second stream.  The
+default workload is the Llama-3-8B-shaped stack: 32 layers, 32 query / 8 KV
+heads, head_dim 128, one conversation with an 8192-token cached prefix and a
+512-token new turn, donor pool 4x the blocks needed with seeded random
+placement (synthetic N(0,1) bf16 data; inputs are resident in HBM before the
+timed region).
+
+Prints one JSON line.  `value` = new-turn tokens per second through the
+whole stack.  `roofline` is for the attention kernel (MFMA-bound), timed
+with HIP events on its own stream; `details` adds the fetch kernel's HBM
+bandwidth, the attention-only and serial stack times, and the overlap
+overhead.  `cpu_baseline` times the CPU oracle on a bounded sample of the
+same workload (a few layers, extrapolated to the stack).
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "prefill tokens/s incl. layer-wise prefix-KV reload; fetch HBM GB/s; MFMA util"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+PMC_TRAFFIC = None   # HBM bytes per attention launch from rocprofv3 --pmc (see profiles/)
+
+
+def attention_flops(wl):
+    """Algorithmic flops of one layer's attention: 4 * D * H_q per visible
+    (query, key) pair; pairs per sequence = N * P + N (N + 1) / 2."""
+    pairs = sum(int(n) * int(p) + int(n) * (int(n) + 1) // 2 for p, n in zip(wl.prefix_len, wl.new_len))
+    return 4.0 * wl.head_dim * wl.n_q_heads * pairs
+
+
+def fetch_payload_bytes(wl, device_tier_only=True):
+    """Prefix KV bytes moved by one layer's fetch (K and V)."""
+    row = 2 * wl.n_kv_heads * wl.head_dim * 2
+    return row * int(np.sum(wl.prefix_len))
+
+
+def cpu_baseline(wl, dp, inputs, budget_s=15.0):
+    """The oracle (gather + append + attention) timed on the host cores for
+    as many layers as fit in the budget (at least one), extrapolated to the
+    whole stack."""
+    from oracle import attention as oa
+    from oracle import kvcache as ok
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    t_layers = []
+    for layer in range(wl.n_layers):
+        pool_l = dp.layer_slice_u16(layer)
+        q, kn, vn = (t.view(__import__("torch").int16).cpu().numpy().view(np.uint16) for t in inputs[layer])
+        t0 = time.perf_counter()
+        ka, va = ok.gather_layer(pool_l, wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, 0)
+        kf, vf = ok.append_new(ka, va, kn, vn, wl.prefix_len, wl.new_len)
+        oa.attention(oa.bf16_bits_to_f64(q), oa.bf16_bits_to_f64(kf), oa.bf16_bits_to_f64(vf),
+                     wl.prefix_len, wl.new_len)
+        t_layers.append(time.perf_counter() - t0)
+        if sum(t_layers) >= budget_s:
+            break
+    per_layer = float(np.mean(t_layers))
+    return {"value": wl.total_q / (per_layer * wl.n_layers), "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"float64 oracle gather+append+attention on {len(t_layers)} of {wl.n_layers} layers "
+                      f"({per_layer:.2f} s/layer), extrapolated to the {wl.n_layers}-layer stack"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested); "
+              "the path's multi-GPU sharding is described, not run.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_16135_amd import swiftcache as sc
+    from paper_2606_16135_amd import workloads as W
+    from paper_2606_16135_amd.torch_pool import DevicePool
+    sc.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    wl = W.config(args.config)
+    dp = DevicePool(sc, wl, fill="torch")
+    L = wl.n_layers
+    inputs = [W.layer_inputs_torch(wl, l, "cuda") for l in range(L)]
+    outs = [torch.empty((wl.total_q, wl.n_q_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+            for _ in range(L)]
+    slot_t = [(torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda"),
+               torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda"))
+              for _ in range(2)]
+    slots = [sc.active(k.data_ptr(), v.data_ptr(), wl.total_kv) for k, v in slot_t]
+    compute = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+    qp = [i[0].data_ptr() for i in inputs]
+    kp = [i[1].data_ptr() for i in inputs]
+    vp = [i[2].data_ptr() for i in inputs]
+    op = [o.data_ptr() for o in outs]
+
+    def stack(flags):
+        sc.sc_prefill_stack(dp.handle, dp.table, qp, kp, vp, op, slots, wl.n_q_heads, flags, 0.0,
+                            compute.cuda_stream, copy.cuda_stream)
+
+    # ---- headline: overlapped stack --------------------------------------
+    for _ in range(args.warmup):
+        stack(sc.SC_STACK_OVERLAP)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        stack(sc.SC_STACK_OVERLAP)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_step = 1e3 * elapsed / args.steps
+    value = wl.total_q * args.steps / elapsed
+    out_ok = all(bool(torch.isfinite(o.float()).all()) for o in outs)
+
+    def timed_stack(flags, reps):
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record(compute)
+        for _ in range(reps):
+            stack(flags)
+        ev1.record(compute)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / reps
+
+    reps = max(1, args.steps)
+    t_attn_only = timed_stack(sc.SC_STACK_ATTN_ONLY, reps)      # attention kernels of L layers
+    t_serial = timed_stack(sc.SC_STACK_SERIAL, reps)
+    t_overlap = timed_stack(sc.SC_STACK_OVERLAP, reps)
+
+    # ---- fetch kernel alone, timed on its own stream ---------------------
+    with torch.cuda.stream(copy):
+        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        f0.record(copy)
+        for r in range(reps):
+            for l in range(L):
+                sc.sc_fetch_layer_kv(dp.handle, dp.table, l, slots[l & 1], copy.cuda_stream)
+        f1.record(copy)
+    torch.cuda.synchronize()
+    t_fetch = f0.elapsed_time(f1) / (reps * L) * 1e-3          # seconds per layer
+    fetch_gbs = 2.0 * fetch_payload_bytes(wl) / t_fetch / 1e9
+
+    flops = attention_flops(wl)
+    t_attn_layer = t_attn_only / L * 1e-3
+    achieved_tflops = flops / t_attn_layer / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved_tflops, 2), "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved_tflops / BF16_PEAK_TFLOPS, 4),
+                "traffic": PMC_TRAFFIC,
+                "kernel": "attn_fwd_kernel<128> + attn_merge_kernel (one attention call)",
+                "flops_per_launch": flops, "avg_launch_us": round(t_attn_layer * 1e6, 2)}
+
+    details = {
+        "stack_ms": {"overlap": round(t_overlap, 3), "attn_only": round(t_attn_only, 3),
+                     "serial": round(t_serial, 3)},
+        "overlap_overhead": round(t_overlap / t_attn_only - 1.0, 4),
+        "fetch": {"us_per_layer": round(t_fetch * 1e6, 2), "hbm_gbs": round(fetch_gbs, 1),
+                  "frac_of_hbm_peak": round(fetch_gbs / HBM_PEAK_GBS, 4),
+                  "payload_bytes_per_layer": fetch_payload_bytes(wl)},
+        "outputs_finite": out_ok,
+        "device": torch.cuda.get_device_name(0),
+    }
+
+    result = {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
+              "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 3),
+              "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+              "data": "synthetic",
+              "config": {"workload": wl.name, "layers": L, "q_heads": wl.n_q_heads,
+                         "kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
+                         "prefix_len": [int(x) for x in wl.prefix_len][:16],
+                         "new_len": [int(x) for x in wl.new_len][:16], "block_size": wl.block_size,
+                         "pool_blocks": wl.n_blocks, "host_tier_blocks": wl.n_host_blocks},
+              "roofline": roofline, "details": details}
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, dp, inputs)
+    print(json.dumps(result), flush=True)
+    dp.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -237,6 +237,25 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
                            const sc_active *slots /* [2] */, int32_t n_q_heads, float scale,
                            uint32_t flags, void *compute_stream, void *copy_stream);
 
+/*
+ * Host-only introspection of the attention work decomposition (no device
+ * work, no allocation).  For a batch with the given lengths, returns in
+ * *n_items the number of workgroup slots; when `items` is non-NULL it also
+ * receives them as int32 octets
+ *   {seq, kv_head, q0, n_queries, key_begin, key_end, split, 0}
+ * (seq = -1 marks an idle padding slot; slot w runs on XCD w % 8), and when
+ * `splits` is non-NULL it receives each sequence's key-split count.  Every
+ * workgroup covers rows (queries [q0, q0 + n_queries) x the group of query
+ * heads of kv_head) and keys [key_begin, key_end); the splits of one query
+ * tile partition [0, P + q0 + n_queries).  target_items <= 0 selects the
+ * default for a 256-CU device.
+ * Errors: SC_ERR_INVALID (null, negative length, heads as in
+ * sc_prefill_attn), SC_ERR_RANGE (items non-NULL and capacity too small).
+ */
+sc_status sc_attn_plan_query(int32_t batch, const int32_t *prefix_len, const int32_t *new_len,
+                             int32_t n_q_heads, int32_t n_kv_heads, int32_t target_items,
+                             int32_t *n_items, int32_t *items, int32_t capacity, int32_t *splits);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *sc_last_error(void);
 

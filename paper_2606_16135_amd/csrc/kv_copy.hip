@@ -1,0 +1,74 @@
+// Row-copy kernel behind the layer KV load (§3.2 "Layer Stream Cache", §3.3
+// "KV Load"), the append of the new turn into the active buffer (§3.2) and
+// the layer KV store back to donor blocks (§3.3 "KV Store").
+//
+// All three move whole token rows (n_kv_heads * head_dim bf16 = row_bytes)
+// between a block of the block-major pool (§3.4) and a packed buffer, so one
+// kernel serves them: workgroup 2*i copies item i's K rows, workgroup 2*i+1
+// its V rows.  A block slice of one layer is contiguous in the pool (K half
+// then V half, Eq. 1), and consecutive rows of a sequence are contiguous in
+// the active buffer, so each item is one contiguous range on both sides.
+//
+// HBM-bound: every lane moves 16-byte chunks with kUnroll loads in flight
+// before the matching stores; the pool side is read with non-temporal loads
+// (it is streamed once per layer and should not evict the attention's K/V
+// working set from L2).  Host-tier blocks are read or written through their
+// device-visible pinned mapping, over the host link.
+#include "sc_internal.h"
+
+namespace sc {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 8;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(kThreads) void kv_copy_kernel(CopyArgs a) {
+  const int item_idx = blockIdx.x >> 1;
+  const int is_v = blockIdx.x & 1;
+  const CopyItem it = a.items[item_idx];
+  const int64_t nchunks = ((int64_t)it.nrows * a.row_bytes) >> 4;
+  const int64_t half_off = is_v ? a.v_half_off : 0;
+  const char *src;
+  char *dst;
+  bool pool_src;
+  if (a.mode == COPY_FETCH) {
+    src = a.tier_base[it.tier] + it.pool_off + a.layer_off + half_off;
+    dst = (is_v ? a.act_v : a.act_k) + it.act_row * a.row_bytes;
+    pool_src = true;
+  } else if (a.mode == COPY_APPEND) {
+    src = (is_v ? a.new_v : a.new_k) + it.src_row * a.row_bytes;
+    dst = (is_v ? a.act_v : a.act_k) + it.act_row * a.row_bytes;
+    pool_src = false;
+  } else {
+    src = (is_v ? a.new_v : a.new_k) + it.src_row * a.row_bytes;
+    dst = a.tier_base[it.tier] + it.pool_off + a.layer_off + half_off;
+    pool_src = false;
+  }
+  const u32x4 *s = reinterpret_cast<const u32x4 *>(src);
+  u32x4 *d = reinterpret_cast<u32x4 *>(dst);
+  for (int64_t base = 0; base < nchunks; base += (int64_t)kThreads * kUnroll) {
+    u32x4 r[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t idx = base + u * kThreads + threadIdx.x;
+      if (idx < nchunks) r[u] = pool_src ? __builtin_nontemporal_load(s + idx) : s[idx];
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t idx = base + u * kThreads + threadIdx.x;
+      if (idx < nchunks) d[idx] = r[u];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream) {
+  if (a.n_items <= 0) return hipSuccess;
+  hipLaunchKernelGGL(kv_copy_kernel, dim3(2 * a.n_items), dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace sc

@@ -1,0 +1,824 @@
+// Host runtime behind the C ABI in include/swiftcache.h: donor pool tiers,
+// block-table validation and device work lists, the attention planner and
+// split-key workspace, and the two-stream layer pipeline (§3.3).
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <cstdlib>
+#include <memory>
+#include <numeric>
+
+#include "sc_internal.h"
+
+namespace sc {
+
+// ---------------------------------------------------------------------------
+// Errors
+// ---------------------------------------------------------------------------
+static thread_local std::string g_last_error;
+
+sc_status fail(sc_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+sc_status fail_hip(hipError_t e, const char *what) {
+  g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+  return e == hipErrorOutOfMemory ? SC_ERR_OOM : SC_ERR_HIP;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+// Makes `dev` current for the duration of a call and restores the caller's.
+class DeviceGuard {
+ public:
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&old_) != hipSuccess) old_ = -1;
+    if (old_ != dev) ok_ = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    if (old_ >= 0) (void)hipSetDevice(old_);
+  }
+  bool ok() const { return ok_; }
+
+ private:
+  int old_ = -1;
+  bool ok_ = true;
+};
+
+// ---------------------------------------------------------------------------
+// Attention planner
+// ---------------------------------------------------------------------------
+namespace {
+constexpr int kXcds = 8;                 // MI355X: workgroup w is dispatched to XCD w % 8
+constexpr int kMinSplitKeys = 8 * kAttnKeyTile;
+constexpr int kMaxSplits = 16;
+}  // namespace
+
+int attn_target_items(int device) {
+  static std::mutex mu;
+  static std::map<int, int> cache;
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = cache.find(device);
+  if (it != cache.end()) return it->second;
+  int cus = 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) cus = 256;
+  // Two resident workgroups per CU (LDS-limited); ask for 1.5 rounds of them
+  // so that uneven items still balance.
+  int target = cus * 3;
+  if (const char *env = std::getenv("SC_ATTN_TARGET_ITEMS")) target = std::max(1, atoi(env));
+  cache[device] = target;
+  return target;
+}
+
+void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N, int n_q_heads,
+                    int n_kv_heads, int target_items, AttnPlan *plan) {
+  const int group = n_q_heads / n_kv_heads;
+  const int rows_q = kAttnRows / group;
+  const int batch = (int)P.size();
+  plan->group = group;
+  plan->rows_q = rows_q;
+  plan->seqs.assign(batch, SeqDesc{});
+  int64_t n_tiles = 0;
+  int64_t cq = 0, ck = 0;
+  for (int b = 0; b < batch; ++b) {
+    SeqDesc &s = plan->seqs[b];
+    s.cu_q = (int32_t)cq;
+    s.cu_k = (int32_t)ck;
+    s.prefix = P[b];
+    s.n_new = N[b];
+    s.n_splits = 1;
+    cq += N[b];
+    ck += (int64_t)P[b] + N[b];
+    n_tiles += (int64_t)((N[b] + rows_q - 1) / rows_q) * n_kv_heads;
+  }
+  plan->total_q = cq;
+
+  // Split-key chunk: the largest multiple of the key tile that still yields
+  // at least target_items workgroups, but never below kMinSplitKeys.
+  auto items_for = [&](int64_t chunk) {
+    int64_t tot = 0;
+    for (int b = 0; b < batch; ++b) {
+      const int64_t tiles = (int64_t)((N[b] + rows_q - 1) / rows_q) * n_kv_heads;
+      const int64_t kv = (int64_t)P[b] + N[b];
+      const int64_t s = std::min<int64_t>(kMaxSplits, std::max<int64_t>(1, (kv + chunk - 1) / chunk));
+      tot += tiles * s;
+    }
+    return tot;
+  };
+  int64_t max_kv = 0;
+  for (int b = 0; b < batch; ++b) max_kv = std::max<int64_t>(max_kv, (int64_t)P[b] + N[b]);
+  int64_t chunk = std::max<int64_t>(kMinSplitKeys, ((max_kv + kAttnKeyTile - 1) / kAttnKeyTile) * kAttnKeyTile);
+  if (n_tiles > 0 && n_tiles < target_items) {
+    int64_t lo = kMinSplitKeys, hi = chunk;
+    // largest chunk (multiple of the tile) with items_for(chunk) >= target
+    if (items_for(lo) < target_items) {
+      chunk = lo;
+    } else {
+      while (hi - lo > kAttnKeyTile) {
+        int64_t mid = ((lo + hi) / 2 / kAttnKeyTile) * kAttnKeyTile;
+        if (mid <= lo) mid = lo + kAttnKeyTile;
+        if (items_for(mid) >= target_items) lo = mid; else hi = mid;
+      }
+      chunk = lo;
+    }
+  }
+  int max_splits = 1;
+  for (int b = 0; b < batch; ++b) {
+    const int64_t kv = (int64_t)P[b] + N[b];
+    int s = 1;
+    if (n_tiles < target_items)
+      s = (int)std::min<int64_t>(kMaxSplits, std::max<int64_t>(1, (kv + chunk - 1) / chunk));
+    plan->seqs[b].n_splits = s;
+    max_splits = std::max(max_splits, s);
+  }
+  plan->max_splits = max_splits;
+
+  // Items, grouped by (sequence, KV head) so that one group's K/V stays in
+  // one XCD's L2.
+  struct GroupItems {
+    int64_t cost = 0;
+    std::vector<WorkItem> items;
+  };
+  std::vector<GroupItems> groups;
+  for (int b = 0; b < batch; ++b) {
+    const int S = plan->seqs[b].n_splits;
+    for (int g = 0; g < n_kv_heads; ++g) {
+      GroupItems gi;
+      for (int q0 = 0; q0 < N[b]; q0 += rows_q) {
+        const int nq = std::min(rows_q, N[b] - q0);
+        const int keys = P[b] + q0 + nq;
+        const int ntile = (keys + kAttnKeyTile - 1) / kAttnKeyTile;
+        for (int s = 0; s < S; ++s) {
+          const int t0 = (int)((int64_t)s * ntile / S);
+          const int t1 = (int)((int64_t)(s + 1) * ntile / S);
+          WorkItem w{};
+          w.seq = b;
+          w.kvh = g;
+          w.q0 = q0;
+          w.nq = nq;
+          w.k_begin = t0 * kAttnKeyTile;
+          w.k_end = std::min(t1 * kAttnKeyTile, keys);
+          if (w.k_end < w.k_begin) w.k_end = w.k_begin;
+          w.split = s;
+          gi.cost += (w.k_end - w.k_begin) + kAttnKeyTile;
+          gi.items.push_back(w);
+        }
+      }
+      if (!gi.items.empty()) groups.push_back(std::move(gi));
+    }
+  }
+  std::stable_sort(groups.begin(), groups.end(),
+                   [](const GroupItems &x, const GroupItems &y) { return x.cost > y.cost; });
+  std::vector<int64_t> load(kXcds, 0);
+  std::vector<std::vector<WorkItem>> per_xcd(kXcds);
+  for (auto &gi : groups) {
+    const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+    load[x] += gi.cost;
+    per_xcd[x].insert(per_xcd[x].end(), gi.items.begin(), gi.items.end());
+  }
+  size_t max_len = 0;
+  int n_real = 0;
+  for (auto &v : per_xcd) {
+    // Longest items first; equal costs keep split-major order so that the
+    // workgroups resident together read the same key range.
+    std::stable_sort(v.begin(), v.end(), [](const WorkItem &x, const WorkItem &y) {
+      const int cx = x.k_end - x.k_begin, cy = y.k_end - y.k_begin;
+      if (cx != cy) return cx > cy;
+      if (x.seq != y.seq) return x.seq < y.seq;
+      if (x.split != y.split) return x.split < y.split;
+      return x.q0 < y.q0;
+    });
+    max_len = std::max(max_len, v.size());
+    n_real += (int)v.size();
+  }
+  plan->items.assign(max_len * kXcds, WorkItem{-1, 0, 0, 0, 0, 0, 0, 0});
+  for (int x = 0; x < kXcds; ++x)
+    for (size_t j = 0; j < per_xcd[x].size(); ++j) plan->items[j * kXcds + x] = per_xcd[x][j];
+  plan->n_items = (int)plan->items.size();
+  plan->n_real_items = n_real;
+}
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Split-key workspace: one grow-only buffer per (device, stream).  Work on
+// one stream is ordered, so reuse across calls on the same stream is safe.
+// ---------------------------------------------------------------------------
+struct Workspace {
+  void *ptr = nullptr;
+  size_t bytes = 0;
+};
+std::mutex g_ws_mu;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+
+sc_status get_workspace(int device, hipStream_t stream, size_t bytes, void **out) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  Workspace &ws = g_ws[{device, stream}];
+  if (ws.bytes < bytes) {
+    if (ws.ptr) {
+      SC_HIP(hipStreamSynchronize(stream));
+      SC_HIP(hipFree(ws.ptr));
+      ws.ptr = nullptr;
+      ws.bytes = 0;
+    }
+    SC_HIP(hipMalloc(&ws.ptr, bytes));
+    ws.bytes = bytes;
+  }
+  *out = ws.ptr;
+  return SC_OK;
+}
+
+sc_status upload_plan(AttnPlan *plan) {
+  if (plan->n_items == 0) return SC_OK;
+  SC_HIP(hipMalloc(&plan->d_items, plan->items.size() * sizeof(WorkItem)));
+  SC_HIP(hipMalloc(&plan->d_seqs, plan->seqs.size() * sizeof(SeqDesc)));
+  SC_HIP(hipMemcpy(plan->d_items, plan->items.data(), plan->items.size() * sizeof(WorkItem),
+                   hipMemcpyHostToDevice));
+  SC_HIP(hipMemcpy(plan->d_seqs, plan->seqs.data(), plan->seqs.size() * sizeof(SeqDesc),
+                   hipMemcpyHostToDevice));
+  return SC_OK;
+}
+
+void free_plan(AttnPlan *plan) {
+  if (plan->d_items) (void)hipFree(plan->d_items);
+  if (plan->d_seqs) (void)hipFree(plan->d_seqs);
+  plan->d_items = nullptr;
+  plan->d_seqs = nullptr;
+}
+
+// Plans for single-sequence calls, keyed by (device, P, N, Hq, Hkv).
+std::mutex g_plan_mu;
+std::map<std::tuple<int, int, int, int, int>, std::unique_ptr<AttnPlan>> g_single_plans;
+
+sc_status single_plan(int device, int P, int N, int hq, int hkv, AttnPlan **out) {
+  std::lock_guard<std::mutex> lk(g_plan_mu);
+  auto key = std::make_tuple(device, P, N, hq, hkv);
+  auto it = g_single_plans.find(key);
+  if (it != g_single_plans.end()) {
+    *out = it->second.get();
+    return SC_OK;
+  }
+  if (g_single_plans.size() >= 256) {
+    // Plans may still be referenced by queued kernels: drain before freeing.
+    SC_HIP(hipDeviceSynchronize());
+    for (auto &kv : g_single_plans) free_plan(kv.second.get());
+    g_single_plans.clear();
+  }
+  auto plan = std::make_unique<AttnPlan>();
+  plan_attention({P}, {N}, hq, hkv, attn_target_items(device), plan.get());
+  sc_status st = upload_plan(plan.get());
+  if (st != SC_OK) {
+    free_plan(plan.get());
+    return st;
+  }
+  *out = plan.get();
+  g_single_plans[key] = std::move(plan);
+  return SC_OK;
+}
+
+sc_status run_attention(int device, const AttnPlan &plan, const void *q, const void *k, const void *v,
+                        void *out, float *lse, int hq, int hkv, int head_dim, float scale,
+                        hipStream_t stream) {
+  if (plan.n_items == 0) return SC_OK;
+  AttnArgs a{};
+  a.q = static_cast<const uint16_t *>(q);
+  a.k = static_cast<const uint16_t *>(k);
+  a.v = static_cast<const uint16_t *>(v);
+  a.out = static_cast<uint16_t *>(out);
+  a.lse = lse;
+  a.items = plan.d_items;
+  a.seqs = plan.d_seqs;
+  a.n_seqs = (int32_t)plan.seqs.size();
+  a.total_q = (int32_t)plan.total_q;
+  a.n_q_heads = hq;
+  a.n_kv_heads = hkv;
+  a.group = plan.group;
+  a.rows_q = plan.rows_q;
+  if (!(scale > 0.f)) scale = 1.f / std::sqrt((float)head_dim);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  if (plan.max_splits > 1) {
+    const size_t rows = (size_t)plan.max_splits * plan.total_q * hq;
+    void *ws = nullptr;
+    sc_status st = get_workspace(device, stream, rows * ((size_t)head_dim + 1) * sizeof(float), &ws);
+    if (st != SC_OK) return st;
+    a.part_o = static_cast<float *>(ws);
+    a.part_lse = a.part_o + rows * head_dim;
+  }
+  hipError_t e = launch_attn_fwd(a, head_dim, plan.n_items, stream);
+  if (e != hipSuccess) return fail_hip(e, "attn_fwd launch");
+  if (plan.max_splits > 1) {
+    e = launch_attn_merge(a, head_dim, stream);
+    if (e != hipSuccess) return fail_hip(e, "attn_merge launch");
+  }
+  return SC_OK;
+}
+
+sc_status check_heads(int hq, int hkv, int head_dim) {
+  if (hq <= 0 || hkv <= 0 || hq % hkv != 0)
+    return fail(SC_ERR_INVALID, "n_q_heads (%d) must be a positive multiple of n_kv_heads (%d)", hq, hkv);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(SC_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", head_dim);
+  if (hq / hkv > 16) return fail(SC_ERR_UNSUPPORTED, "GQA group %d > 16 not supported", hq / hkv);
+  return SC_OK;
+}
+
+sc_status table_plan(sc_table *t, int hq, AttnPlan **out) {
+  const sc_pool_desc &d = t->pool->desc;
+  sc_status st = check_heads(hq, d.n_kv_heads, d.head_dim);
+  if (st != SC_OK) return st;
+  std::lock_guard<std::mutex> lk(t->mu);
+  auto key = std::make_pair(hq, d.n_kv_heads);
+  auto it = t->plans.find(key);
+  if (it != t->plans.end()) {
+    *out = &it->second;
+    return SC_OK;
+  }
+  AttnPlan &plan = t->plans[key];
+  plan_attention(t->P, t->N, hq, d.n_kv_heads, attn_target_items(d.device), &plan);
+  st = upload_plan(&plan);
+  if (st != SC_OK) {
+    free_plan(&plan);
+    t->plans.erase(key);
+    return st;
+  }
+  *out = &plan;
+  return SC_OK;
+}
+
+CopyArgs copy_args(const sc_pool *p, const sc_table *t, int mode) {
+  CopyArgs a{};
+  a.mode = mode;
+  a.row_bytes = (int64_t)p->row_bytes;
+  a.v_half_off = (int64_t)(p->slice_bytes / 2);
+  a.tier_base[0] = p->dev_base;
+  a.tier_base[1] = p->host_dev;
+  if (mode == COPY_FETCH) {
+    a.items = t->d_items;
+    a.n_items = t->n_fetch;
+  } else if (mode == COPY_APPEND) {
+    a.items = t->d_items + t->n_fetch;
+    a.n_items = t->n_append;
+  } else {
+    a.items = t->d_items + t->n_fetch + t->n_append;
+    a.n_items = t->n_store;
+  }
+  return a;
+}
+
+sc_status check_active(const sc_table *t, const sc_active *dst) {
+  if (dst == nullptr || dst->k == nullptr || dst->v == nullptr)
+    return fail(SC_ERR_INVALID, "null active buffer");
+  if (dst->capacity_tokens < t->total_kv)
+    return fail(SC_ERR_RANGE, "active buffer holds %lld tokens, the table needs %lld",
+                (long long)dst->capacity_tokens, (long long)t->total_kv);
+  return SC_OK;
+}
+
+sc_status do_fetch(sc_pool *p, const sc_table *t, int layer, const sc_active *dst, hipStream_t s) {
+  CopyArgs a = copy_args(p, t, COPY_FETCH);
+  a.layer_off = (int64_t)layer * (int64_t)p->slice_bytes;
+  a.act_k = static_cast<char *>(dst->k);
+  a.act_v = static_cast<char *>(dst->v);
+  hipError_t e = launch_kv_copy(a, s);
+  return e == hipSuccess ? SC_OK : fail_hip(e, "fetch launch");
+}
+
+sc_status do_append(sc_pool *p, const sc_table *t, const void *kn, const void *vn, const sc_active *dst,
+                    hipStream_t s) {
+  CopyArgs a = copy_args(p, t, COPY_APPEND);
+  a.new_k = static_cast<const char *>(kn);
+  a.new_v = static_cast<const char *>(vn);
+  a.act_k = static_cast<char *>(dst->k);
+  a.act_v = static_cast<char *>(dst->v);
+  hipError_t e = launch_kv_copy(a, s);
+  return e == hipSuccess ? SC_OK : fail_hip(e, "append launch");
+}
+
+sc_status do_store(sc_pool *p, const sc_table *t, int layer, const void *kn, const void *vn, hipStream_t s) {
+  CopyArgs a = copy_args(p, t, COPY_STORE);
+  a.layer_off = (int64_t)layer * (int64_t)p->slice_bytes;
+  a.new_k = static_cast<const char *>(kn);
+  a.new_v = static_cast<const char *>(vn);
+  hipError_t e = launch_kv_copy(a, s);
+  return e == hipSuccess ? SC_OK : fail_hip(e, "store launch");
+}
+
+}  // namespace
+}  // namespace sc
+
+using namespace sc;
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+const char *sc_last_error(void) { return g_last_error.c_str(); }
+
+const char *sc_version(void) { return "swiftcache-mi355x 0.1 (gfx950)"; }
+
+sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
+  clear_error();
+  if (desc == nullptr || out == nullptr) return fail(SC_ERR_INVALID, "null argument");
+  *out = nullptr;
+  const sc_pool_desc &d = *desc;
+  if (d.n_layers <= 0 || d.n_kv_heads <= 0 || d.block_size <= 0 || d.block_size > 256 ||
+      d.n_device_blocks < 0 || d.n_host_blocks < 0 || d.n_device_blocks + d.n_host_blocks <= 0 ||
+      d.reserved != 0)
+    return fail(SC_ERR_INVALID, "invalid pool description");
+  if (d.head_dim != 64 && d.head_dim != 128)
+    return fail(SC_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", d.head_dim);
+  if (d.n_device_blocks + d.n_host_blocks > INT32_MAX)
+    return fail(SC_ERR_RANGE, "too many blocks for 32-bit block ids");
+  // Pools over caller-owned HBM without a host tier make no HIP call here.
+  const bool needs_hip = (d.n_device_blocks > 0 && !d.device_base) || d.n_host_blocks > 0;
+  std::unique_ptr<DeviceGuard> guard;
+  if (needs_hip) {
+    guard.reset(new DeviceGuard(d.device));
+    if (!guard->ok()) return fail(SC_ERR_INVALID, "cannot select device %d", d.device);
+  }
+  std::unique_ptr<sc_pool> p(new sc_pool());
+  p->desc = d;
+  p->row_bytes = (size_t)d.n_kv_heads * d.head_dim * 2;
+  p->slice_bytes = 2 * (size_t)d.block_size * p->row_bytes;   // Eq. 1 with bf16
+  p->block_bytes = (size_t)d.n_layers * p->slice_bytes;
+  const size_t dev_bytes = (size_t)d.n_device_blocks * p->block_bytes;
+  const size_t host_bytes = (size_t)d.n_host_blocks * p->block_bytes;
+  if (d.n_device_blocks > 0) {
+    if (d.device_base) {
+      p->dev_base = static_cast<char *>(d.device_base);
+    } else {
+      hipError_t e = hipMalloc(reinterpret_cast<void **>(&p->dev_base), dev_bytes);
+      if (e != hipSuccess) return fail(SC_ERR_OOM, "hipMalloc(%zu) for the device tier: %s", dev_bytes,
+                                       hipGetErrorString(e));
+      p->own_dev = true;
+    }
+  }
+  if (d.n_host_blocks > 0) {
+    if (d.host_base) {
+      p->host_base = static_cast<char *>(d.host_base);
+    } else {
+      hipError_t e = hipHostMalloc(reinterpret_cast<void **>(&p->host_base), host_bytes,
+                                   hipHostMallocMapped | hipHostMallocPortable);
+      if (e != hipSuccess) {
+        if (p->own_dev) (void)hipFree(p->dev_base);
+        return fail(SC_ERR_OOM, "hipHostMalloc(%zu) for the host tier: %s", host_bytes, hipGetErrorString(e));
+      }
+      p->own_host = true;
+    }
+    void *devp = nullptr;
+    hipError_t e = hipHostGetDevicePointer(&devp, p->host_base, 0);
+    if (e != hipSuccess || devp == nullptr) {
+      if (p->own_dev) (void)hipFree(p->dev_base);
+      if (p->own_host) (void)hipHostFree(p->host_base);
+      return fail(SC_ERR_INVALID, "host tier is not pinned, mapped memory: %s", hipGetErrorString(e));
+    }
+    p->host_dev = static_cast<char *>(devp);
+  }
+  *out = p.release();
+  return SC_OK;
+}
+
+void sc_pool_destroy(sc_pool *pool) {
+  if (!pool) return;
+  if (pool->own_dev || pool->own_host) {
+    DeviceGuard guard(pool->desc.device);
+    if (pool->own_dev && pool->dev_base) (void)hipFree(pool->dev_base);
+    if (pool->own_host && pool->host_base) (void)hipHostFree(pool->host_base);
+  }
+  delete pool;
+}
+
+sc_status sc_pool_layout_get(const sc_pool *pool, sc_pool_layout *out) {
+  clear_error();
+  if (!pool || !out) return fail(SC_ERR_INVALID, "null argument");
+  out->device_base = pool->dev_base;
+  out->host_base = pool->host_base;
+  out->slice_bytes = pool->slice_bytes;
+  out->block_bytes = pool->block_bytes;
+  out->row_bytes = pool->row_bytes;
+  out->n_device_blocks = pool->desc.n_device_blocks;
+  out->n_host_blocks = pool->desc.n_host_blocks;
+  return SC_OK;
+}
+
+sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids, const int32_t *cu_blocks,
+                          const int32_t *prefix_len, const int32_t *new_len, void *stream, sc_table **out) {
+  clear_error();
+  if (!pool || !cu_blocks || !prefix_len || !new_len || !out) return fail(SC_ERR_INVALID, "null argument");
+  *out = nullptr;
+  if (batch <= 0) return fail(SC_ERR_INVALID, "batch must be positive (got %d)", batch);
+  const int bs = pool->desc.block_size;
+  const int64_t n_dev = pool->desc.n_device_blocks;
+  const int64_t n_all = n_dev + pool->desc.n_host_blocks;
+  if (cu_blocks[0] != 0) return fail(SC_ERR_INVALID, "cu_blocks[0] must be 0");
+  int64_t total_kv = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (prefix_len[b] < 0 || new_len[b] < 0)
+      return fail(SC_ERR_INVALID, "negative length in sequence %d", b);
+    const int64_t need = ((int64_t)prefix_len[b] + new_len[b] + bs - 1) / bs;
+    if ((int64_t)cu_blocks[b + 1] - cu_blocks[b] != need)
+      return fail(SC_ERR_INVALID, "sequence %d lists %d blocks, needs ceil((%d+%d)/%d) = %lld", b,
+                  cu_blocks[b + 1] - cu_blocks[b], prefix_len[b], new_len[b], bs, (long long)need);
+    total_kv += (int64_t)prefix_len[b] + new_len[b];
+  }
+  if (total_kv >= INT32_MAX) return fail(SC_ERR_RANGE, "batch too long for 32-bit row indices");
+  const int64_t n_ids = cu_blocks[batch];
+  if (n_ids > 0 && !block_ids) return fail(SC_ERR_INVALID, "null block_ids");
+  std::vector<uint8_t> seen((size_t)n_all, 0);
+  for (int64_t i = 0; i < n_ids; ++i) {
+    const int32_t id = block_ids[i];
+    if (id < 0 || id >= n_all)
+      return fail(SC_ERR_RANGE, "block id %d at entry %lld outside the pool [0, %lld)", id, (long long)i,
+                  (long long)n_all);
+    if (seen[id]) return fail(SC_ERR_INVALID, "block id %d used twice in one table", id);
+    seen[id] = 1;
+  }
+
+  std::unique_ptr<sc_table> t(new sc_table());
+  t->pool = pool;
+  t->batch = batch;
+  t->P.assign(prefix_len, prefix_len + batch);
+  t->N.assign(new_len, new_len + batch);
+  t->cu_q.assign(batch + 1, 0);
+  t->cu_k.assign(batch + 1, 0);
+  for (int b = 0; b < batch; ++b) {
+    t->cu_q[b + 1] = t->cu_q[b] + new_len[b];
+    t->cu_k[b + 1] = t->cu_k[b] + prefix_len[b] + new_len[b];
+  }
+  t->total_q = t->cu_q[batch];
+  t->total_kv = t->cu_k[batch];
+
+  auto locate = [&](int32_t id, CopyItem *it) {
+    it->tier = id >= n_dev ? 1 : 0;
+    const int64_t local = it->tier ? id - n_dev : id;
+    it->pool_off = local * (int64_t)pool->block_bytes;
+  };
+  std::vector<CopyItem> fetch, append, store;
+  for (int b = 0; b < batch; ++b) {
+    const int32_t *ids = block_ids + cu_blocks[b];
+    const int P = prefix_len[b], N = new_len[b];
+    for (int j = 0; j * bs < P; ++j) {
+      CopyItem it{};
+      locate(ids[j], &it);
+      it.act_row = t->cu_k[b] + (int64_t)j * bs;
+      it.nrows = std::min(bs, P - j * bs);
+      fetch.push_back(it);
+    }
+    for (int i0 = 0; i0 < N; i0 += bs) {
+      CopyItem it{};
+      it.src_row = t->cu_q[b] + i0;
+      it.act_row = t->cu_k[b] + P + i0;
+      it.nrows = std::min(bs, N - i0);
+      append.push_back(it);
+    }
+    for (int64_t pos = P; pos < (int64_t)P + N;) {
+      const int64_t blk = pos / bs;
+      const int64_t end = std::min<int64_t>((blk + 1) * bs, (int64_t)P + N);
+      CopyItem it{};
+      locate(ids[blk], &it);
+      it.pool_off += (pos % bs) * (int64_t)pool->row_bytes;
+      it.src_row = t->cu_q[b] + (pos - P);
+      it.nrows = (int32_t)(end - pos);
+      store.push_back(it);
+      pos = end;
+    }
+  }
+  t->n_fetch = (int32_t)fetch.size();
+  t->n_append = (int32_t)append.size();
+  t->n_store = (int32_t)store.size();
+  std::vector<CopyItem> &all = t->h_items;
+  all.reserve(fetch.size() + append.size() + store.size());
+  all.insert(all.end(), fetch.begin(), fetch.end());
+  all.insert(all.end(), append.begin(), append.end());
+  all.insert(all.end(), store.begin(), store.end());
+  DeviceGuard guard(pool->desc.device);
+  if (!all.empty()) {
+    const size_t bytes = all.size() * sizeof(CopyItem);
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(&t->d_items), bytes);
+    if (e != hipSuccess) return fail(SC_ERR_OOM, "hipMalloc for table items: %s", hipGetErrorString(e));
+    // The source stays alive in the table until it is destroyed.
+    e = hipMemcpyAsync(t->d_items, all.data(), bytes, hipMemcpyHostToDevice, (hipStream_t)stream);
+    if (e != hipSuccess) {
+      (void)hipFree(t->d_items);
+      return fail_hip(e, "table upload");
+    }
+  }
+  *out = t.release();
+  return SC_OK;
+}
+
+void sc_table_destroy(sc_table *table) {
+  if (!table) return;
+  if (table->d_items || !table->plans.empty()) {
+    DeviceGuard guard(table->pool->desc.device);
+    if (table->d_items) (void)hipFree(table->d_items);
+    for (auto &kv : table->plans) free_plan(&kv.second);
+  }
+  delete table;
+}
+
+sc_status sc_attn_plan_query(int32_t batch, const int32_t *prefix_len, const int32_t *new_len,
+                             int32_t n_q_heads, int32_t n_kv_heads, int32_t target_items, int32_t *n_items,
+                             int32_t *items, int32_t capacity, int32_t *splits) {
+  clear_error();
+  if (batch <= 0 || !prefix_len || !new_len || !n_items) return fail(SC_ERR_INVALID, "null argument");
+  sc_status st = check_heads(n_q_heads, n_kv_heads, 128);
+  if (st != SC_OK) return st;
+  for (int b = 0; b < batch; ++b)
+    if (prefix_len[b] < 0 || new_len[b] < 0) return fail(SC_ERR_INVALID, "negative length");
+  AttnPlan plan;
+  plan_attention(std::vector<int32_t>(prefix_len, prefix_len + batch),
+                 std::vector<int32_t>(new_len, new_len + batch), n_q_heads, n_kv_heads,
+                 target_items > 0 ? target_items : 768, &plan);
+  *n_items = plan.n_items;
+  if (items) {
+    if (capacity < plan.n_items) return fail(SC_ERR_RANGE, "capacity %d < %d items", capacity, plan.n_items);
+    std::memcpy(items, plan.items.data(), plan.items.size() * sizeof(WorkItem));
+  }
+  if (splits)
+    for (int b = 0; b < batch; ++b) splits[b] = plan.seqs[b].n_splits;
+  return SC_OK;
+}
+
+sc_status sc_table_totals(const sc_table *table, int64_t *total_q, int64_t *total_kv) {
+  clear_error();
+  if (!table) return fail(SC_ERR_INVALID, "null table");
+  if (total_q) *total_q = table->total_q;
+  if (total_kv) *total_kv = table->total_kv;
+  return SC_OK;
+}
+
+sc_status sc_fetch_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer, const sc_active *dst,
+                            void *stream) {
+  clear_error();
+  if (!pool || !table) return fail(SC_ERR_INVALID, "null argument");
+  if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
+  if (layer < 0 || layer >= pool->desc.n_layers)
+    return fail(SC_ERR_RANGE, "layer %d outside [0, %d)", layer, pool->desc.n_layers);
+  sc_status st = check_active(table, dst);
+  if (st != SC_OK) return st;
+  DeviceGuard guard(pool->desc.device);
+  return do_fetch(pool, table, layer, dst, (hipStream_t)stream);
+}
+
+sc_status sc_append_new_kv(sc_pool *pool, const sc_table *table, const void *k_new, const void *v_new,
+                           const sc_active *dst, void *stream) {
+  clear_error();
+  if (!pool || !table) return fail(SC_ERR_INVALID, "null argument");
+  if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
+  if (table->total_q > 0 && (!k_new || !v_new)) return fail(SC_ERR_INVALID, "null k_new/v_new");
+  sc_status st = check_active(table, dst);
+  if (st != SC_OK) return st;
+  DeviceGuard guard(pool->desc.device);
+  return do_append(pool, table, k_new, v_new, dst, (hipStream_t)stream);
+}
+
+sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer, const void *k_new,
+                            const void *v_new, void *stream) {
+  clear_error();
+  if (!pool || !table) return fail(SC_ERR_INVALID, "null argument");
+  if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
+  if (layer < 0 || layer >= pool->desc.n_layers)
+    return fail(SC_ERR_RANGE, "layer %d outside [0, %d)", layer, pool->desc.n_layers);
+  if (table->total_q > 0 && (!k_new || !v_new)) return fail(SC_ERR_INVALID, "null k_new/v_new");
+  DeviceGuard guard(pool->desc.device);
+  return do_store(pool, table, layer, k_new, v_new, (hipStream_t)stream);
+}
+
+sc_status sc_prefill_attn(const void *q, const void *k_active, const void *v_active, int32_t prefix_len,
+                          int32_t new_len, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, float scale,
+                          void *out, float *lse, void *stream) {
+  clear_error();
+  if (prefix_len < 0 || new_len < 0) return fail(SC_ERR_INVALID, "negative length");
+  sc_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
+  if (st != SC_OK) return st;
+  if (new_len == 0) return SC_OK;
+  if (!q || !k_active || !v_active || !out) return fail(SC_ERR_INVALID, "null argument");
+  int device = 0;
+  SC_HIP(hipGetDevice(&device));
+  AttnPlan *plan = nullptr;
+  st = single_plan(device, prefix_len, new_len, n_q_heads, n_kv_heads, &plan);
+  if (st != SC_OK) return st;
+  return run_attention(device, *plan, q, k_active, v_active, out, lse, n_q_heads, n_kv_heads, head_dim,
+                       scale, (hipStream_t)stream);
+}
+
+sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, const void *q, const sc_active *kv,
+                                 int32_t n_q_heads, float scale, void *out, float *lse, void *stream) {
+  clear_error();
+  if (!pool || !table) return fail(SC_ERR_INVALID, "null argument");
+  if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
+  sc_status st = check_active(table, kv);
+  if (st != SC_OK) return st;
+  if (table->total_q == 0) return SC_OK;
+  if (!q || !out) return fail(SC_ERR_INVALID, "null argument");
+  DeviceGuard guard(pool->desc.device);
+  AttnPlan *plan = nullptr;
+  st = table_plan(const_cast<sc_table *>(table), n_q_heads, &plan);
+  if (st != SC_OK) return st;
+  const sc_pool_desc &d = pool->desc;
+  return run_attention(d.device, *plan, q, kv->k, kv->v, out, lse, n_q_heads, d.n_kv_heads, d.head_dim, scale,
+                       (hipStream_t)stream);
+}
+
+sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, const void *const *q_per_layer,
+                           const void *const *knew_per_layer, const void *const *vnew_per_layer,
+                           void *const *out_per_layer, const sc_active *slots, int32_t n_q_heads, float scale,
+                           uint32_t flags, void *compute_stream, void *copy_stream) {
+  clear_error();
+  if (!pool || !table || !q_per_layer || !knew_per_layer || !vnew_per_layer || !out_per_layer || !slots)
+    return fail(SC_ERR_INVALID, "null argument");
+  if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
+  if (n_layers <= 0 || n_layers > pool->desc.n_layers)
+    return fail(SC_ERR_RANGE, "n_layers %d outside [1, %d]", n_layers, pool->desc.n_layers);
+  if (flags & ~(uint32_t)(SC_STACK_MODE_MASK | SC_STACK_NO_STORE)) return fail(SC_ERR_INVALID, "unknown flags");
+  const uint32_t mode = flags & SC_STACK_MODE_MASK;
+  if (mode > SC_STACK_ATTN_ONLY) return fail(SC_ERR_INVALID, "unknown stack mode");
+  const bool do_st = !(flags & SC_STACK_NO_STORE);
+  const int n_slots = mode == SC_STACK_SERIAL ? 1 : 2;
+  for (int s = 0; s < n_slots; ++s) {
+    sc_status st = check_active(table, &slots[s]);
+    if (st != SC_OK) return st;
+  }
+  if (mode == SC_STACK_OVERLAP && copy_stream == nullptr)
+    return fail(SC_ERR_INVALID, "overlapped mode needs a copy stream");
+  for (int l = 0; l < n_layers; ++l) {
+    if (!q_per_layer[l] || !out_per_layer[l] || (table->total_q > 0 && (!knew_per_layer[l] || !vnew_per_layer[l])))
+      return fail(SC_ERR_INVALID, "null per-layer pointer at layer %d", l);
+  }
+  DeviceGuard guard(pool->desc.device);
+  AttnPlan *plan = nullptr;
+  sc_status st = table_plan(const_cast<sc_table *>(table), n_q_heads, &plan);
+  if (st != SC_OK) return st;
+  const sc_pool_desc &d = pool->desc;
+  hipStream_t cs = (hipStream_t)compute_stream;
+  hipStream_t xs = (hipStream_t)copy_stream;
+  auto attn = [&](int l, const sc_active &slot) {
+    return run_attention(d.device, *plan, q_per_layer[l], slot.k, slot.v, out_per_layer[l], nullptr, n_q_heads,
+                         d.n_kv_heads, d.head_dim, scale, cs);
+  };
+
+  if (mode == SC_STACK_ATTN_ONLY) {
+    for (int l = 0; l < n_layers; ++l) {
+      st = attn(l, slots[l & 1]);
+      if (st != SC_OK) return st;
+    }
+    return SC_OK;
+  }
+  if (mode == SC_STACK_SERIAL) {
+    for (int l = 0; l < n_layers; ++l) {
+      if ((st = do_fetch(pool, table, l, &slots[0], cs)) != SC_OK) return st;
+      if ((st = do_append(pool, table, knew_per_layer[l], vnew_per_layer[l], &slots[0], cs)) != SC_OK) return st;
+      if ((st = attn(l, slots[0])) != SC_OK) return st;
+      if (do_st && (st = do_store(pool, table, l, knew_per_layer[l], vnew_per_layer[l], cs)) != SC_OK) return st;
+    }
+    return SC_OK;
+  }
+
+  // Overlapped: events ready[s] (slot s filled) and free_[s] (slot s read).
+  hipEvent_t ev[5] = {};
+  for (auto &e : ev) {
+    hipError_t he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+    if (he != hipSuccess) {
+      for (auto &x : ev)
+        if (x) (void)hipEventDestroy(x);
+      return fail_hip(he, "hipEventCreate");
+    }
+  }
+  hipEvent_t *ready = ev, *free_ = ev + 2, start = ev[4];
+  auto body = [&]() -> sc_status {
+    // The copy stream starts after everything already queued on `compute`.
+    SC_HIP(hipEventRecord(start, cs));
+    SC_HIP(hipStreamWaitEvent(xs, start, 0));
+    for (int l = 0; l < n_layers; ++l) {
+      const int s = l & 1;
+      if (l >= 2) SC_HIP(hipStreamWaitEvent(xs, free_[s], 0));
+      sc_status r;
+      if ((r = do_fetch(pool, table, l, &slots[s], xs)) != SC_OK) return r;
+      if ((r = do_append(pool, table, knew_per_layer[l], vnew_per_layer[l], &slots[s], xs)) != SC_OK) return r;
+      SC_HIP(hipEventRecord(ready[s], xs));
+      if (do_st && (r = do_store(pool, table, l, knew_per_layer[l], vnew_per_layer[l], xs)) != SC_OK) return r;
+      SC_HIP(hipStreamWaitEvent(cs, ready[s], 0));
+      if ((r = attn(l, slots[s])) != SC_OK) return r;
+      SC_HIP(hipEventRecord(free_[s], cs));
+    }
+    // The compute stream ends after the last store.
+    SC_HIP(hipEventRecord(start, xs));
+    SC_HIP(hipStreamWaitEvent(cs, start, 0));
+    return SC_OK;
+  };
+  st = body();
+  for (auto &e : ev) (void)hipEventDestroy(e);
+  return st;
+}
+
+}  // extern "C"

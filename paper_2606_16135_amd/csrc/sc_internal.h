@@ -1,0 +1,165 @@
+// Internal declarations shared by the host runtime (sc_api.cpp) and the
+// kernel translation units (kv_copy.hip, attn_fwd.hip).  Not installed.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <map>
+#include <mutex>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/swiftcache.h"
+
+namespace sc {
+
+// ---------------------------------------------------------------------------
+// Error state
+// ---------------------------------------------------------------------------
+sc_status fail(sc_status st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+sc_status fail_hip(hipError_t e, const char *what);
+void clear_error();
+
+#define SC_HIP(call)                                   \
+  do {                                                 \
+    hipError_t e_ = (call);                            \
+    if (e_ != hipSuccess) return ::sc::fail_hip(e_, #call); \
+  } while (0)
+
+// ---------------------------------------------------------------------------
+// Copy work items (fetch / append / store).  One item moves `nrows` token
+// rows of K and, in a second workgroup, of V.
+//   FETCH : pool tier `tier` at byte offset pool_off (+ layer slice) -> active
+//           rows starting at act_row.
+//   APPEND: k_new rows starting at src_row -> active rows starting at act_row.
+//   STORE : k_new rows starting at src_row -> pool tier at pool_off (+ layer).
+// ---------------------------------------------------------------------------
+struct CopyItem {
+  int64_t pool_off;   // bytes from the tier base to the first row (layer 0, K half)
+  int64_t act_row;    // first row in the active buffer (FETCH/APPEND)
+  int64_t src_row;    // first row of k_new / v_new (APPEND/STORE)
+  int32_t nrows;
+  int32_t tier;       // 0 = device tier, 1 = host tier
+};
+static_assert(sizeof(CopyItem) == 32, "CopyItem layout");
+
+enum CopyMode { COPY_FETCH = 0, COPY_APPEND = 1, COPY_STORE = 2 };
+
+struct CopyArgs {
+  const CopyItem *items;
+  int32_t n_items;
+  int32_t mode;
+  int64_t row_bytes;      // bytes of one token row of K (or V) of one layer
+  int64_t layer_off;      // layer * slice_bytes
+  int64_t v_half_off;     // slice_bytes / 2: V half of a block slice
+  char *tier_base[2];     // device-visible bases of the device and host tiers
+  char *act_k;
+  char *act_v;
+  const char *new_k;
+  const char *new_v;
+};
+
+hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream);
+
+// ---------------------------------------------------------------------------
+// Attention work decomposition
+// ---------------------------------------------------------------------------
+struct SeqDesc {
+  int32_t cu_q;       // first query row of the sequence
+  int32_t cu_k;       // first active-buffer row of the sequence
+  int32_t prefix;     // P
+  int32_t n_new;      // N
+  int32_t n_splits;   // key splits of every query tile of this sequence
+  int32_t pad[3];
+};
+static_assert(sizeof(SeqDesc) == 32, "SeqDesc layout");
+
+// One workgroup: rows (query, head) = queries [q0, q0 + nq) of sequence `seq`
+// times the `group` query heads of KV head `kvh`; keys [k_begin, k_end).
+struct WorkItem {
+  int32_t seq;        // -1: padding slot, the workgroup exits
+  int32_t kvh;
+  int32_t q0;
+  int32_t nq;
+  int32_t k_begin;    // multiple of the key tile
+  int32_t k_end;
+  int32_t split;
+  int32_t pad;
+};
+static_assert(sizeof(WorkItem) == 32, "WorkItem layout");
+
+struct AttnArgs {
+  const uint16_t *q;
+  const uint16_t *k;
+  const uint16_t *v;
+  uint16_t *out;
+  float *lse;             // nullable, [Hq][total_q]
+  const WorkItem *items;
+  const SeqDesc *seqs;
+  float *part_o;          // [max_splits][total_q][Hq][D] fp32, normalised partial outputs
+  float *part_lse;        // [max_splits][total_q][Hq]
+  int32_t n_seqs;
+  int32_t total_q;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t group;
+  int32_t rows_q;         // queries per workgroup tile
+  float scale_log2;       // softmax scale * log2(e)
+};
+
+// Tile geometry the planner and the kernel agree on.
+constexpr int kAttnRows = 128;   // (query, head) rows per workgroup
+constexpr int kAttnKeyTile = 64; // keys per LDS tile
+
+hipError_t launch_attn_fwd(const AttnArgs &a, int head_dim, int n_items, hipStream_t stream);
+hipError_t launch_attn_merge(const AttnArgs &a, int head_dim, hipStream_t stream);
+
+struct AttnPlan {
+  int group = 0;
+  int rows_q = 0;
+  int max_splits = 1;
+  int n_items = 0;                 // grid size (includes padding slots)
+  int n_real_items = 0;
+  std::vector<WorkItem> items;
+  std::vector<SeqDesc> seqs;
+  WorkItem *d_items = nullptr;
+  SeqDesc *d_seqs = nullptr;
+  int64_t total_q = 0;
+};
+
+// Builds the work list for a batch (host only; no device work).
+void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N, int n_q_heads,
+                    int n_kv_heads, int target_items, AttnPlan *plan);
+int attn_target_items(int device);
+
+}  // namespace sc
+
+// ---------------------------------------------------------------------------
+// Opaque objects
+// ---------------------------------------------------------------------------
+struct sc_pool {
+  sc_pool_desc desc;
+  char *dev_base = nullptr;
+  char *host_base = nullptr;      // host address of the host tier
+  char *host_dev = nullptr;       // device-visible address of the host tier
+  bool own_dev = false;
+  bool own_host = false;
+  size_t slice_bytes = 0;
+  size_t block_bytes = 0;
+  size_t row_bytes = 0;
+};
+
+struct sc_table {
+  sc_pool *pool = nullptr;
+  int32_t batch = 0;
+  std::vector<int32_t> P, N;
+  std::vector<int64_t> cu_q, cu_k;
+  int64_t total_q = 0, total_kv = 0;
+  std::vector<sc::CopyItem> h_items; // host copy (source of the upload)
+  sc::CopyItem *d_items = nullptr;   // fetch items, then append, then store
+  int32_t n_fetch = 0, n_append = 0, n_store = 0;
+  std::mutex mu;
+  std::map<std::pair<int, int>, sc::AttnPlan> plans;   // keyed by (n_q_heads, n_kv_heads)
+};

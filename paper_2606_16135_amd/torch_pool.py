@@ -1,0 +1,86 @@
+"""Device memory for the library from torch: a donor pool over a caller-owned
+device tensor (HBM tier) and a pinned host tensor (host tier), its block
+table, and active-layer buffers.  torch provides memory and streams only;
+every step of the path runs in libswiftcache's kernels."""
+
+import numpy as np
+import torch
+
+
+def to_u16(t):
+    """bf16 tensor (any device) -> numpy uint16 bit patterns."""
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def from_u16(a, device):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device).view(torch.bfloat16)
+
+
+class DevicePool:
+    """A workload's pool in caller-owned memory: a device tensor for the HBM
+    tier and a pinned host tensor for the host tier."""
+
+    def __init__(self, sc, wl, pool_u16=None, fill="numpy"):
+        self.sc, self.wl = sc, wl
+        be = wl.block_elems
+        self.dev = torch.empty(max(1, wl.n_device_blocks) * be, dtype=torch.bfloat16, device="cuda")
+        self.host = None
+        if wl.n_host_blocks:
+            self.host = torch.empty(wl.n_host_blocks * be, dtype=torch.bfloat16).pin_memory()
+        if pool_u16 is not None:
+            flat = pool_u16.reshape(wl.n_blocks, be)
+            self.dev.view(torch.int16)[: wl.n_device_blocks * be].copy_(
+                torch.from_numpy(flat[: wl.n_device_blocks].reshape(-1).view(np.int16)))
+            if self.host is not None:
+                self.host.view(torch.int16).copy_(
+                    torch.from_numpy(flat[wl.n_device_blocks:].reshape(-1).view(np.int16)))
+        elif fill == "torch":
+            from paper_2606_16135_amd.workloads import fill_pool_torch
+            fill_pool_torch(wl, self.dev, self.host)
+        torch.cuda.synchronize()
+        self.handle = sc.sc_pool_create(wl.n_layers, wl.n_kv_heads, wl.head_dim, wl.block_size,
+                                        wl.n_device_blocks, wl.n_host_blocks, 0,
+                                        self.dev.data_ptr(),
+                                        self.host.data_ptr() if self.host is not None else 0)
+        self.table = sc.sc_table_create(self.handle, wl.block_ids, wl.cu_blocks, wl.prefix_len,
+                                        wl.new_len, torch.cuda.current_stream().cuda_stream)
+
+    def layer_slice_u16(self, layer):
+        """Layer `layer` of every pool block, as a 6-D uint16 array with a
+        single layer: [n_blocks][1][2][B][H_kv][D] (input for the oracle)."""
+        wl = self.wl
+        shp = (2, wl.block_size, wl.n_kv_heads, wl.head_dim)
+        parts = []
+        if wl.n_device_blocks:
+            d = self.dev.view(torch.int16)[: wl.n_device_blocks * wl.block_elems]
+            d = d.view(wl.n_device_blocks, wl.n_layers, *shp)[:, layer].cpu().numpy()
+            parts.append(d)
+        if wl.n_host_blocks:
+            h = self.host.view(torch.int16).view(wl.n_host_blocks, wl.n_layers, *shp)[:, layer].numpy()
+            parts.append(h.copy())
+        return np.concatenate(parts).view(np.uint16)[:, None]
+
+    def full_u16(self):
+        wl = self.wl
+        parts = []
+        if wl.n_device_blocks:
+            parts.append(self.dev.view(torch.int16)[: wl.n_device_blocks * wl.block_elems].cpu().numpy())
+        if wl.n_host_blocks:
+            parts.append(self.host.view(torch.int16).numpy().copy())
+        return np.concatenate(parts).view(np.uint16).reshape(wl.pool_shape())
+
+    def close(self):
+        self.sc.sc_table_destroy(self.table)
+        self.sc.sc_pool_destroy(self.handle)
+
+
+def new_active(sc, wl, fill_bits=0xFFFF, extra=0):
+    """K and V active-layer buffers of sum(P+N) (+ extra) rows, filled with
+    the 16-bit pattern `fill_bits`, and their sc_active descriptor."""
+    cap = wl.total_kv + extra
+    fill = int(np.uint16(fill_bits).view(np.int16))
+    k = torch.full((cap, wl.n_kv_heads, wl.head_dim), fill, dtype=torch.int16, device="cuda")
+    v = torch.full_like(k, fill)
+    k = k.view(torch.bfloat16)
+    v = v.view(torch.bfloat16)
+    return k, v, sc.active(k.data_ptr(), v.data_ptr(), cap)

@@ -1,0 +1,174 @@
+"""Host logic of the C ABI, on the CPU: the library loads and exports every
+declared symbol; argument validation; the attention work decomposition."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "swiftcache.h")
+
+
+@pytest.fixture(scope="module")
+def sc():
+    from paper_2606_16135_amd import swiftcache
+    swiftcache.load()
+    return swiftcache
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sc_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(sc):
+    lib = ctypes.CDLL(sc.LIB_PATH)
+    names = declared_functions()
+    assert len(names) >= 14
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(sc.EXPORTED) == names
+
+
+def test_version(sc):
+    assert "gfx950" in sc.sc_version()
+
+
+FAKE_BASE = 0x10000   # never dereferenced: every call below fails validation first
+
+
+def _pool(sc, n_blocks=8, layers=2, bs=4):
+    return sc.sc_pool_create(layers, 2, 64, bs, n_blocks, 0, 0, FAKE_BASE, 0)
+
+
+def test_pool_validation(sc):
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_pool_create(2, 2, 96, 16, 8, 0, 0, FAKE_BASE, 0)
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_pool_create(0, 2, 64, 16, 8, 0, 0, FAKE_BASE, 0)
+    assert e.value.status == sc.SC_ERR_INVALID
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_pool_create(2, 2, 64, 16, 0, 0, 0, FAKE_BASE, 0)
+    assert e.value.status == sc.SC_ERR_INVALID
+
+
+def test_pool_layout_follows_eq1(sc):
+    p = sc.sc_pool_create(3, 8, 128, 16, 5, 0, 0, FAKE_BASE, 0)
+    try:
+        lay = sc.sc_pool_layout_get(p)
+        assert lay.slice_bytes == 2 * 16 * 8 * 128 * 2 == 65536
+        assert lay.block_bytes == 3 * 65536
+        assert lay.row_bytes == 8 * 128 * 2
+        assert lay.device_base == FAKE_BASE
+    finally:
+        sc.sc_pool_destroy(p)
+
+
+@pytest.mark.parametrize("ids,cu,P,N,status", [
+    ([0, 1, 2], [0, 3], [9], [4], "INVALID"),       # 13 tokens need ceil(13/4) = 4 entries
+    ([0, 1], [0, 2], [9], [2], "INVALID"),          # too few entries
+    ([0, 1, 1], [0, 3], [9], [0], "INVALID"),       # duplicate id
+    ([0, 1, 8], [0, 3], [9], [0], "RANGE"),         # id outside the pool
+    ([0, 1, -1], [0, 3], [9], [0], "RANGE"),        # negative id
+    ([0, 1, 2], [0, 3], [-1], [10], "INVALID"),     # negative length
+    ([0, 1, 2], [1, 3], [9], [0], "INVALID"),       # cu_blocks[0] != 0
+])
+def test_table_validation(sc, ids, cu, P, N, status):
+    p = _pool(sc)
+    try:
+        with pytest.raises(sc.SwiftCacheError) as e:
+            sc.sc_table_create(p, ids, cu, P, N)
+        assert e.value.status == getattr(sc, "SC_ERR_" + status)
+    finally:
+        sc.sc_pool_destroy(p)
+
+
+def test_attention_argument_validation(sc):
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn(1, 1, 1, 4, 4, 12, 8, 128, 1)
+    assert e.value.status == sc.SC_ERR_INVALID
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn(1, 1, 1, 4, 4, 8, 8, 80, 1)
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn(1, 1, 1, 4, 4, 64, 2, 128, 1)     # group 32
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn(1, 1, 1, -1, 4, 8, 8, 128, 1)
+    assert e.value.status == sc.SC_ERR_INVALID
+    sc.sc_prefill_attn(0, 0, 0, 5, 0, 8, 8, 128, 0)          # new_len == 0 is a no-op
+
+
+KEY_TILE = 64
+ROWS = 128
+
+
+def _check_plan(sc, P, N, hq, hkv, target):
+    items, splits = sc.sc_attn_plan_query(P, N, hq, hkv, target)
+    group = hq // hkv
+    rows_q = ROWS // group
+    assert len(items) % 8 == 0
+    real = items[items[:, 0] >= 0]
+    # padding slots are only idle workgroups
+    assert np.all(items[items[:, 0] < 0][:, 1:] == 0)
+    # each (seq, kv head) group lives on one XCD
+    xcd_of = {}
+    for slot, it in enumerate(items):
+        if it[0] < 0:
+            continue
+        key = (int(it[0]), int(it[1]))
+        assert xcd_of.setdefault(key, slot % 8) == slot % 8
+    # per query tile, the splits partition [0, P + q0 + nq)
+    tiles = {}
+    for it in real:
+        seq, kvh, q0, nq, kb, ke, s, _ = (int(x) for x in it)
+        assert kb % KEY_TILE == 0 and ke >= kb
+        tiles.setdefault((seq, kvh, q0, nq), []).append((s, kb, ke))
+    expect = set()
+    for b, (p, n) in enumerate(zip(P, N)):
+        for g in range(hkv):
+            for q0 in range(0, n, rows_q):
+                expect.add((b, g, q0, min(rows_q, n - q0)))
+    assert set(tiles) == expect
+    for (seq, kvh, q0, nq), parts in tiles.items():
+        parts.sort()
+        assert [s for s, _, _ in parts] == list(range(splits[seq]))
+        pos = 0
+        for _, kb, ke in parts:
+            if ke > kb:
+                assert kb == pos
+                pos = ke
+        assert pos == P[seq] + q0 + nq
+    return items, splits
+
+
+@pytest.mark.parametrize("P,N,hq,hkv,target", [
+    ([8192], [512], 32, 8, 768),
+    ([32768], [1024], 40, 8, 768),
+    ([131072], [2048], 32, 8, 768),
+    ([256], [64], 8, 8, 768),
+    ([0], [130], 8, 8, 768),
+    ([5000], [40], 8, 2, 768),
+    ([33, 0, 1000, 17], [5, 64, 1, 200], 16, 4, 768),
+    ([7, 9], [0, 3], 8, 8, 4),
+])
+def test_plan_covers_every_row_and_key_once(sc, P, N, hq, hkv, target):
+    _check_plan(sc, P, N, hq, hkv, target)
+
+
+def test_plan_random_batches(sc):
+    rng = np.random.default_rng(0)
+    for _ in range(20):
+        b = int(rng.integers(1, 9))
+        P = rng.integers(0, 3000, size=b).tolist()
+        N = rng.integers(0, 300, size=b).tolist()
+        if sum(N) == 0:
+            N[0] = 1
+        hkv = int(rng.choice([1, 2, 8]))
+        group = int(rng.choice([1, 4, 5]))
+        _check_plan(sc, P, N, hkv * group, hkv, int(rng.integers(16, 2000)))
