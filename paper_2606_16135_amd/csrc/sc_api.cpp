@@ -60,34 +60,53 @@ namespace {
 constexpr int kXcds = 8;                 // MI355X: workgroup w is dispatched to XCD w % 8
 constexpr int kMinSplitKeys = 8 * kAttnKeyTile;
 constexpr int kMaxSplits = 16;
+constexpr int kResidentPerCu = 2;        // LDS- and VGPR-limited workgroups per CU
+constexpr int64_t kItemOverheadKeys = 2 * kAttnKeyTile;  // prologue + epilogue, in key-tile units
+constexpr int64_t kMergeOverheadKeys = kAttnKeyTile;     // partial write + merge-kernel share
+
+struct TileDesc {
+  int32_t seq, kvh, q0, nq, keys;
+};
+
+// Longest-processing-time schedule of `costs` on `slots` identical slots.
+int64_t lpt_makespan(std::vector<int64_t> &costs, int slots) {
+  std::sort(costs.begin(), costs.end(), std::greater<int64_t>());
+  std::vector<int64_t> heap(std::max(1, slots), 0);   // min-heap of slot loads
+  auto cmp = std::greater<int64_t>();
+  std::make_heap(heap.begin(), heap.end(), cmp);
+  for (int64_t c : costs) {
+    std::pop_heap(heap.begin(), heap.end(), cmp);
+    heap.back() += c;
+    std::push_heap(heap.begin(), heap.end(), cmp);
+  }
+  return *std::max_element(heap.begin(), heap.end());
+}
 }  // namespace
 
-int attn_target_items(int device) {
+int attn_slots(int device) {
   static std::mutex mu;
   static std::map<int, int> cache;
   std::lock_guard<std::mutex> lk(mu);
   auto it = cache.find(device);
   if (it != cache.end()) return it->second;
   int cus = 256;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) cus = 256;
-  // Two resident workgroups per CU (LDS-limited); ask for 1.5 rounds of them
-  // so that uneven items still balance.
-  int target = cus * 3;
-  if (const char *env = std::getenv("SC_ATTN_TARGET_ITEMS")) target = std::max(1, atoi(env));
-  cache[device] = target;
-  return target;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || cus <= 0)
+    cus = 256;
+  const int slots = cus * kResidentPerCu;
+  cache[device] = slots;
+  return slots;
 }
 
 void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N, int n_q_heads,
-                    int n_kv_heads, int target_items, AttnPlan *plan) {
+                    int n_kv_heads, int slots, AttnPlan *plan) {
   const int group = n_q_heads / n_kv_heads;
   const int rows_q = kAttnRows / group;
   const int batch = (int)P.size();
   plan->group = group;
   plan->rows_q = rows_q;
   plan->seqs.assign(batch, SeqDesc{});
-  int64_t n_tiles = 0;
-  int64_t cq = 0, ck = 0;
+  int64_t cq = 0, ck = 0, max_kv = 0;
+  std::vector<TileDesc> tiles;
   for (int b = 0; b < batch; ++b) {
     SeqDesc &s = plan->seqs[b];
     s.cu_q = (int32_t)cq;
@@ -97,47 +116,49 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
     s.n_splits = 1;
     cq += N[b];
     ck += (int64_t)P[b] + N[b];
-    n_tiles += (int64_t)((N[b] + rows_q - 1) / rows_q) * n_kv_heads;
+    max_kv = std::max<int64_t>(max_kv, (int64_t)P[b] + N[b]);
+    for (int g = 0; g < n_kv_heads; ++g)
+      for (int q0 = 0; q0 < N[b]; q0 += rows_q) {
+        const int nq = std::min(rows_q, N[b] - q0);
+        tiles.push_back(TileDesc{b, g, q0, nq, P[b] + q0 + nq});
+      }
   }
   plan->total_q = cq;
 
-  // Split-key chunk: the largest multiple of the key tile that still yields
-  // at least target_items workgroups, but never below kMinSplitKeys.
-  auto items_for = [&](int64_t chunk) {
-    int64_t tot = 0;
-    for (int b = 0; b < batch; ++b) {
-      const int64_t tiles = (int64_t)((N[b] + rows_q - 1) / rows_q) * n_kv_heads;
-      const int64_t kv = (int64_t)P[b] + N[b];
-      const int64_t s = std::min<int64_t>(kMaxSplits, std::max<int64_t>(1, (kv + chunk - 1) / chunk));
-      tot += tiles * s;
-    }
-    return tot;
+  // Key-split choice: every sequence is split into chunks of at most `chunk`
+  // keys; try the chunk sizes that give 1..kMaxSplits splits to the longest
+  // sequence and keep the one with the shortest simulated schedule.
+  auto splits_for = [&](int64_t chunk, int b) {
+    const int64_t kv = (int64_t)P[b] + N[b];
+    return (int)std::min<int64_t>(kMaxSplits, std::max<int64_t>(1, (kv + chunk - 1) / chunk));
   };
-  int64_t max_kv = 0;
-  for (int b = 0; b < batch; ++b) max_kv = std::max<int64_t>(max_kv, (int64_t)P[b] + N[b]);
-  int64_t chunk = std::max<int64_t>(kMinSplitKeys, ((max_kv + kAttnKeyTile - 1) / kAttnKeyTile) * kAttnKeyTile);
-  if (n_tiles > 0 && n_tiles < target_items) {
-    int64_t lo = kMinSplitKeys, hi = chunk;
-    // largest chunk (multiple of the tile) with items_for(chunk) >= target
-    if (items_for(lo) < target_items) {
-      chunk = lo;
-    } else {
-      while (hi - lo > kAttnKeyTile) {
-        int64_t mid = ((lo + hi) / 2 / kAttnKeyTile) * kAttnKeyTile;
-        if (mid <= lo) mid = lo + kAttnKeyTile;
-        if (items_for(mid) >= target_items) lo = mid; else hi = mid;
+  int64_t best_chunk = std::max<int64_t>(max_kv, 1), best_span = -1;
+  size_t best_items = 0;
+  for (int s = 1; s <= kMaxSplits && !tiles.empty(); ++s) {
+    int64_t chunk = (max_kv + s - 1) / s;
+    chunk = ((chunk + kAttnKeyTile - 1) / kAttnKeyTile) * kAttnKeyTile;
+    if (s > 1 && chunk < kMinSplitKeys) break;
+    std::vector<int64_t> costs;
+    for (const TileDesc &t : tiles) {
+      const int S = splits_for(chunk, t.seq);
+      const int64_t ntile = (t.keys + kAttnKeyTile - 1) / kAttnKeyTile;
+      for (int sp = 0; sp < S; ++sp) {
+        const int64_t span = ((sp + 1) * ntile / S - sp * ntile / S) * kAttnKeyTile;
+        costs.push_back(span + kItemOverheadKeys + (S > 1 ? kMergeOverheadKeys : 0));
       }
-      chunk = lo;
+    }
+    const size_t n = costs.size();
+    const int64_t span = lpt_makespan(costs, slots);
+    if (best_span < 0 || span < best_span || (span == best_span && n < best_items)) {
+      best_span = span;
+      best_chunk = chunk;
+      best_items = n;
     }
   }
   int max_splits = 1;
   for (int b = 0; b < batch; ++b) {
-    const int64_t kv = (int64_t)P[b] + N[b];
-    int s = 1;
-    if (n_tiles < target_items)
-      s = (int)std::min<int64_t>(kMaxSplits, std::max<int64_t>(1, (kv + chunk - 1) / chunk));
-    plan->seqs[b].n_splits = s;
-    max_splits = std::max(max_splits, s);
+    plan->seqs[b].n_splits = splits_for(best_chunk, b);
+    max_splits = std::max(max_splits, plan->seqs[b].n_splits);
   }
   plan->max_splits = max_splits;
 
@@ -148,27 +169,26 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
     std::vector<WorkItem> items;
   };
   std::vector<GroupItems> groups;
+  size_t ti = 0;
   for (int b = 0; b < batch; ++b) {
     const int S = plan->seqs[b].n_splits;
     for (int g = 0; g < n_kv_heads; ++g) {
       GroupItems gi;
-      for (int q0 = 0; q0 < N[b]; q0 += rows_q) {
-        const int nq = std::min(rows_q, N[b] - q0);
-        const int keys = P[b] + q0 + nq;
-        const int ntile = (keys + kAttnKeyTile - 1) / kAttnKeyTile;
+      for (; ti < tiles.size() && tiles[ti].seq == b && tiles[ti].kvh == g; ++ti) {
+        const TileDesc &t = tiles[ti];
+        const int ntile = (t.keys + kAttnKeyTile - 1) / kAttnKeyTile;
         for (int s = 0; s < S; ++s) {
           const int t0 = (int)((int64_t)s * ntile / S);
           const int t1 = (int)((int64_t)(s + 1) * ntile / S);
           WorkItem w{};
           w.seq = b;
           w.kvh = g;
-          w.q0 = q0;
-          w.nq = nq;
+          w.q0 = t.q0;
+          w.nq = t.nq;
           w.k_begin = t0 * kAttnKeyTile;
-          w.k_end = std::min(t1 * kAttnKeyTile, keys);
-          if (w.k_end < w.k_begin) w.k_end = w.k_begin;
+          w.k_end = std::max(w.k_begin, std::min(t1 * kAttnKeyTile, t.keys));
           w.split = s;
-          gi.cost += (w.k_end - w.k_begin) + kAttnKeyTile;
+          gi.cost += (w.k_end - w.k_begin) + kItemOverheadKeys;
           gi.items.push_back(w);
         }
       }
@@ -219,6 +239,7 @@ struct Workspace {
 std::mutex g_ws_mu;
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
 
+// Partial log-sum-exps and outputs of split-key attention.
 sc_status get_workspace(int device, hipStream_t stream, size_t bytes, void **out) {
   std::lock_guard<std::mutex> lk(g_ws_mu);
   Workspace &ws = g_ws[{device, stream}];
@@ -226,8 +247,7 @@ sc_status get_workspace(int device, hipStream_t stream, size_t bytes, void **out
     if (ws.ptr) {
       SC_HIP(hipStreamSynchronize(stream));
       SC_HIP(hipFree(ws.ptr));
-      ws.ptr = nullptr;
-      ws.bytes = 0;
+      ws = Workspace{};
     }
     SC_HIP(hipMalloc(&ws.ptr, bytes));
     ws.bytes = bytes;
@@ -273,7 +293,7 @@ sc_status single_plan(int device, int P, int N, int hq, int hkv, AttnPlan **out)
     g_single_plans.clear();
   }
   auto plan = std::make_unique<AttnPlan>();
-  plan_attention({P}, {N}, hq, hkv, attn_target_items(device), plan.get());
+  plan_attention({P}, {N}, hq, hkv, attn_slots(device), plan.get());
   sc_status st = upload_plan(plan.get());
   if (st != SC_OK) {
     free_plan(plan.get());
@@ -330,19 +350,20 @@ sc_status check_heads(int hq, int hkv, int head_dim) {
   return SC_OK;
 }
 
-sc_status table_plan(sc_table *t, int hq, AttnPlan **out) {
+sc_status table_plan(sc_table *t, int hq, AttnPlan **out, int slots = 0) {
   const sc_pool_desc &d = t->pool->desc;
   sc_status st = check_heads(hq, d.n_kv_heads, d.head_dim);
   if (st != SC_OK) return st;
+  if (slots <= 0) slots = attn_slots(d.device);
   std::lock_guard<std::mutex> lk(t->mu);
-  auto key = std::make_pair(hq, d.n_kv_heads);
+  auto key = std::make_pair(hq, slots);
   auto it = t->plans.find(key);
   if (it != t->plans.end()) {
     *out = &it->second;
     return SC_OK;
   }
   AttnPlan &plan = t->plans[key];
-  plan_attention(t->P, t->N, hq, d.n_kv_heads, attn_target_items(d.device), &plan);
+  plan_attention(t->P, t->N, hq, d.n_kv_heads, slots, &plan);
   st = upload_plan(&plan);
   if (st != SC_OK) {
     free_plan(&plan);
@@ -350,6 +371,50 @@ sc_status table_plan(sc_table *t, int hq, AttnPlan **out) {
     return st;
   }
   *out = &plan;
+  return SC_OK;
+}
+
+// ---------------------------------------------------------------------------
+// CU-partitioned streams for the layer pipeline when the fetch reads the
+// host tier.  Such a fetch takes as long as a layer's attention and its
+// workgroups wait on the host link for most of that time, so it must not
+// compete with attention for CU slots: the library keeps, per device, a copy
+// stream restricted to kHostFetchCus CUs and an attention stream restricted
+// to the others.  CU mask bit i selects logical CU i; logical CUs are
+// interleaved across the XCDs, so the low bits take the same number of CUs
+// from every XCD.
+// ---------------------------------------------------------------------------
+constexpr int kHostFetchCus = 16;
+
+struct SplitStreams {
+  hipStream_t attn = nullptr;
+  hipStream_t copy = nullptr;
+  int attn_cus = 0;
+};
+std::mutex g_split_mu;
+std::map<int, SplitStreams> g_split;
+
+sc_status split_streams(int device, SplitStreams **out) {
+  std::lock_guard<std::mutex> lk(g_split_mu);
+  auto it = g_split.find(device);
+  if (it != g_split.end()) {
+    *out = &it->second;
+    return SC_OK;
+  }
+  int cus = 0;
+  SC_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device));
+  if (cus <= 2 * kHostFetchCus) return fail(SC_ERR_UNSUPPORTED, "device has only %d CUs", cus);
+  const int words = (cus + 31) / 32;
+  std::vector<uint32_t> copy_mask(words, 0u), attn_mask(words, 0u);
+  for (int c = 0; c < cus; ++c) {
+    std::vector<uint32_t> &m = c < kHostFetchCus ? copy_mask : attn_mask;
+    m[c / 32] |= 1u << (c % 32);
+  }
+  SplitStreams ss;
+  SC_HIP(hipExtStreamCreateWithCUMask(&ss.attn, (uint32_t)words, attn_mask.data()));
+  SC_HIP(hipExtStreamCreateWithCUMask(&ss.copy, (uint32_t)words, copy_mask.data()));
+  ss.attn_cus = cus - kHostFetchCus;
+  *out = &(g_split[device] = ss);
   return SC_OK;
 }
 
@@ -593,6 +658,7 @@ sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids
     }
   }
   t->n_fetch = (int32_t)fetch.size();
+  for (const CopyItem &it : fetch) t->n_fetch_host += it.tier;
   t->n_append = (int32_t)append.size();
   t->n_store = (int32_t)store.size();
   std::vector<CopyItem> &all = t->h_items;
@@ -627,7 +693,7 @@ void sc_table_destroy(sc_table *table) {
 }
 
 sc_status sc_attn_plan_query(int32_t batch, const int32_t *prefix_len, const int32_t *new_len,
-                             int32_t n_q_heads, int32_t n_kv_heads, int32_t target_items, int32_t *n_items,
+                             int32_t n_q_heads, int32_t n_kv_heads, int32_t slots, int32_t *n_items,
                              int32_t *items, int32_t capacity, int32_t *splits) {
   clear_error();
   if (batch <= 0 || !prefix_len || !new_len || !n_items) return fail(SC_ERR_INVALID, "null argument");
@@ -638,7 +704,7 @@ sc_status sc_attn_plan_query(int32_t batch, const int32_t *prefix_len, const int
   AttnPlan plan;
   plan_attention(std::vector<int32_t>(prefix_len, prefix_len + batch),
                  std::vector<int32_t>(new_len, new_len + batch), n_q_heads, n_kv_heads,
-                 target_items > 0 ? target_items : 768, &plan);
+                 slots > 0 ? slots : 512, &plan);
   *n_items = plan.n_items;
   if (items) {
     if (capacity < plan.n_items) return fail(SC_ERR_RANGE, "capacity %d < %d items", capacity, plan.n_items);
@@ -756,12 +822,21 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
       return fail(SC_ERR_INVALID, "null per-layer pointer at layer %d", l);
   }
   DeviceGuard guard(pool->desc.device);
-  AttnPlan *plan = nullptr;
-  sc_status st = table_plan(const_cast<sc_table *>(table), n_q_heads, &plan);
-  if (st != SC_OK) return st;
   const sc_pool_desc &d = pool->desc;
-  hipStream_t cs = (hipStream_t)compute_stream;
-  hipStream_t xs = (hipStream_t)copy_stream;
+  // A fetch that reaches into the host tier runs on CU-partitioned streams
+  // (see split_streams); the caller's streams then only order the work.
+  SplitStreams *ss = nullptr;
+  if (mode == SC_STACK_OVERLAP && table->n_fetch_host > 0) {
+    sc_status st = split_streams(d.device, &ss);
+    if (st != SC_OK) return st;
+  }
+  AttnPlan *plan = nullptr;
+  sc_status st = table_plan(const_cast<sc_table *>(table), n_q_heads, &plan,
+                            ss ? ss->attn_cus * kResidentPerCu : 0);
+  if (st != SC_OK) return st;
+  hipStream_t caller_cs = (hipStream_t)compute_stream;
+  hipStream_t cs = ss ? ss->attn : caller_cs;
+  hipStream_t xs = ss ? ss->copy : (hipStream_t)copy_stream;
   auto attn = [&](int l, const sc_active &slot) {
     return run_attention(d.device, *plan, q_per_layer[l], slot.k, slot.v, out_per_layer[l], nullptr, n_q_heads,
                          d.n_kv_heads, d.head_dim, scale, cs);
@@ -785,7 +860,7 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
   }
 
   // Overlapped: events ready[s] (slot s filled) and free_[s] (slot s read).
-  hipEvent_t ev[5] = {};
+  hipEvent_t ev[6] = {};
   for (auto &e : ev) {
     hipError_t he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
     if (he != hipSuccess) {
@@ -794,11 +869,13 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
       return fail_hip(he, "hipEventCreate");
     }
   }
-  hipEvent_t *ready = ev, *free_ = ev + 2, start = ev[4];
+  hipEvent_t *ready = ev, *free_ = ev + 2, start = ev[4], done = ev[5];
   auto body = [&]() -> sc_status {
-    // The copy stream starts after everything already queued on `compute`.
-    SC_HIP(hipEventRecord(start, cs));
+    // Both streams start after everything already queued on the caller's
+    // compute stream.
+    SC_HIP(hipEventRecord(start, caller_cs));
     SC_HIP(hipStreamWaitEvent(xs, start, 0));
+    if (cs != caller_cs) SC_HIP(hipStreamWaitEvent(cs, start, 0));
     for (int l = 0; l < n_layers; ++l) {
       const int s = l & 1;
       if (l >= 2) SC_HIP(hipStreamWaitEvent(xs, free_[s], 0));
@@ -811,9 +888,13 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
       if ((r = attn(l, slots[s])) != SC_OK) return r;
       SC_HIP(hipEventRecord(free_[s], cs));
     }
-    // The compute stream ends after the last store.
+    // The caller's compute stream ends after the last attention and store.
     SC_HIP(hipEventRecord(start, xs));
-    SC_HIP(hipStreamWaitEvent(cs, start, 0));
+    SC_HIP(hipStreamWaitEvent(caller_cs, start, 0));
+    if (cs != caller_cs) {
+      SC_HIP(hipEventRecord(done, cs));
+      SC_HIP(hipStreamWaitEvent(caller_cs, done, 0));
+    }
     return SC_OK;
   };
   st = body();

@@ -130,9 +130,10 @@ struct AttnPlan {
 };
 
 // Builds the work list for a batch (host only; no device work).
+// `slots` = workgroups the device runs at once (CUs x resident workgroups).
 void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N, int n_q_heads,
-                    int n_kv_heads, int target_items, AttnPlan *plan);
-int attn_target_items(int device);
+                    int n_kv_heads, int slots, AttnPlan *plan);
+int attn_slots(int device);
 
 }  // namespace sc
 
@@ -160,6 +161,7 @@ struct sc_table {
   std::vector<sc::CopyItem> h_items; // host copy (source of the upload)
   sc::CopyItem *d_items = nullptr;   // fetch items, then append, then store
   int32_t n_fetch = 0, n_append = 0, n_store = 0;
+  int32_t n_fetch_host = 0;          // fetch items that read the host tier
   std::mutex mu;
-  std::map<std::pair<int, int>, sc::AttnPlan> plans;   // keyed by (n_q_heads, n_kv_heads)
+  std::map<std::pair<int, int>, sc::AttnPlan> plans;   // keyed by (n_q_heads, slots)
 };
