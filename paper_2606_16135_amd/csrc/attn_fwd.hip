@@ -6,35 +6,51 @@
 //   o = sum_{j <= P + i} softmax_j(scale * q . k_j) v_j,  KV head g = h / group.
 //
 // Work decomposition (built on the host, see plan_attention): a workgroup
-// owns 128 (query, head) rows = rows_q consecutive queries times the `group`
-// query heads that share one KV head, and a range of keys.  Packing the
-// heads of a group into the rows makes every K/V tile that is staged through
-// LDS serve all of them.  Long key ranges are split over several workgroups
-// (split-key): each writes a normalised fp32 partial output and its
-// log-sum-exp, and attn_merge_kernel combines them exactly
+// of 8 waves owns 256 (query, head) rows = rows_q consecutive queries times
+// the `group` query heads that share one KV head, and a range of keys.
+// Packing the heads of a group into the rows makes every K/V tile staged
+// through LDS serve all of them.  Long key ranges are split over several
+// workgroups (split-key): each writes a normalised fp32 partial output and
+// its log-sum-exp, and attn_merge_kernel combines them exactly
 // (o = sum_s exp(lse_s - lse) o_s).  The merge is a separate launch: merging
 // in the last-arriving workgroup would need device-scope fences, whose L2
 // write-back / invalidate stalls the other workgroups streaming K/V.
 //
-// Per workgroup: 4 waves, each owning 32 rows.  Keys are walked in tiles of
-// 64 that are double-buffered in LDS: the next tile's global loads are in
-// flight while the current tile is consumed.  Per tile and wave:
-//   S^T (32 keys x 32 rows) += K_tile . Q^T    MFMA 32x32x16 bf16, K-dim = D
-//   online softmax on S^T: every lane holds 16 keys of ONE row per 32-key
-//     block, so the row max needs one exchange between the two 32-lane
-//     halves of the wave; exp2 with scale * log2(e) folded in
-//   O^T (D x 32 rows) += V^T . P^T            MFMA 32x32x16 bf16, K-dim = keys
-// The probabilities never leave registers: the S^T accumulator layout is the
-// B-operand layout of the PV product once rounded to bf16, for a fixed
-// permutation of the 16 keys of each MFMA step.  V^T operands come from the
-// row-major V tile through LDS transpose reads (ds_read_b64_tr_b16): in each
-// 16-lane group, lanes 4r..4r+3 read 4 dims each of key r and lane j gets
-// dim j of the 4 keys.
+// Per key tile of 32 and per wave (32 rows):
+//   S^T (32 keys x 32 rows) = K_tile . Q^T         MFMA 32x32x16 bf16, fp32 out
+//   P = exp2(c S^T - m),  c = scale * log2(e)      online softmax, log2 domain
+//   O^T (D x 32 rows) += V^T . P^T                 MFMA 32x32x16 bf16
+// The scale stays in fp32: folding it into a bf16 copy of q moves scores by
+// about 1% of q's rounding, enough to exceed the tolerance when two keys
+// compete for a row.  Every lane holds 16 keys of ONE row (the other 16 are
+// in the other half of the wave).  The probabilities never leave registers:
+// the S^T accumulator layout is the B-operand layout of the PV product once
+// rounded to bf16, for a fixed permutation of the 16 keys of each MFMA step.
+// V^T operands come from the row-major V tile through LDS transpose reads
+// (ds_read_b64_tr_b16: in each 16-lane group, lanes 4r..4r+3 read 4 dims
+// each of key r and lane j gets dim j of the 4 keys).  Row sums use
+// v_dot2c_f32_bf16 on the packed bf16 probabilities, i.e. the same rounded
+// values the PV product consumes.
 //
-// The running max is only moved (and O, l rescaled) when a row's tile max
-// exceeds it by more than kRescaleSlack (log2 units); otherwise the
-// exponentials stay below 2^kRescaleSlack.  The result is the same softmax,
-// with fewer rescale passes over the accumulators.
+// Software pipeline.  A single wave issues MFMAs at half the SIMD's matrix
+// rate and VALU ops at half its vector rate, so each wave interleaves both:
+// iteration j issues QK(j+1) and PV(j-1) (16 MFMAs) in the same basic block
+// as the softmax of tile j, and both waves of a SIMD do so.  With head_dim
+// 128 one exponential per score already costs as much SIMD time as the two
+// MFMA products, so the softmax is cut to its minimum: p = exp2(c s - m),
+// the bf16 packing and the row sum.  The reference max m is the exact max
+// of the first tile and moves only when a lane's tile sum exceeds
+// kSumLimit: softmax is invariant to the reference, and fp32/bf16 keep their
+// relative precision at any scale, so a stale reference changes nothing but
+// the exponent range, which the limit bounds.  No per-tile row max is
+// computed on the common path.
+//
+// K and V tiles each live in a 2-entry LDS ring (slot = tile parity).
+// Iteration j reads K(j+1) and V(j-1), writes K(j+2) and V(j) from registers
+// loaded in iteration j-1, loads K(j+3) and V(j+1), and ends with one
+// workgroup barrier that orders LDS only (global loads stay in flight
+// across it).  The loop is unrolled by two so that slots and score
+// registers are fixed at compile time.
 #include "sc_internal.h"
 
 #include <cmath>
@@ -44,6 +60,7 @@ namespace sc {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -52,11 +69,14 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;            // 8 waves, 2 per SIMD
 constexpr int KT = kAttnKeyTile;
-constexpr float kRescaleSlack = 8.0f;
-static_assert(kAttnRows == 4 * 32, "four waves of 32 rows");
-static_assert(KT == 64, "two 32-key MFMA blocks per tile");
+// A lane's tile sum above this sends the wave through settle_max.  Every
+// probability is then below 2^20, so O and l stay far from fp32 overflow
+// for any sequence length; rows never pay for a max they do not need.
+constexpr float kSumLimit = 1048576.0f;
+static_assert(kAttnRows == 8 * 32, "eight waves of 32 rows");
+static_assert(KT == 32, "one 32-key MFMA block per tile");
 
 // 32x32 MFMA accumulator layout: element r of lane l holds C[m][n] with
 // n = l % 32 and m = 8 * (r / 4) + 4 * (l / 32) + r % 4.
@@ -64,8 +84,9 @@ __device__ __forceinline__ int acc_m(int r, int half) { return 8 * (r >> 2) + 4 
 
 template <int D>
 struct Geo {
-  static constexpr int kChunksPerRow = D / 8;                        // 16-byte chunks per key row
-  static constexpr int kChunksPerThread = KT * kChunksPerRow / kThreads;
+  static constexpr int kChunksPerRow = D / 8;                     // 16-byte chunks per key row
+  static constexpr int kTileChunks = KT * kChunksPerRow;          // chunks of K (or V) per tile
+  static constexpr int kChunksPerThread = 2 * kTileChunks / kThreads;  // K and V of one tile over the workgroup
   // K rows: 16-byte reads of 16 consecutive keys fall on disjoint banks.
   static constexpr int kLdsK = D + 8;
   // V rows: the 8 rows of one transpose read (64 bytes each) fall on
@@ -73,13 +94,11 @@ struct Geo {
   static constexpr int kLdsV = D + 32;
   static constexpr int kTileK = KT * kLdsK;
   static constexpr int kTileV = KT * kLdsV;
-  static constexpr int kBuf = kTileK + kTileV;
-  static_assert(kChunksPerThread * kThreads == KT * kChunksPerRow, "tile split");
+  static constexpr int kSmem = 2 * kTileK + 2 * kTileV;
+  static_assert(kChunksPerThread * kThreads == 2 * kTileChunks, "tile split");
 };
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
-
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 // Two floats to packed bf16 (round to nearest even), one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
@@ -87,228 +106,308 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, p);
 }
 
-// Value of the same lane in the other 32-lane half of the wave.
+// Sum of the two bf16 halves of `p` added to `acc` (v_dot2c_f32_bf16 with 1, 1).
+__device__ __forceinline__ float add_pair(uint32_t p, float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p), one, acc, false);
+}
+
+// Max with the same lane of the other 32-lane half of the wave.
 __device__ __forceinline__ float max_with_other_half(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, x),
                                                   __builtin_bit_cast(uint32_t, x), false, false);
   return fmaxf(__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1]));
 }
 
-// One 64-key tile for one wave: S^T, (mask), online softmax, O^T += V^T P^T.
-template <int D, bool MASK>
-__device__ __forceinline__ void attend_tile(const uint16_t *smem_buf, const bf16x8 (&qf)[D / 16],
-                                            f32x16 (&oacc)[D / 32], float &m_run, float &l_run, int lane,
-                                            float scale_log2, int kt, int k_end, int my_last) {
+// Workgroup barrier that orders LDS only: this wave's LDS accesses complete
+// before it, global loads stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// S^T(tile) = K_tile . Q^T: D / 16 dependent MFMAs.
+template <int D>
+__device__ __forceinline__ void qk_tile(const uint16_t *sk, const bf16x8 (&qf)[D / 16], f32x16 &s, int lane) {
   using G_ = Geo<D>;
-  const int half = lane >> 5;
-  const int col = lane & 31;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) s[r] = 0.f;
+  const uint16_t *krow = sk + (lane & 31) * G_::kLdsK + 8 * (lane >> 5);
+#pragma unroll
+  for (int k = 0; k < D / 16; ++k)
+    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(*reinterpret_cast<const u32x4 *>(krow + 16 * k)),
+                                                qf[k], s, 0, 0, 0);
+}
 
-  // Two independent accumulation chains (the two 32-key blocks), interleaved.
-  f32x16 sacc[2];
+// O^T += V^T . P^T.  MFMA step t covers keys 16 t + [0, 16); k-slot e of a
+// lane in half `half` holds key 16 t + 4 half + (e < 4 ? e : e + 4), which
+// is accumulator element 8 t + e of S^T, i.e. pf[t] element e.
+template <int D>
+__device__ __forceinline__ void pv_tile(const uint16_t *sv, const u32x4 (&pf)[2], f32x16 (&oacc)[D / 32],
+                                        int lane) {
+  using G_ = Geo<D>;
+  constexpr int NC = D / 32;
+  const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int tr_dim = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const uint16_t *vb = sv + tr_row * G_::kLdsV + tr_dim;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
-  const uint16_t *krow = smem_buf + col * G_::kLdsK + 8 * half;
-#pragma unroll
-  for (int s = 0; s < D / 16; ++s)
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4 *>(krow + 32 * kb * G_::kLdsK + 16 * s));
-      sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[kb], 0, 0, 0);
+    for (int c = 0; c < NC; ++c) {
+      const uint16_t *p = vb + 16 * t * G_::kLdsV + 32 * c;
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)p);
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p + 8 * G_::kLdsV));
+      u32x4 vw;
+      vw[0] = __builtin_bit_cast(u32x2, lo)[0];
+      vw[1] = __builtin_bit_cast(u32x2, lo)[1];
+      vw[2] = __builtin_bit_cast(u32x2, hi)[0];
+      vw[3] = __builtin_bit_cast(u32x2, hi)[1];
+      oacc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vw), as_bf16x8(pf[t]), oacc[c], 0, 0, 0);
     }
+}
 
-  if (MASK) {
-    // Element (kb, r) holds key kt + 32 kb + acc_m(r, half); it is visible
-    // when that offset is <= lim (the last visible key of this row in the
-    // range, relative to kt), i.e. when 32 kb + acc_m(r, 0) <= lim - 4 half.
-    const int lim = min(k_end - 1, my_last) - kt - 4 * half;
+// Masks keys past a row's last visible key: element r holds key offset
+// acc_m(r, half) within the tile, and lim is the row's last visible offset
+// minus 4 half.
+__device__ __forceinline__ void apply_mask(f32x16 &s, int lim) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        if (32 * kb + acc_m(r, 0) > lim) sacc[kb][r] = -INFINITY;
-  }
+  for (int r = 0; r < 16; ++r)
+    if (acc_m(r, 0) > lim) s[r] = -INFINITY;
+}
 
-  // Row max over this lane's 32 scores: four independent chains.
+// Row max of sl2 * s over the tile's 32 keys (both wave halves); -inf when
+// every key of the row is masked.
+__device__ __forceinline__ float tile_max(const f32x16 &s, float sl2) {
   float m4[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) m4[i] = fmaxf(sacc[i >> 1][8 * (i & 1)], sacc[i >> 1][8 * (i & 1) + 1]);
-#pragma unroll
-  for (int r = 2; r < 8; ++r)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) m4[i] = fmaxf(m4[i], sacc[i >> 1][8 * (i & 1) + r]);
-  float mx = fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]));
-  mx = max_with_other_half(mx);
-  const float tmax = mx * scale_log2;
-  const bool need = tmax > m_run + kRescaleSlack;
-  if (__ballot(need)) {
-    const float m_new = need ? tmax : m_run;
-    const float corr = __builtin_amdgcn_exp2f(m_run - m_new);
-    l_run *= corr;
-#pragma unroll
-    for (int c = 0; c < D / 32; ++c)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[c][r] *= corr;
-    m_run = m_new;
-  }
-  const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-  // Exponentials, summed in four independent chains.
-  float rs4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float p = __builtin_amdgcn_exp2f(sacc[kb][r] * scale_log2 - m_use);
-      sacc[kb][r] = p;
-      rs4[(kb << 1) | (r >> 3)] += p;
-    }
-  l_run += (rs4[0] + rs4[1]) + (rs4[2] + rs4[3]);
+  for (int i = 0; i < 4; ++i) m4[i] = fmaxf(fmaxf(s[4 * i], s[4 * i + 1]), fmaxf(s[4 * i + 2], s[4 * i + 3]));
+  return max_with_other_half(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]))) * sl2;
+}
 
-  // O^T += V^T . P^T.  MFMA step (kb, t) covers keys 32 kb + 16 t + [0, 16);
-  // k-slot e of a lane in half `half` holds key 32 kb + 16 t + 4 half +
-  // (e < 4 ? e : e + 4), matching accumulator elements 8 t + e.
-  const uint16_t *sv = smem_buf + G_::kTileK;
-  const int grp = lane >> 4;                  // 16-lane group: half = grp / 2
-  const int tr_row = (lane & 15) >> 2;        // key within the transpose read
-  const int tr_dim = 16 * (grp & 1) + 4 * (lane & 3);
+// p = exp2(sl2 * s - m) for this lane's 16 keys, packed to bf16, and the sum
+// of the packed values (the weights the PV product uses).
+__device__ __forceinline__ float softmax_tile(const f32x16 &s, u32x4 (&pf)[2], float sl2, float m) {
+  float r2[2] = {0.f, 0.f};
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
+  for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      u32x4 pw;
-      pw[0] = pack_bf16(sacc[kb][8 * t + 0], sacc[kb][8 * t + 1]);
-      pw[1] = pack_bf16(sacc[kb][8 * t + 2], sacc[kb][8 * t + 3]);
-      pw[2] = pack_bf16(sacc[kb][8 * t + 4], sacc[kb][8 * t + 5]);
-      pw[3] = pack_bf16(sacc[kb][8 * t + 6], sacc[kb][8 * t + 7]);
-      const bf16x8 pf = as_bf16x8(pw);
-      const int key_lo = 32 * kb + 16 * t + 4 * half + tr_row;
-#pragma unroll
-      for (int c = 0; c < D / 32; ++c) {
-        const int off = key_lo * G_::kLdsV + 32 * c + tr_dim;
-        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(sv + off));
-        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(sv + off + 8 * G_::kLdsV));
-        u32x4 vw;
-        vw[0] = __builtin_bit_cast(u32x2, lo)[0];
-        vw[1] = __builtin_bit_cast(u32x2, lo)[1];
-        vw[2] = __builtin_bit_cast(u32x2, hi)[0];
-        vw[3] = __builtin_bit_cast(u32x2, hi)[1];
-        oacc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vw), pf, oacc[c], 0, 0, 0);
-      }
+    for (int e = 0; e < 8; e += 2) {
+      const uint32_t w = pack_bf16(__builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * t + e], sl2, -m)),
+                                   __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * t + e + 1], sl2, -m)));
+      pf[t][e >> 1] = w;
+      r2[t] = add_pair(w, r2[t]);
     }
+  return r2[0] + r2[1];
+}
+
+template <int D>
+struct WaveState {
+  bf16x8 qf[D / 16];
+  f32x16 oacc[D / 32];
+  f32x16 s[2];        // raw scores of the even / odd tiles
+  u32x4 pf_prev[2];   // P(j-1) for the PV product
+  float m_run;        // reference max of sl2 * s, log2 units (0 until a key is visible)
+  float l_run;        // this lane's share of the denominator
+};
+
+// Rare path, taken by a whole wave when some lane's tile sum left the safe
+// range: move every row's reference max to the true running max, rescale l
+// and O (O already holds PV(j-1), computed against the old reference), and
+// redo the tile's exponentials.  Returns the new tile sum.
+template <int D>
+__device__ __forceinline__ float settle_max(WaveState<D> &w, const f32x16 &s, u32x4 (&pf)[2], float sl2) {
+  const float m_new = fmaxf(w.m_run, tile_max(s, sl2));
+  const float corr = __builtin_amdgcn_exp2f(w.m_run - m_new);
+  w.m_run = m_new;
+  w.l_run *= corr;
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) w.oacc[c][r] *= corr;
+  return softmax_tile(s, pf, sl2, m_new);
 }
 
 template <int D>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   using G_ = Geo<D>;
   constexpr int NCH = G_::kChunksPerThread;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * G_::kBuf];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[G_::kSmem];
 
-  const WorkItem w = a.items[blockIdx.x];
-  if (w.seq < 0) return;
-  const SeqDesc sd = a.seqs[w.seq];
+  const WorkItem wi = a.items[blockIdx.x];
+  if (wi.seq < 0) return;
+  const SeqDesc sd = a.seqs[wi.seq];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5;
   const int col = lane & 31;
   const int group = a.group;
   const int row = wave * 32 + col;
   const int qi = row / group;
   const int hg = row - qi * group;
-  const bool valid = qi < w.nq;
-  const int qpos = w.q0 + (valid ? qi : w.nq - 1);
-  const int h = w.kvh * group + hg;
+  const bool valid = qi < wi.nq;
+  const int qpos = wi.q0 + (valid ? qi : wi.nq - 1);
+  const int h = wi.kvh * group + hg;
   const int64_t qrow = (int64_t)(sd.cu_q + qpos) * a.n_q_heads + h;
 
-  // Q^T fragments (B operand): lane holds Q[row][16 s + 8 half .. + 7].
-  bf16x8 qf[D / 16];
+  WaveState<D> w;
+  // Q^T fragments (B operand): lane holds Q[row][16 k + 8 half .. + 7].
   {
     const u32x4 *qp = reinterpret_cast<const u32x4 *>(a.q + qrow * D);
 #pragma unroll
-    for (int s = 0; s < D / 16; ++s) {
+    for (int k = 0; k < D / 16; ++k) {
       u32x4 x = {0u, 0u, 0u, 0u};
-      if (valid) x = qp[2 * s + half];
-      qf[s] = as_bf16x8(x);
+      if (valid) x = qp[2 * k + half];
+      w.qf[k] = as_bf16x8(x);
     }
   }
-
-  const int64_t kv_stride = (int64_t)a.n_kv_heads * D;
-  const uint16_t *kbase = a.k + (int64_t)sd.cu_k * kv_stride + (int64_t)w.kvh * D;
-  const uint16_t *vbase = a.v + (int64_t)sd.cu_k * kv_stride + (int64_t)w.kvh * D;
-  const int diag_all = sd.prefix + w.q0;   // keys <= diag_all are visible to every row
-  const int my_last = sd.prefix + qpos;    // this row sees keys <= my_last
-  const int k_end = w.k_end;
-
-  u32x4 kr[NCH], vr[NCH];
-  // Rows at or past k_end are loaded from row k_end - 1 (valid memory) and
-  // masked; only the last tile of the range has such rows.
-  auto load_tile = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int c = tid + kThreads * i;
-      const int key = min(kt + c / G_::kChunksPerRow, k_end - 1);
-      const int cc = c % G_::kChunksPerRow;
-      kr[i] = *reinterpret_cast<const u32x4 *>(kbase + key * kv_stride + cc * 8);
-      vr[i] = *reinterpret_cast<const u32x4 *>(vbase + key * kv_stride + cc * 8);
-    }
-  };
-  auto store_tile = [&](int buf) {
-    uint16_t *sk = smem + buf * G_::kBuf;
-    uint16_t *sv = sk + G_::kTileK;
-#pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int c = tid + kThreads * i;
-      const int r = c / G_::kChunksPerRow;
-      const int cc = c % G_::kChunksPerRow;
-      *reinterpret_cast<u32x4 *>(sk + r * G_::kLdsK + cc * 8) = kr[i];
-      *reinterpret_cast<u32x4 *>(sv + r * G_::kLdsV + cc * 8) = vr[i];
-    }
-  };
-
-  float m_run = -INFINITY;  // reference max of scaled scores, log2 units
-  float l_run = 0.f;        // this lane's share of the denominator
-  f32x16 oacc[D / 32];
+  const float sl2 = a.scale_log2;   // scale * log2(e)
 #pragma unroll
   for (int c = 0; c < D / 32; ++c)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[c][r] = 0.f;
+    for (int r = 0; r < 16; ++r) w.oacc[c][r] = 0.f;
+  w.m_run = 0.f;
+  w.l_run = 0.f;
 
-  if (w.k_begin < k_end) {
-    load_tile(w.k_begin);
-    store_tile(0);
-    __syncthreads();
-    int buf = 0;
-    int kt = w.k_begin;
-    // Tiles before kt_mask lie wholly inside the range and at or below every
-    // row's diagonal; the rest need the mask.  One loop per kind keeps a
-    // single tile body live at a time.
-    const int kt_full = w.k_begin + ((min(k_end, diag_all + 1) - w.k_begin) / KT) * KT;
-    const int kt_mask = max(w.k_begin, kt_full);
-    auto run = [&](auto mask_tag, int stop) {
-      constexpr bool kMask = decltype(mask_tag)::value;
-      for (; kt < stop; kt += KT) {
-        const bool has_next = kt + KT < k_end;
-        if (has_next) load_tile(kt + KT);
-        attend_tile<D, kMask>(smem + buf * G_::kBuf, qf, oacc, m_run, l_run, lane, a.scale_log2, kt, k_end,
-                              my_last);
-        if (has_next) store_tile(buf ^ 1);
-        __syncthreads();
-        buf ^= 1;
+  // This item's keys [k_begin, k_end) of KV head kvh: rows of kv_stride
+  // elements, D of them used.  Tile t is read through a buffer resource that
+  // starts at its first row and ends after the item's last row, so rows past
+  // the range (the ragged last tile, tiles past the end) read as zero
+  // without touching memory outside it; those keys are masked.
+  const int64_t kv_stride = (int64_t)a.n_kv_heads * D;
+  const int k_begin = wi.k_begin;
+  const int k_end = wi.k_end;
+  const int n = (k_end - k_begin + KT - 1) / KT;
+  const int64_t first_row = ((int64_t)sd.cu_k + k_begin) * kv_stride + (int64_t)wi.kvh * D;
+  const uint16_t *const kb = a.k + first_row;
+  const uint16_t *const vb = a.v + first_row;
+  // Byte counts fit in 31 bits (checked on the host).
+  const uint32_t range_bytes = (uint32_t)((((int64_t)(k_end - k_begin) - 1) * kv_stride + D) * 2);
+  const uint32_t tile_bytes = (uint32_t)(KT * kv_stride * 2);
+  auto rsrc = [&](const uint16_t *base, int t) {
+    const uint32_t off = (uint32_t)t * tile_bytes;
+    return __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char *>(reinterpret_cast<const char *>(base) + off), (short)0,
+        (int)(range_bytes > off ? range_bytes - off : 0u), 0x00020000);
+  };
+
+  // Staging: chunk c = tid + 512 i of a (K tile, V tile) pair; whether it is
+  // a K or a V chunk is uniform over a wave.
+  int voff[NCH], lds_off[NCH];
+  bool is_v[NCH];
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) {
+    is_v[i] = wave * 64 + kThreads * i >= G_::kTileChunks;
+    const int c = tid + kThreads * i - (is_v[i] ? G_::kTileChunks : 0);
+    const int r = c / G_::kChunksPerRow, cc = c % G_::kChunksPerRow;
+    voff[i] = (int)((r * kv_stride + cc * 8) * 2);
+    lds_off[i] = is_v[i] ? 2 * G_::kTileK + r * G_::kLdsV + cc * 8 : r * G_::kLdsK + cc * 8;
+  }
+  // A negative tile index (prologue only) skips that half of the pair.
+  u32x4 lr[NCH];
+  auto stage_load = [&](int kj, int vj) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int t = is_v[i] ? vj : kj;
+      if (t >= 0)
+        lr[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc(is_v[i] ? vb : kb, t),
+                                                                                 voff[i], 0, 0));
+    }
+  };
+  // par_k / par_v: ring slots (tile parity) the K and V chunks go to.
+  auto stage_store = [&](bool k_on, bool v_on, int par_k, int par_v) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      if (is_v[i] ? v_on : k_on) {
+        const int slot_off = is_v[i] ? par_v * G_::kTileV : par_k * G_::kTileK;
+        *reinterpret_cast<u32x4 *>(smem + lds_off[i] + slot_off) = lr[i];
       }
+    }
+  };
+  auto slot_k = [&](int par) { return smem + par * G_::kTileK; };
+  auto slot_v = [&](int par) { return smem + 2 * G_::kTileK + par * G_::kTileV; };
+
+  // First tile that needs the mask, the same for the whole workgroup: it
+  // reaches past the key range or past the diagonal of the first query.
+  const int diag0 = sd.prefix + wi.q0;
+  const int j_mask = max(0, min(n, (min(k_end, diag0 + 1) - k_begin) / KT));
+  const int my_last = min(k_end - 1, sd.prefix + qpos);
+  auto lim_of = [&](int j) { return my_last - (k_begin + j * KT) - 4 * half; };
+
+  if (n > 0) {
+    // Prologue: K(0) into the ring, then QK(0); K(1) goes in and K(2), V(0)
+    // are loaded for iteration 0.
+    stage_load(0, -1);
+    stage_store(true, false, 0, 0);
+    stage_load(1, -1);
+    lds_barrier();
+    qk_tile<D>(slot_k(0), w.qf, w.s[0], lane);
+    stage_store(true, false, 1, 0);
+    stage_load(2, 0);
+    lds_barrier();
+
+    // Iteration j (tile parity PAR): QK(j+1) and PV(j-1) on the MFMA pipe,
+    // softmax(j) on the VALU, then K(j+2), V(j) into the ring and K(j+3),
+    // V(j+1) from memory.  Tile j's scores live in s[PAR].
+    auto iterate = [&](auto par_tag, auto mask_tag, auto qk_tag, auto pv_tag, auto first_tag, int j) {
+      constexpr int PAR = decltype(par_tag)::value;
+      constexpr bool kMask = decltype(mask_tag)::value;
+      constexpr bool kQk = decltype(qk_tag)::value;
+      constexpr bool kPv = decltype(pv_tag)::value;
+      constexpr bool kFirst = decltype(first_tag)::value;
+      __builtin_assume(j >= 0);
+      f32x16 &sc = w.s[PAR];
+      u32x4 pf[2];
+      if (kQk) qk_tile<D>(slot_k(PAR ^ 1), w.qf, w.s[PAR ^ 1], lane);
+      if (kPv) pv_tile<D>(slot_v(PAR ^ 1), w.pf_prev, w.oacc, lane);
+      if (kMask) apply_mask(sc, lim_of(j));
+      if (kFirst) {
+        const float tm = tile_max(sc, sl2);
+        w.m_run = tm > -INFINITY ? tm : 0.f;
+      }
+      float rs = softmax_tile(sc, pf, sl2, w.m_run);
+      if (!kFirst && __builtin_amdgcn_ballot_w64(!(rs <= kSumLimit))) rs = settle_max<D>(w, sc, pf, sl2);
+      w.l_run += rs;
+      stage_store(true, true, PAR, PAR);
+      stage_load(j + 3, j + 1);
+      lds_barrier();
+      w.pf_prev[0] = pf[0];
+      w.pf_prev[1] = pf[1];
     };
-    run(std::integral_constant<bool, false>(), kt_mask);
-    run(std::integral_constant<bool, true>(), k_end);
+    using T = std::true_type;
+    using F = std::false_type;
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    // j = 0: masked variant (exact for any tile), exact max.
+    if (n > 1) iterate(P0(), T(), T(), F(), T(), 0); else iterate(P0(), T(), F(), F(), T(), 0);
+    // Steady state j = 1 .. n - 2, unrolled by two so that tile parity is
+    // known at compile time: unmasked tiles, then masked ones.
+    int j = 1;
+    auto steady = [&](auto mask_tag, int j_end) {
+      if (j < j_end && (j & 1) == 0) iterate(P0(), mask_tag, T(), T(), F(), j++);
+      for (; j + 1 < j_end; j += 2) {
+        iterate(P1(), mask_tag, T(), T(), F(), j);
+        iterate(P0(), mask_tag, T(), T(), F(), j + 1);
+      }
+      if (j < j_end) iterate(P1(), mask_tag, T(), T(), F(), j++);
+    };
+    steady(F(), min(j_mask, n - 1));
+    steady(T(), n - 1);
+    // j = n - 1: PV(n-2) and softmax(n-1), then drain PV(n-1).
+    if (n >= 2) {
+      if ((n - 1) & 1) iterate(P1(), T(), F(), T(), F(), n - 1); else iterate(P0(), T(), F(), T(), F(), n - 1);
+    }
+    pv_tile<D>(slot_v((n - 1) & 1), w.pf_prev, w.oacc, lane);
   }
 
   // Combine the two halves' denominators and normalise.
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = w.l_run + __shfl_xor(w.l_run, 32);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  const float lse_val = l_tot > 0.f ? (m_run + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
-  const int S = sd.n_splits;
-  if (S == 1) {
-    if (!valid) return;
+  const float lse_val = l_tot > 0.f ? (w.m_run + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
+  if (!valid) return;
+  if (sd.n_splits == 1) {
     uint16_t *orow = a.out + qrow * D;
 #pragma unroll
     for (int c = 0; c < D / 32; ++c)
@@ -316,8 +415,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
       for (int g4 = 0; g4 < 4; ++g4) {
         const int dim = 32 * c + 8 * g4 + 4 * half;
         u32x2 pk;
-        pk[0] = pack_bf16(oacc[c][4 * g4 + 0] * inv, oacc[c][4 * g4 + 1] * inv);
-        pk[1] = pack_bf16(oacc[c][4 * g4 + 2] * inv, oacc[c][4 * g4 + 3] * inv);
+        pk[0] = pack_bf16(w.oacc[c][4 * g4 + 0] * inv, w.oacc[c][4 * g4 + 1] * inv);
+        pk[1] = pack_bf16(w.oacc[c][4 * g4 + 2] * inv, w.oacc[c][4 * g4 + 3] * inv);
         *reinterpret_cast<u32x2 *>(orow + dim) = pk;
       }
     if (a.lse != nullptr && half == 0) a.lse[(int64_t)h * a.total_q + sd.cu_q + qpos] = lse_val;
@@ -325,8 +424,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   }
 
   // Split-key: write this split's normalised partial and its log-sum-exp.
-  if (!valid) return;
-  const int64_t prow = (int64_t)w.split * a.total_q * a.n_q_heads + qrow;
+  const int64_t prow = (int64_t)wi.split * a.total_q * a.n_q_heads + qrow;
   float *po = a.part_o + prow * D;
 #pragma unroll
   for (int c = 0; c < D / 32; ++c)
@@ -334,10 +432,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
     for (int g4 = 0; g4 < 4; ++g4) {
       const int dim = 32 * c + 8 * g4 + 4 * half;
       f32x4 x;
-      x[0] = oacc[c][4 * g4 + 0] * inv;
-      x[1] = oacc[c][4 * g4 + 1] * inv;
-      x[2] = oacc[c][4 * g4 + 2] * inv;
-      x[3] = oacc[c][4 * g4 + 3] * inv;
+      x[0] = w.oacc[c][4 * g4 + 0] * inv;
+      x[1] = w.oacc[c][4 * g4 + 1] * inv;
+      x[2] = w.oacc[c][4 * g4 + 2] * inv;
+      x[3] = w.oacc[c][4 * g4 + 3] * inv;
       *reinterpret_cast<f32x4 *>(po + dim) = x;
     }
   if (half == 0) a.part_lse[prow] = lse_val;

@@ -58,11 +58,11 @@ class DeviceGuard {
 // ---------------------------------------------------------------------------
 namespace {
 constexpr int kXcds = 8;                 // MI355X: workgroup w is dispatched to XCD w % 8
-constexpr int kMinSplitKeys = 8 * kAttnKeyTile;
+constexpr int kMinSplitKeys = 512;
 constexpr int kMaxSplits = 16;
-constexpr int kResidentPerCu = 2;        // LDS- and VGPR-limited workgroups per CU
-constexpr int64_t kItemOverheadKeys = 2 * kAttnKeyTile;  // prologue + epilogue, in key-tile units
-constexpr int64_t kMergeOverheadKeys = kAttnKeyTile;     // partial write + merge-kernel share
+constexpr int kResidentPerCu = 1;        // one 8-wave workgroup per CU (LDS ring, 2 waves per SIMD)
+constexpr int64_t kItemOverheadKeys = 128;  // prologue + epilogue, in keys
+constexpr int64_t kMergeOverheadKeys = 64;  // partial write + merge-kernel share, in keys
 
 struct TileDesc {
   int32_t seq, kvh, q0, nq, keys;
@@ -308,6 +308,12 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
                         void *out, float *lse, int hq, int hkv, int head_dim, float scale,
                         hipStream_t stream) {
   if (plan.n_items == 0) return SC_OK;
+  // The kernel addresses one sequence's rows of one KV head with 32-bit
+  // byte offsets.
+  for (const SeqDesc &s : plan.seqs)
+    if (((int64_t)s.prefix + s.n_new) * hkv * head_dim * 2 >= ((int64_t)1 << 31))
+      return fail(SC_ERR_UNSUPPORTED, "sequence of %lld tokens x %d KV heads x head_dim %d exceeds 2 GiB of keys",
+                  (long long)s.prefix + s.n_new, hkv, head_dim);
   AttnArgs a{};
   a.q = static_cast<const uint16_t *>(q);
   a.k = static_cast<const uint16_t *>(k);

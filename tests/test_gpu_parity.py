@@ -92,7 +92,11 @@ def test_layer_path_matches_oracle(name, q_scale):
             torch.cuda.synchronize()
             compare_attention(to_u16(out), o_ref, f"{name} layer {layer} varlen")
             lse_g = lse.cpu().numpy().astype(np.float64)[:, :wl.total_q]
-            np.testing.assert_allclose(lse_g, lse_ref, atol=1e-3, rtol=1e-4)
+            # The kernel's denominator sums the bf16-rounded probabilities
+            # (the same weights that multiply V), each within 2^-9 relative
+            # of its exact value, so ln l is off by at most about 2^-9 plus
+            # fp32 accumulation: 2^-8 bounds it.
+            np.testing.assert_allclose(lse_g, lse_ref, atol=2.0 ** -8, rtol=1e-4)
             if wl.batch == 1:
                 out1 = torch.empty_like(out)
                 lse1 = torch.empty_like(lse)

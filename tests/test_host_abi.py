@@ -104,8 +104,8 @@ def test_attention_argument_validation(sc):
     sc.sc_prefill_attn(0, 0, 0, 5, 0, 8, 8, 128, 0)          # new_len == 0 is a no-op
 
 
-KEY_TILE = 64
-ROWS = 128
+KEY_TILE = 32
+ROWS = 256
 
 
 def _check_plan(sc, P, N, hq, hkv, target):
