@@ -290,7 +290,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
     const uint32_t off = (uint32_t)t * tile_bytes;
     return __builtin_amdgcn_make_buffer_rsrc(
         const_cast<char *>(reinterpret_cast<const char *>(base) + off), (short)0,
-        (int)(range_bytes > off ? range_bytes - off : 0u), 0x00020000);
+        __builtin_amdgcn_readfirstlane((int)(range_bytes > off ? range_bytes - off : 0u)), 0x00020000);
   };
 
   // Staging: chunk c = tid + 512 i of a (K tile, V tile) pair; whether it is

@@ -1,0 +1,128 @@
+"""GPU parity at the five benchmark shapes, in the launch configuration the
+benchmark times: the whole layer stack runs once through sc_prefill_stack
+(overlapped mode, two active slots, every layer fetched, appended, attended
+and stored), on the same seeded device-generated pool and inputs.
+
+Checked on layers {0, L/2, L-1} against the oracle, which works from a host
+snapshot of those layers taken before the stack ran:
+
+* fetch + append: every byte of the active layer (all tokens, all KV heads);
+  layer L-1 is read from the slot the stack itself filled, layers 0 and L/2
+  are fetched again into a slot after the stack (prefix rows are not touched
+  by the store, so the snapshot still defines them);
+* attention: sampled (sequence, query, head) rows of the stack's own output
+  -- the first and last query of every sequence, queries on both sides of a
+  256-row tile edge, and seeded random ones -- computed one by one by the
+  oracle, to |gpu - oracle| <= 2e-2 + 1e-2 |oracle|;
+* store: every byte of every block the table references, after the stack,
+  against the oracle's store applied to the snapshot.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import attention as oa
+from oracle import kvcache as ok
+from paper_2606_16135_amd import workloads as W
+
+from _gpu_util import compare_attention, require_gpu, to_u16
+
+pytestmark = pytest.mark.gpu
+
+
+def _bits_to_f32(u16):
+    """bf16 bit patterns to float32 (exact), for the oracle's row sampler."""
+    return (u16.astype(np.uint32) << 16).view(np.float32)
+
+
+def _sample_rows(wl, rng, per_seq_random=2):
+    rows = []
+    for b, n in enumerate(wl.new_len):
+        n = int(n)
+        if n == 0:
+            continue
+        qs = {0, n - 1}
+        for edge in (64, 128, 256):          # query-tile edges for groups 4/5/8
+            if edge < n:
+                qs.update({edge - 1, edge})
+        qs.update(int(x) for x in rng.integers(0, n, size=per_seq_random))
+        heads = {0, wl.n_q_heads - 1} | {int(x) for x in rng.integers(0, wl.n_q_heads, size=2)}
+        for i in sorted(qs):
+            for h in sorted(heads):
+                rows.append((b, i, h))
+    return rows
+
+
+def _sub_pool(dp, layer, ids):
+    """Layer `layer` of the referenced blocks only, in table order."""
+    return dp.layer_slice_u16(layer)[ids]
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("cfg", [2, 3, 4, 5])
+def test_benchmark_shape_stack_matches_oracle(cfg):
+    sc = require_gpu()
+    import torch
+    from paper_2606_16135_amd.torch_pool import DevicePool
+
+    wl = W.config(cfg)
+    L = wl.n_layers
+    check_layers = sorted({0, L // 2, L - 1})
+    print(f"\n[fullsize] cfg {cfg} {wl.name}: L={L} total_q={wl.total_q} total_kv={wl.total_kv}", flush=True)
+    dp = DevicePool(sc, wl, fill="torch")
+    try:
+        ids = np.asarray(wl.block_ids, dtype=np.int64)
+        local_ids = np.arange(len(ids), dtype=np.int32)      # table order in the snapshot
+        snap = {l: _sub_pool(dp, l, ids) for l in check_layers}
+
+        inputs = [W.layer_inputs_torch(wl, l, "cuda") for l in range(L)]
+        outs = [torch.empty((wl.total_q, wl.n_q_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+                for _ in range(L)]
+        slot_t = [(torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda"),
+                   torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda"))
+                  for _ in range(2)]
+        slots = [sc.active(k.data_ptr(), v.data_ptr(), wl.total_kv) for k, v in slot_t]
+        compute = torch.cuda.current_stream()
+        copy = torch.cuda.Stream()
+        sc.sc_prefill_stack(dp.handle, dp.table, [i[0].data_ptr() for i in inputs],
+                            [i[1].data_ptr() for i in inputs], [i[2].data_ptr() for i in inputs],
+                            [o.data_ptr() for o in outs], slots, wl.n_q_heads, sc.SC_STACK_OVERLAP, 0.0,
+                            compute.cuda_stream, copy.cuda_stream)
+        torch.cuda.synchronize()
+        print(f"[fullsize] cfg {cfg}: stack done", flush=True)
+
+        last_slot = [to_u16(slot_t[(L - 1) & 1][0]), to_u16(slot_t[(L - 1) & 1][1])]
+        rng = np.random.default_rng(wl.seed_for("fullsize-rows"))
+        for l in check_layers:
+            q, kn, vn = (to_u16(t) for t in inputs[l])
+            k_act, v_act = ok.gather_layer(snap[l], local_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, 0)
+            k_full, v_full = ok.append_new(k_act, v_act, kn, vn, wl.prefix_len, wl.new_len)
+
+            # fetch + append, every byte
+            if l == L - 1:
+                kg, vg = last_slot
+            else:
+                sc.sc_fetch_layer_kv(dp.handle, dp.table, l, slots[0], compute.cuda_stream)
+                sc.sc_append_new_kv(dp.handle, dp.table, inputs[l][1].data_ptr(), inputs[l][2].data_ptr(),
+                                    slots[0], compute.cuda_stream)
+                torch.cuda.synchronize()
+                kg, vg = to_u16(slot_t[0][0]), to_u16(slot_t[0][1])
+            assert np.array_equal(kg, k_full), f"cfg {cfg} layer {l}: K fetch/append"
+            assert np.array_equal(vg, v_full), f"cfg {cfg} layer {l}: V fetch/append"
+
+            # attention, sampled rows of the stack's output
+            rows = _sample_rows(wl, rng)
+            o_ref, _ = oa.attention_rows(_bits_to_f32(q), _bits_to_f32(k_full), _bits_to_f32(v_full),
+                                         wl.prefix_len, wl.new_len, rows)
+            cu_q, _ = ok.seq_offsets(wl.prefix_len, wl.new_len)
+            og = to_u16(outs[l])
+            got = np.stack([og[cu_q[b] + i, h] for b, i, h in rows])
+            stats = compare_attention(got, o_ref, f"cfg {cfg} layer {l} ({len(rows)} rows)")
+
+            # store: every referenced block of this layer
+            expect = ok.store_layer(snap[l], local_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, 0, kn, vn)
+            after = _sub_pool(dp, l, ids)
+            assert np.array_equal(after, expect), f"cfg {cfg} layer {l}: store"
+            print(f"[fullsize] cfg {cfg} layer {l}: fetch/append/store exact, attention {stats}", flush=True)
+    finally:
+        dp.close()
