@@ -35,7 +35,11 @@ sys.path.insert(0, ROOT)
 METRIC = "prefill tokens/s incl. layer-wise prefix-KV reload; fetch HBM GB/s; MFMA util"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
-PMC_TRAFFIC = None   # HBM bytes per attention launch from rocprofv3 --pmc (see profiles/)
+# HBM bytes of one attention call (forward + merge) from two rocprofv3 --pmc
+# passes (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors that map the same
+# counters to a plain 256 MiB copy), per workload, for the kernels as they
+# are now; profiles/attention_<workload>.md holds the commands and readings.
+PMC_TRAFFIC = {"llama3-8b-P8192-N512": 114503920}
 
 
 def attention_flops(wl):
@@ -202,7 +206,7 @@ def main():
     achieved_tflops = flops / t_attn_layer / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved_tflops, 2), "peak": BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved_tflops / BF16_PEAK_TFLOPS, 4),
-                "traffic": PMC_TRAFFIC,
+                "traffic": PMC_TRAFFIC.get(wl.name),
                 "kernel": "attn_fwd_kernel<128> + attn_merge_kernel (one attention call)",
                 "flops_per_launch": flops, "avg_launch_us": round(t_attn_layer * 1e6, 2)}
 
