@@ -441,55 +441,64 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   if (half == 0) a.part_lse[prow] = lse_val;
 }
 
-// 32 lanes per (token, head) row of a split sequence, D / 32 dims per lane:
-// weights exp(lse_s - max) over the splits, weighted sum of the partials.
+// Split-key merge: D / 8 lanes per (token, head) row, 8 dims per lane.
+// Weights exp(lse_s - max) over the splits, weighted sum of the partials;
+// the loads of several splits are issued before they are used.
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-  constexpr int PER_LANE = D / 32;
-  const int64_t row = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 5;
-  const int sub = threadIdx.x & 31;
-  if (row >= (int64_t)a.total_q * a.n_q_heads) return;
+  constexpr int LPR = D / 8;
+  constexpr int RPB = 256 / LPR;
+  const int64_t rows = (int64_t)a.total_q * a.n_q_heads;
+  const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
+  const int sub = threadIdx.x % LPR;
+  if (row >= rows) return;
   const int token = (int)(row / a.n_q_heads);
   const int h = (int)(row - (int64_t)token * a.n_q_heads);
-  int lo = 0, hi = a.n_seqs - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.seqs[mid].cu_q <= token) lo = mid; else hi = mid - 1;
+  int lo = 0;
+  if (a.n_seqs > 1) {
+    int hi = a.n_seqs - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.seqs[mid].cu_q <= token) lo = mid; else hi = mid - 1;
+    }
   }
   const int S = a.seqs[lo].n_splits;
   if (S <= 1) return;
-  const int64_t stride = (int64_t)a.total_q * a.n_q_heads;
+  float ls[kAttnMaxSplits];
   float mx = -INFINITY;
-  for (int s = 0; s < S; ++s) mx = fmaxf(mx, a.part_lse[s * stride + row]);
-  float acc[PER_LANE];
 #pragma unroll
-  for (int j = 0; j < PER_LANE; ++j) acc[j] = 0.f;
+  for (int s = 0; s < kAttnMaxSplits; ++s) {
+    ls[s] = s < S ? a.part_lse[s * rows + row] : -INFINITY;
+    mx = fmaxf(mx, ls[s]);
+  }
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
-  for (int s = 0; s < S; ++s) {
-    const float ls = a.part_lse[s * stride + row];
-    const float wgt = (ls == -INFINITY) ? 0.f : __expf(ls - mx);
-    wsum += wgt;
-    const float *po = a.part_o + (s * stride + row) * D + sub * PER_LANE;
-    if (PER_LANE == 4) {
-      const f32x4 x = *reinterpret_cast<const f32x4 *>(po);
+  const float *po = a.part_o + row * D + sub * 8;
 #pragma unroll
-      for (int j = 0; j < PER_LANE; ++j) acc[j] += wgt * x[j & 3];
-    } else {
-      const f32x2 x = *reinterpret_cast<const f32x2 *>(po);
+  for (int s0 = 0; s0 < kAttnMaxSplits; s0 += 4) {
+    if (s0 >= S) break;
+    f32x4 x[4][2];
 #pragma unroll
-      for (int j = 0; j < PER_LANE; ++j) acc[j] += wgt * x[j & 1];
-    }
+    for (int u = 0; u < 4; ++u)
+      if (s0 + u < S) {
+        const f32x4 *p = reinterpret_cast<const f32x4 *>(po + (int64_t)(s0 + u) * rows * D);
+        x[u][0] = p[0];
+        x[u][1] = p[1];
+      }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (s0 + u < S) {
+        const float wgt = ls[s0 + u] == -INFINITY ? 0.f : __expf(ls[s0 + u] - mx);
+        wsum += wgt;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += wgt * x[u][e >> 2][e & 3];
+      }
   }
   const float winv = wsum > 0.f ? 1.f / wsum : 0.f;
-  uint16_t *orow = a.out + row * D + sub * PER_LANE;
-  if (PER_LANE == 4) {
-    u32x2 pk;
-    pk[0] = pack_bf16(acc[0] * winv, acc[1 % PER_LANE] * winv);
-    pk[1] = pack_bf16(acc[2 % PER_LANE] * winv, acc[3 % PER_LANE] * winv);
-    *reinterpret_cast<u32x2 *>(orow) = pk;
-  } else {
-    *reinterpret_cast<uint32_t *>(orow) = pack_bf16(acc[0] * winv, acc[1 % PER_LANE] * winv);
-  }
+  u32x4 pk;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) pk[e] = pack_bf16(acc[2 * e] * winv, acc[2 * e + 1] * winv);
+  *reinterpret_cast<u32x4 *>(a.out + row * D + sub * 8) = pk;
   if (a.lse != nullptr && sub == 0)
     a.lse[(int64_t)h * a.total_q + token] = wsum > 0.f ? mx + __logf(wsum) : -INFINITY;
 }
@@ -508,7 +517,7 @@ hipError_t launch_attn_fwd(const AttnArgs &a, int head_dim, int n_items, hipStre
 hipError_t launch_attn_merge(const AttnArgs &a, int head_dim, hipStream_t stream) {
   const int64_t rows = (int64_t)a.total_q * a.n_q_heads;
   if (rows <= 0) return hipSuccess;
-  const unsigned blocks = (unsigned)((rows * 32 + 255) / 256);
+  const unsigned blocks = (unsigned)((rows * (head_dim / 8) + 255) / 256);
   if (head_dim == 128)
     hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(blocks), dim3(256), 0, stream, a);
   else

@@ -59,7 +59,7 @@ class DeviceGuard {
 namespace {
 constexpr int kXcds = 8;                 // MI355X: workgroup w is dispatched to XCD w % 8
 constexpr int kMinSplitKeys = 512;
-constexpr int kMaxSplits = 16;
+constexpr int kMaxSplits = kAttnMaxSplits;
 constexpr int kResidentPerCu = 1;        // one 8-wave workgroup per CU (LDS ring, 2 waves per SIMD)
 constexpr int64_t kItemOverheadKeys = 128;  // prologue + epilogue, in keys
 constexpr int64_t kMergeOverheadKeys = 64;  // partial write + merge-kernel share, in keys

@@ -112,6 +112,7 @@ struct AttnArgs {
 // Tile geometry the planner and the kernel agree on.
 constexpr int kAttnRows = 256;   // (query, head) rows per workgroup
 constexpr int kAttnKeyTile = 32; // keys per LDS tile
+constexpr int kAttnMaxSplits = 16; // key splits per sequence (merge kernel bound)
 
 hipError_t launch_attn_fwd(const AttnArgs &a, int head_dim, int n_items, hipStream_t stream);
 hipError_t launch_attn_merge(const AttnArgs &a, int head_dim, hipStream_t stream);
