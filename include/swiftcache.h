@@ -216,6 +216,12 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
  * are needed because this path has no FFN to hide the load behind (the
  * paper loads layer i while the FFN of layer i-1 runs).  On return all work
  * is enqueued and the compute stream is ordered after every store.
+ * "Wait for slot s" is done by the attention kernel itself on a device
+ * counter the copy stream advances (no stream-level wait in front of every
+ * attention) whenever a copy workgroup can always run beside an attention
+ * workgroup; otherwise it is a stream event wait.  The device wait is bounded
+ * (about a second per workgroup); a workgroup that gives up writes NaN rows,
+ * so a lost dependency is visible in the output, never silent.
  * Arrays of per-layer device pointers (host arrays of length n_layers):
  *   q_per_layer, knew_per_layer, vnew_per_layer, out_per_layer.
  * flags: SC_STACK_OVERLAP (two streams, two slots), SC_STACK_SERIAL

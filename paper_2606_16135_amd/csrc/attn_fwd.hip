@@ -75,6 +75,8 @@ constexpr int KT = kAttnKeyTile;
 // probability is then below 2^20, so O and l stay far from fp32 overflow
 // for any sequence length; rows never pay for a max they do not need.
 constexpr float kSumLimit = 1048576.0f;
+// Polls of the ready flag before a workgroup gives up (about a second).
+constexpr int kReadySpinLimit = 1 << 22;
 static_assert(kAttnRows == 8 * 32, "eight waves of 32 rows");
 static_assert(KT == 32, "one 32-key MFMA block per tile");
 
@@ -336,7 +338,34 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   const int my_last = min(k_end - 1, sd.prefix + qpos);
   auto lim_of = [&](int j) { return my_last - (k_begin + j * KT) - 4 * half; };
 
-  if (n > 0) {
+  // Device-side dependency on the copy stream (see AttnArgs::ready_flag).
+  // The poll is a relaxed device-scope load (no cache invalidation per
+  // workgroup: an acquire here would invalidate the XCD's L2 under the
+  // other workgroups' K/V).  No stale K/V lines can be cached: this kernel's
+  // dispatch invalidated the caches after the last reader of the slot (two
+  // layers back, same stream) had finished, nothing reads the slot until the
+  // flag is set, and the copy kernels' completion wrote their data back
+  // before the flag was written.
+  bool timed_out = false;
+  if (a.ready_flag != nullptr) {
+    __shared__ int s_timeout;
+    if (tid == 0) {
+      int spins = 0, late = 0;
+      while (__hip_atomic_load(a.ready_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < a.ready_value) {
+        if (++spins > kReadySpinLimit) {
+          late = 1;
+          __hip_atomic_store(a.ready_timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(8);
+      }
+      s_timeout = late;
+    }
+    __syncthreads();
+    timed_out = s_timeout != 0;
+  }
+
+  if (n > 0 && !timed_out) {
     // Prologue: K(0) into the ring, then QK(0); K(1) goes in and K(2), V(0)
     // are loaded for iteration 0.
     stage_load(0, -1);
@@ -404,8 +433,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
 
   // Combine the two halves' denominators and normalise.
   const float l_tot = w.l_run + __shfl_xor(w.l_run, 32);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  const float lse_val = l_tot > 0.f ? (w.m_run + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
+  const float inv = timed_out ? __builtin_nanf("") : l_tot > 0.f ? 1.f / l_tot : 0.f;
+  const float lse_val = timed_out ? __builtin_nanf("")
+                        : l_tot > 0.f ? (w.m_run + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
   if (!valid) return;
   if (sd.n_splits == 1) {
     uint16_t *orow = a.out + qrow * D;
@@ -512,6 +542,17 @@ hipError_t launch_attn_fwd(const AttnArgs &a, int head_dim, int n_items, hipStre
   else
     hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(n_items), dim3(kThreads), 0, stream, a);
   return hipGetLastError();
+}
+
+int attn_fwd_vgprs(int head_dim) {
+  hipFuncAttributes at{};
+  const void *f = head_dim == 128 ? reinterpret_cast<const void *>(&attn_fwd_kernel<128>)
+                                  : reinterpret_cast<const void *>(&attn_fwd_kernel<64>);
+  return hipFuncGetAttributes(&at, f) == hipSuccess ? at.numRegs : -1;
+}
+
+size_t attn_fwd_lds_bytes(int head_dim) {
+  return head_dim == 128 ? sizeof(uint16_t) * Geo<128>::kSmem : sizeof(uint16_t) * Geo<64>::kSmem;
 }
 
 hipError_t launch_attn_merge(const AttnArgs &a, int head_dim, hipStream_t stream) {

@@ -68,15 +68,26 @@ __global__ __launch_bounds__(kThreads) void kv_store_kernel(CopyArgs a) { copy_r
 
 }  // namespace
 
-hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream) {
+int kv_copy_vgprs() {
+  int m = 0;
+  for (const void *f : {reinterpret_cast<const void *>(&kv_fetch_kernel), reinterpret_cast<const void *>(&kv_append_kernel),
+                        reinterpret_cast<const void *>(&kv_store_kernel)}) {
+    hipFuncAttributes at{};
+    if (hipFuncGetAttributes(&at, f) != hipSuccess) return -1;
+    m = at.numRegs > m ? at.numRegs : m;
+  }
+  return m;
+}
+
+hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_reserve) {
   if (a.n_items <= 0) return hipSuccess;
   const dim3 grid(2 * a.n_items), block(kThreads);
   if (a.mode == COPY_FETCH)
-    hipLaunchKernelGGL(kv_fetch_kernel, grid, block, 0, stream, a);
+    hipLaunchKernelGGL(kv_fetch_kernel, grid, block, lds_reserve, stream, a);
   else if (a.mode == COPY_APPEND)
-    hipLaunchKernelGGL(kv_append_kernel, grid, block, 0, stream, a);
+    hipLaunchKernelGGL(kv_append_kernel, grid, block, lds_reserve, stream, a);
   else
-    hipLaunchKernelGGL(kv_store_kernel, grid, block, 0, stream, a);
+    hipLaunchKernelGGL(kv_store_kernel, grid, block, lds_reserve, stream, a);
   return hipGetLastError();
 }
 

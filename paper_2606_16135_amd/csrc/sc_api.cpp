@@ -304,9 +304,13 @@ sc_status single_plan(int device, int P, int N, int hq, int hkv, AttnPlan **out)
   return SC_OK;
 }
 
+// ready_flag / ready_value: optional device-side wait (overlapped stack);
+// after_fwd: optional event recorded once the forward kernel (the only one
+// that reads K/V) is enqueued.
 sc_status run_attention(int device, const AttnPlan &plan, const void *q, const void *k, const void *v,
                         void *out, float *lse, int hq, int hkv, int head_dim, float scale,
-                        hipStream_t stream) {
+                        hipStream_t stream, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
+                        hipEvent_t after_fwd = nullptr) {
   if (plan.n_items == 0) return SC_OK;
   // The kernel addresses one sequence's rows of one KV head with 32-bit
   // byte offsets.
@@ -338,8 +342,14 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
     a.part_o = static_cast<float *>(ws);
     a.part_lse = a.part_o + rows * head_dim;
   }
+  if (ready_flag) {
+    a.ready_flag = ready_flag;
+    a.ready_value = ready_value;
+    a.ready_timeout = reinterpret_cast<uint32_t *>(const_cast<uint64_t *>(ready_flag + 1));
+  }
   hipError_t e = launch_attn_fwd(a, head_dim, plan.n_items, stream);
   if (e != hipSuccess) return fail_hip(e, "attn_fwd launch");
+  if (after_fwd) SC_HIP(hipEventRecord(after_fwd, stream));
   if (plan.max_splits > 1) {
     e = launch_attn_merge(a, head_dim, stream);
     if (e != hipSuccess) return fail_hip(e, "attn_merge launch");
@@ -424,6 +434,48 @@ sc_status split_streams(int device, SplitStreams **out) {
   return SC_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Copy kernels beside attention (device tier).  In the overlapped stack the
+// fetch of layer l+1 is released when attention of layer l-1 ends, the same
+// moment attention of layer l becomes ready; if copy workgroups take a CU's
+// VGPRs or LDS first, the attention workgroup waits for them and the fetch
+// lands on the critical path.  Each copy workgroup therefore reserves enough
+// (unused) LDS that at most kCopyBesideAttn of them fit on a CU, and that
+// many still leave room for one attention workgroup.
+// ---------------------------------------------------------------------------
+constexpr int kCopyBesideAttn = 2;
+std::mutex g_reserve_mu;
+std::map<std::pair<int, int>, size_t> g_reserve;
+
+// Whether a copy workgroup can always start on a CU that holds an attention
+// workgroup (one wave per SIMD beside the attention's two; 512 VGPRs per
+// SIMD lane, allocated in steps of 8).  Only then may attention wait for the
+// copy stream on the device without risking a wait on itself.
+bool copy_fits_beside_attention(int head_dim) {
+  const int av = attn_fwd_vgprs(head_dim), cv = kv_copy_vgprs();
+  if (av <= 0 || cv <= 0) return false;
+  auto alloc = [](int v) { return (v + 7) / 8 * 8; };
+  return 2 * alloc(av) + alloc(cv) <= 512;
+}
+
+size_t copy_lds_reserve(int device, int head_dim) {
+  std::lock_guard<std::mutex> lk(g_reserve_mu);
+  auto key = std::make_pair(device, head_dim);
+  auto it = g_reserve.find(key);
+  if (it != g_reserve.end()) return it->second;
+  int lds_cu = 0, lds_block = 0;
+  size_t r = 0;
+  if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device) == hipSuccess &&
+      hipDeviceGetAttribute(&lds_block, hipDeviceAttributeMaxSharedMemoryPerBlock, device) == hipSuccess &&
+      lds_cu > 0) {
+    const size_t cand = ((size_t)lds_cu / (kCopyBesideAttn + 1) + 1024 + 255) & ~(size_t)255;
+    if (cand <= (size_t)lds_block && kCopyBesideAttn * cand + attn_fwd_lds_bytes(head_dim) <= (size_t)lds_cu)
+      r = cand;
+  }
+  g_reserve[key] = r;
+  return r;
+}
+
 CopyArgs copy_args(const sc_pool *p, const sc_table *t, int mode) {
   CopyArgs a{};
   a.mode = mode;
@@ -453,32 +505,34 @@ sc_status check_active(const sc_table *t, const sc_active *dst) {
   return SC_OK;
 }
 
-sc_status do_fetch(sc_pool *p, const sc_table *t, int layer, const sc_active *dst, hipStream_t s) {
+sc_status do_fetch(sc_pool *p, const sc_table *t, int layer, const sc_active *dst, hipStream_t s,
+                   size_t lds_reserve = 0) {
   CopyArgs a = copy_args(p, t, COPY_FETCH);
   a.layer_off = (int64_t)layer * (int64_t)p->slice_bytes;
   a.act_k = static_cast<char *>(dst->k);
   a.act_v = static_cast<char *>(dst->v);
-  hipError_t e = launch_kv_copy(a, s);
+  hipError_t e = launch_kv_copy(a, s, lds_reserve);
   return e == hipSuccess ? SC_OK : fail_hip(e, "fetch launch");
 }
 
 sc_status do_append(sc_pool *p, const sc_table *t, const void *kn, const void *vn, const sc_active *dst,
-                    hipStream_t s) {
+                    hipStream_t s, size_t lds_reserve = 0) {
   CopyArgs a = copy_args(p, t, COPY_APPEND);
   a.new_k = static_cast<const char *>(kn);
   a.new_v = static_cast<const char *>(vn);
   a.act_k = static_cast<char *>(dst->k);
   a.act_v = static_cast<char *>(dst->v);
-  hipError_t e = launch_kv_copy(a, s);
+  hipError_t e = launch_kv_copy(a, s, lds_reserve);
   return e == hipSuccess ? SC_OK : fail_hip(e, "append launch");
 }
 
-sc_status do_store(sc_pool *p, const sc_table *t, int layer, const void *kn, const void *vn, hipStream_t s) {
+sc_status do_store(sc_pool *p, const sc_table *t, int layer, const void *kn, const void *vn, hipStream_t s,
+                   size_t lds_reserve = 0) {
   CopyArgs a = copy_args(p, t, COPY_STORE);
   a.layer_off = (int64_t)layer * (int64_t)p->slice_bytes;
   a.new_k = static_cast<const char *>(kn);
   a.new_v = static_cast<const char *>(vn);
-  hipError_t e = launch_kv_copy(a, s);
+  hipError_t e = launch_kv_copy(a, s, lds_reserve);
   return e == hipSuccess ? SC_OK : fail_hip(e, "store launch");
 }
 
@@ -690,9 +744,10 @@ sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids
 
 void sc_table_destroy(sc_table *table) {
   if (!table) return;
-  if (table->d_items || !table->plans.empty()) {
+  if (table->d_items || table->d_sync || !table->plans.empty()) {
     DeviceGuard guard(table->pool->desc.device);
     if (table->d_items) (void)hipFree(table->d_items);
+    if (table->d_sync) (void)hipFree(table->d_sync);
     for (auto &kv : table->plans) free_plan(&kv.second);
   }
   delete table;
@@ -843,9 +898,10 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
   hipStream_t caller_cs = (hipStream_t)compute_stream;
   hipStream_t cs = ss ? ss->attn : caller_cs;
   hipStream_t xs = ss ? ss->copy : (hipStream_t)copy_stream;
-  auto attn = [&](int l, const sc_active &slot) {
+  auto attn = [&](int l, const sc_active &slot, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
+                  hipEvent_t after_fwd = nullptr) {
     return run_attention(d.device, *plan, q_per_layer[l], slot.k, slot.v, out_per_layer[l], nullptr, n_q_heads,
-                         d.n_kv_heads, d.head_dim, scale, cs);
+                         d.n_kv_heads, d.head_dim, scale, cs, ready_flag, ready_value, after_fwd);
   };
 
   if (mode == SC_STACK_ATTN_ONLY) {
@@ -865,7 +921,27 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
     return SC_OK;
   }
 
-  // Overlapped: events ready[s] (slot s filled) and free_[s] (slot s read).
+  // Overlapped.  Attention of layer l waits on the device for the copy
+  // stream's count of filled slots (table->d_sync[0], written by the copy
+  // stream after the append); a stream-level wait here would put a
+  // command-processor round trip (about 12 us measured) in front of every
+  // attention.  The copy stream, which has slack, waits on events free_[s]
+  // (attention of the layer that last used slot s has read it).
+  // Disjoint CU sets (host tier) never block each other.
+  const bool device_wait = ss != nullptr || copy_fits_beside_attention(d.head_dim);
+  uint64_t *sync = nullptr, base = 0;
+  if (device_wait) {
+    std::lock_guard<std::mutex> lk(const_cast<sc_table *>(table)->mu);
+    sc_table *t = const_cast<sc_table *>(table);
+    if (!t->d_sync) {
+      SC_HIP(hipMalloc(reinterpret_cast<void **>(&t->d_sync), 2 * sizeof(uint64_t)));
+      const uint64_t zero[2] = {0, 0};
+      SC_HIP(hipMemcpy(t->d_sync, zero, sizeof(zero), hipMemcpyHostToDevice));
+    }
+    sync = t->d_sync;
+    base = t->sync_gen;
+    t->sync_gen += (uint64_t)n_layers + 1;
+  }
   hipEvent_t ev[6] = {};
   for (auto &e : ev) {
     hipError_t he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
@@ -876,6 +952,8 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
     }
   }
   hipEvent_t *ready = ev, *free_ = ev + 2, start = ev[4], done = ev[5];
+  // Host-tier fetches already run on their own CUs (split streams).
+  const size_t reserve = ss ? 0 : copy_lds_reserve(d.device, d.head_dim);
   auto body = [&]() -> sc_status {
     // Both streams start after everything already queued on the caller's
     // compute stream.
@@ -886,13 +964,22 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
       const int s = l & 1;
       if (l >= 2) SC_HIP(hipStreamWaitEvent(xs, free_[s], 0));
       sc_status r;
-      if ((r = do_fetch(pool, table, l, &slots[s], xs)) != SC_OK) return r;
-      if ((r = do_append(pool, table, knew_per_layer[l], vnew_per_layer[l], &slots[s], xs)) != SC_OK) return r;
-      SC_HIP(hipEventRecord(ready[s], xs));
-      if (do_st && (r = do_store(pool, table, l, knew_per_layer[l], vnew_per_layer[l], xs)) != SC_OK) return r;
-      SC_HIP(hipStreamWaitEvent(cs, ready[s], 0));
-      if ((r = attn(l, slots[s])) != SC_OK) return r;
-      SC_HIP(hipEventRecord(free_[s], cs));
+      if ((r = do_fetch(pool, table, l, &slots[s], xs, reserve)) != SC_OK) return r;
+      if ((r = do_append(pool, table, knew_per_layer[l], vnew_per_layer[l], &slots[s], xs, reserve)) != SC_OK)
+        return r;
+      if (device_wait) {
+        SC_HIP(hipStreamWriteValue64(xs, sync, base + l + 1, 0));
+      } else {
+        SC_HIP(hipEventRecord(ready[s], xs));
+      }
+      if (do_st && (r = do_store(pool, table, l, knew_per_layer[l], vnew_per_layer[l], xs, reserve)) != SC_OK)
+        return r;
+      if (device_wait) {
+        if ((r = attn(l, slots[s], sync, base + l + 1, free_[s])) != SC_OK) return r;
+      } else {
+        SC_HIP(hipStreamWaitEvent(cs, ready[s], 0));
+        if ((r = attn(l, slots[s], nullptr, 0, free_[s])) != SC_OK) return r;
+      }
     }
     // The caller's compute stream ends after the last attention and store.
     SC_HIP(hipEventRecord(start, xs));

@@ -61,7 +61,9 @@ struct CopyArgs {
   const char *new_v;
 };
 
-hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream);
+// lds_reserve: bytes of LDS each copy workgroup reserves without using them
+// (limits how many copy workgroups share a CU with attention; 0 = none).
+hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_reserve = 0);
 
 // ---------------------------------------------------------------------------
 // Attention work decomposition
@@ -107,6 +109,13 @@ struct AttnArgs {
   int32_t group;
   int32_t rows_q;         // queries per workgroup tile
   float scale_log2;       // softmax scale * log2(e)
+  // Optional device-side dependency (overlapped layer stack): before reading
+  // K/V, each workgroup waits until *ready_flag >= ready_value, polling at
+  // most kReadySpinLimit times; on time-out it sets *ready_timeout and
+  // writes NaN rows instead of results.  ready_flag == nullptr: no wait.
+  const uint64_t *ready_flag;
+  uint64_t ready_value;
+  uint32_t *ready_timeout;
 };
 
 // Tile geometry the planner and the kernel agree on.
@@ -115,6 +124,9 @@ constexpr int kAttnKeyTile = 32; // keys per LDS tile
 constexpr int kAttnMaxSplits = 16; // key splits per sequence (merge kernel bound)
 
 hipError_t launch_attn_fwd(const AttnArgs &a, int head_dim, int n_items, hipStream_t stream);
+size_t attn_fwd_lds_bytes(int head_dim);
+int attn_fwd_vgprs(int head_dim);   // per work item, -1 if unknown
+int kv_copy_vgprs();                // largest of the three copy kernels
 hipError_t launch_attn_merge(const AttnArgs &a, int head_dim, hipStream_t stream);
 
 struct AttnPlan {
@@ -165,4 +177,8 @@ struct sc_table {
   int32_t n_fetch_host = 0;          // fetch items that read the host tier
   std::mutex mu;
   std::map<std::pair<int, int>, sc::AttnPlan> plans;   // keyed by (n_q_heads, slots)
+  // Overlapped stack: [0] = count of layers whose active slot is filled
+  // (written by the copy stream, polled by attention), [1] = time-out flag.
+  uint64_t *d_sync = nullptr;
+  uint64_t sync_gen = 1;
 };
