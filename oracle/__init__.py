@@ -18,6 +18,11 @@ Contents
               log-sum-exp merge of attention over disjoint key sets
               (paper §2.1-§2.2: every token attends to all tokens before it;
               §5 "Model": GQA).
+``capacity``  the master's layer stream cache and regular cache sizes and
+              the longest supported context (§3.2, Eq. 1-5).
+``elastic``   the worker's elastic cache: layer-major vs block-major resize
+              moves, the minimum elastic unit (Eq. 6-9) and the scale-up /
+              scale-down decisions of Algorithm 1 (§3.4-§3.5).
 
 Precision: bf16 inputs are upcast exactly to float64 and everything is
 computed in float64 (the paper fixes half precision for storage only).
@@ -28,4 +33,4 @@ docstrings for which pin covers which function.  No function is "parity
 unpinned".
 """
 
-from . import attention, kvcache  # noqa: F401
+from . import attention, capacity, elastic, kvcache  # noqa: F401
