@@ -210,6 +210,21 @@ def main():
                 "kernel": "attn_fwd_kernel<128> + attn_merge_kernel (one attention call)",
                 "flops_per_launch": flops, "avg_launch_us": round(t_attn_layer * 1e6, 2)}
 
+    # Elastic donor tier (§3.4): the block-major pool shrinks / grows in
+    # place; time the host call, and state what a layer-major cache would
+    # move for the same resize ((L - 1) * kept blocks * slice bytes).
+    lay = sc.sc_pool_layout_get(dp.handle)
+    cap, keep = lay.n_device_blocks, int(np.max(wl.block_ids[wl.block_ids < lay.n_device_blocks]) + 1
+                                        if np.any(wl.block_ids < lay.n_device_blocks) else 0)
+    t0r = time.perf_counter()
+    for _ in range(1000):
+        sc.sc_pool_resize(dp.handle, keep)
+        sc.sc_pool_resize(dp.handle, cap)
+    resize_us = (time.perf_counter() - t0r) / 2000 * 1e6
+    elastic = {"resize_host_us": round(resize_us, 3), "blocks_released": int(cap - keep),
+               "bytes_moved": 0,
+               "layer_major_bytes_moved": int((L - 1) * keep * lay.slice_bytes)}
+
     details = {
         "stack_ms": {"overlap": round(t_overlap, 3), "attn_only": round(t_attn_only, 3),
                      "serial": round(t_serial, 3)},
@@ -217,6 +232,7 @@ def main():
         "fetch": {"us_per_layer": round(t_fetch * 1e6, 2), "hbm_gbs": round(fetch_gbs, 1),
                   "frac_of_hbm_peak": round(fetch_gbs / HBM_PEAK_GBS, 4),
                   "payload_bytes_per_layer": fetch_payload_bytes(wl)},
+        "elastic": elastic,
         "outputs_finite": out_ok,
         "device": torch.cuda.get_device_name(0),
     }

@@ -96,8 +96,9 @@ typedef struct {
   size_t slice_bytes;        /* Eq. 1: bytes of one block of one layer */
   size_t block_bytes;        /* n_layers * slice_bytes */
   size_t row_bytes;          /* one token of one layer, K or V: n_kv_heads*head_dim*2 */
-  int64_t n_device_blocks;
+  int64_t n_device_blocks;   /* HBM tier capacity (fixes the id split)   */
   int64_t n_host_blocks;
+  int64_t device_blocks_lent;/* HBM blocks currently usable (sc_pool_resize), <= n_device_blocks */
 } sc_pool_layout;
 
 /* Active-layer buffer (the layer stream cache slot, §3.2): caller-owned
@@ -261,6 +262,91 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
 sc_status sc_attn_plan_query(int32_t batch, const int32_t *prefix_len, const int32_t *new_len,
                              int32_t n_q_heads, int32_t n_kv_heads, int32_t slots,
                              int32_t *n_items, int32_t *items, int32_t capacity, int32_t *splits);
+
+/* ------------------------------------------------------------------------
+ * Elastic donor tier and capacity planning (host only, no device work).
+ * ---------------------------------------------------------------------- */
+
+/*
+ * Resize the pool's HBM tier in place (§3.4 "Block-Major Layout": the
+ * elastic cache grows by appending blocks at the end and shrinks by
+ * releasing the last ones; with all layers of a block contiguous, nothing
+ * else moves, so the cost is O(1) whatever the layer count).  Afterwards ids
+ * [0, n_device_blocks) are usable; ids of the host tier do not change (they
+ * start at the HBM capacity given at creation).  Tables created later may
+ * only use ids below the new count.
+ * Errors: SC_ERR_INVALID (null pool); SC_ERR_RANGE (n_device_blocks < 0 or
+ * above the capacity the pool was created with); SC_ERR_INVALID when a live
+ * table still references an HBM block at or above the new count (the
+ * message names it).
+ */
+sc_status sc_pool_resize(sc_pool *pool, int64_t n_device_blocks);
+
+/* Shape of a model's KV cache (one entry per model in the formulas below). */
+typedef struct {
+  int32_t n_layers;
+  int32_t block_size;        /* tokens per block */
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t dtype_bytes;
+} sc_model_shape;
+
+/* Capacity of the master's caches, §3.2. */
+typedef struct {
+  int64_t m_block_bytes;      /* Eq. 1: 2 * B * H_kv * D * dtype           */
+  int64_t k_master;           /* Eq. 3: floor(C_master / M_block)          */
+  int64_t sum_k_workers;      /* sum over workers of Eq. 2                 */
+  int64_t n_lsc;              /* Eq. 4: min(sum K_i, K_master)             */
+  int64_t n_rc;               /* Eq. 5: floor((K_master - sum K_i) / L), 0 if negative */
+  int64_t max_context_tokens; /* (N_LSC + N_RC) * B                        */
+  int64_t conventional_blocks;/* floor(K_master / L): without the LSC      */
+} sc_capacity;
+
+/*
+ * LSC / RC sizing (§3.2, Eq. 1-5) for a master of shape `master` with
+ * master_cache_bytes of its own KV memory and n_workers workers lending
+ * worker_cache_bytes[i] bytes.  k_workers (nullable) receives Eq. 2 per
+ * worker.  Errors: SC_ERR_INVALID (null, non-positive shape, negative bytes,
+ * n_workers < 0); SC_ERR_RANGE (a product overflows 64 bits).
+ */
+sc_status sc_plan_capacity(const sc_model_shape *master, int64_t master_cache_bytes,
+                           const int64_t *worker_cache_bytes, int32_t n_workers,
+                           int64_t *k_workers, sc_capacity *out);
+
+/*
+ * Minimum elastic unit (§3.4, Eq. 6-9): BE = L * B * H_kv * D elements per
+ * block of each model, LCM = lcm(BE_master, BE_worker), MEU = LCM / BE.
+ * Scaling the master by k * meu_master blocks and the worker by
+ * k * meu_worker blocks trades the same number of elements.
+ * Errors: SC_ERR_INVALID (null, non-positive shape); SC_ERR_RANGE (overflow).
+ */
+sc_status sc_elastic_unit(const sc_model_shape *master, const sc_model_shape *worker,
+                          int64_t *meu_master, int64_t *meu_worker);
+
+/*
+ * Algorithm 1, ScaleUp: a worker holding worker_blocks blocks of
+ * worker_block_size tokens receives a request of request_len tokens.  If it
+ * needs more than it holds, it grows by the smallest multiple k of
+ * meu_worker covering the shortfall and the master gives up k * meu_master
+ * blocks; otherwise both deltas are 0.
+ * Errors: SC_ERR_INVALID (null, negative counts, non-positive block size or
+ * units); SC_ERR_RANGE (overflow).
+ */
+sc_status sc_scale_up(int64_t worker_blocks, int32_t worker_block_size, int64_t meu_worker,
+                      int64_t meu_master, int64_t request_len, int64_t *worker_delta,
+                      int64_t *master_delta);
+
+/*
+ * Algorithm 1, ScaleDown: window_lens[n_window] are the lengths of the
+ * requests seen in the last t seconds (an empty window keeps no block).  If
+ * the worker holds more than the longest of them needs, it releases the
+ * largest multiple k of meu_worker that fits in the surplus and the master
+ * gains k * meu_master blocks; otherwise both deltas are 0.
+ * Errors: as sc_scale_up; window_lens may be NULL when n_window is 0.
+ */
+sc_status sc_scale_down(int64_t worker_blocks, int32_t worker_block_size, int64_t meu_worker,
+                        int64_t meu_master, const int64_t *window_lens, int32_t n_window,
+                        int64_t *worker_delta, int64_t *master_delta);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char *sc_last_error(void);

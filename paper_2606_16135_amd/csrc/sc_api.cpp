@@ -572,6 +572,7 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
   }
   std::unique_ptr<sc_pool> p(new sc_pool());
   p->desc = d;
+  p->dev_lent = d.n_device_blocks;
   p->row_bytes = (size_t)d.n_kv_heads * d.head_dim * 2;
   p->slice_bytes = 2 * (size_t)d.block_size * p->row_bytes;   // Eq. 1 with bf16
   p->block_bytes = (size_t)d.n_layers * p->slice_bytes;
@@ -622,6 +623,21 @@ void sc_pool_destroy(sc_pool *pool) {
   delete pool;
 }
 
+sc_status sc_pool_resize(sc_pool *pool, int64_t n_device_blocks) {
+  clear_error();
+  if (!pool) return fail(SC_ERR_INVALID, "null pool");
+  if (n_device_blocks < 0 || n_device_blocks > pool->desc.n_device_blocks)
+    return fail(SC_ERR_RANGE, "HBM blocks %lld outside [0, %lld] (the capacity given at creation)",
+                (long long)n_device_blocks, (long long)pool->desc.n_device_blocks);
+  std::lock_guard<std::mutex> lk(pool->mu);
+  if (!pool->live_max_dev.empty() && *pool->live_max_dev.rbegin() >= n_device_blocks)
+    return fail(SC_ERR_INVALID, "a live table still references HBM block %lld", (long long)*pool->live_max_dev.rbegin());
+  // Block-major layout: the blocks that stay keep their addresses; the ones
+  // released (or appended) are the last ones.  No data moves.
+  pool->dev_lent = n_device_blocks;
+  return SC_OK;
+}
+
 sc_status sc_pool_layout_get(const sc_pool *pool, sc_pool_layout *out) {
   clear_error();
   if (!pool || !out) return fail(SC_ERR_INVALID, "null argument");
@@ -632,6 +648,8 @@ sc_status sc_pool_layout_get(const sc_pool *pool, sc_pool_layout *out) {
   out->row_bytes = pool->row_bytes;
   out->n_device_blocks = pool->desc.n_device_blocks;
   out->n_host_blocks = pool->desc.n_host_blocks;
+  std::lock_guard<std::mutex> lk(const_cast<sc_pool *>(pool)->mu);
+  out->device_blocks_lent = pool->dev_lent;
   return SC_OK;
 }
 
@@ -659,13 +677,23 @@ sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids
   const int64_t n_ids = cu_blocks[batch];
   if (n_ids > 0 && !block_ids) return fail(SC_ERR_INVALID, "null block_ids");
   std::vector<uint8_t> seen((size_t)n_all, 0);
+  int64_t lent;
+  {
+    std::lock_guard<std::mutex> lk(pool->mu);
+    lent = pool->dev_lent;
+  }
+  int64_t max_dev_id = -1;
   for (int64_t i = 0; i < n_ids; ++i) {
     const int32_t id = block_ids[i];
     if (id < 0 || id >= n_all)
       return fail(SC_ERR_RANGE, "block id %d at entry %lld outside the pool [0, %lld)", id, (long long)i,
                   (long long)n_all);
+    if (id < n_dev && id >= lent)
+      return fail(SC_ERR_RANGE, "block id %d at entry %lld is beyond the %lld HBM blocks the pool lends now", id,
+                  (long long)i, (long long)lent);
     if (seen[id]) return fail(SC_ERR_INVALID, "block id %d used twice in one table", id);
     seen[id] = 1;
+    if (id < n_dev) max_dev_id = std::max<int64_t>(max_dev_id, id);
   }
 
   std::unique_ptr<sc_table> t(new sc_table());
@@ -738,12 +766,29 @@ sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids
       return fail_hip(e, "table upload");
     }
   }
+  {
+    // Register with the pool; a resize may have shrunk it meanwhile.
+    std::lock_guard<std::mutex> lk(pool->mu);
+    if (max_dev_id >= pool->dev_lent) {
+      if (t->d_items) (void)hipFree(t->d_items);
+      t->d_items = nullptr;
+      return fail(SC_ERR_RANGE, "the pool shrank below block %lld while the table was being created",
+                  (long long)max_dev_id);
+    }
+    t->max_dev_id = max_dev_id;
+    pool->live_max_dev.insert(max_dev_id);
+  }
   *out = t.release();
   return SC_OK;
 }
 
 void sc_table_destroy(sc_table *table) {
   if (!table) return;
+  {
+    std::lock_guard<std::mutex> lk(table->pool->mu);
+    auto it = table->pool->live_max_dev.find(table->max_dev_id);
+    if (it != table->pool->live_max_dev.end()) table->pool->live_max_dev.erase(it);
+  }
   if (table->d_items || table->d_sync || !table->plans.empty()) {
     DeviceGuard guard(table->pool->desc.device);
     if (table->d_items) (void)hipFree(table->d_items);

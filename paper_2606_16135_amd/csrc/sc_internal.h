@@ -6,6 +6,7 @@
 
 #include <cstdint>
 #include <map>
+#include <set>
 #include <mutex>
 #include <string>
 #include <tuple>
@@ -155,6 +156,11 @@ int attn_slots(int device);
 // ---------------------------------------------------------------------------
 struct sc_pool {
   sc_pool_desc desc;
+  // Elastic HBM tier (sc_pool_resize): ids [0, dev_lent) are usable; the
+  // largest HBM id each live table references (-1: none), for the shrink check.
+  int64_t dev_lent = 0;
+  std::mutex mu;
+  std::multiset<int64_t> live_max_dev;
   char *dev_base = nullptr;
   char *host_base = nullptr;      // host address of the host tier
   char *host_dev = nullptr;       // device-visible address of the host tier
@@ -167,6 +173,7 @@ struct sc_pool {
 
 struct sc_table {
   sc_pool *pool = nullptr;
+  int64_t max_dev_id = -1;           // largest HBM block id in the table
   int32_t batch = 0;
   std::vector<int32_t> P, N;
   std::vector<int64_t> cu_q, cu_k;

@@ -35,7 +35,8 @@ EXPORTED = [
     "sc_pool_create", "sc_pool_destroy", "sc_pool_layout_get", "sc_table_create",
     "sc_table_destroy", "sc_table_totals", "sc_fetch_layer_kv", "sc_append_new_kv",
     "sc_prefill_attn", "sc_prefill_attn_varlen", "sc_store_layer_kv", "sc_prefill_stack",
-    "sc_attn_plan_query", "sc_last_error", "sc_version",
+    "sc_attn_plan_query", "sc_pool_resize", "sc_plan_capacity", "sc_elastic_unit", "sc_scale_up",
+    "sc_scale_down", "sc_last_error", "sc_version",
 ]
 
 
@@ -57,7 +58,19 @@ class sc_pool_layout(ctypes.Structure):
     _fields_ = [("device_base", ctypes.c_void_p), ("host_base", ctypes.c_void_p),
                 ("slice_bytes", ctypes.c_size_t), ("block_bytes", ctypes.c_size_t),
                 ("row_bytes", ctypes.c_size_t), ("n_device_blocks", ctypes.c_int64),
-                ("n_host_blocks", ctypes.c_int64)]
+                ("n_host_blocks", ctypes.c_int64), ("device_blocks_lent", ctypes.c_int64)]
+
+
+class sc_model_shape(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("block_size", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("dtype_bytes", ctypes.c_int32)]
+
+
+class sc_capacity(ctypes.Structure):
+    _fields_ = [("m_block_bytes", ctypes.c_int64), ("k_master", ctypes.c_int64),
+                ("sum_k_workers", ctypes.c_int64), ("n_lsc", ctypes.c_int64), ("n_rc", ctypes.c_int64),
+                ("max_context_tokens", ctypes.c_int64), ("conventional_blocks", ctypes.c_int64)]
 
 
 class sc_active(ctypes.Structure):
@@ -94,6 +107,14 @@ def load():
                                    ctypes.POINTER(VP), ctypes.POINTER(VP),
                                    ctypes.POINTER(sc_active), I32, F32, ctypes.c_uint32, VP, VP]),
         "sc_attn_plan_query": (I32, [I32, i32p, i32p, I32, I32, I32, i32p, i32p, I32, i32p]),
+        "sc_pool_resize": (I32, [P, I64]),
+        "sc_plan_capacity": (I32, [ctypes.POINTER(sc_model_shape), I64, ctypes.POINTER(I64), I32,
+                                   ctypes.POINTER(I64), ctypes.POINTER(sc_capacity)]),
+        "sc_elastic_unit": (I32, [ctypes.POINTER(sc_model_shape), ctypes.POINTER(sc_model_shape),
+                                  ctypes.POINTER(I64), ctypes.POINTER(I64)]),
+        "sc_scale_up": (I32, [I64, I32, I64, I64, I64, ctypes.POINTER(I64), ctypes.POINTER(I64)]),
+        "sc_scale_down": (I32, [I64, I32, I64, I64, ctypes.POINTER(I64), I32, ctypes.POINTER(I64),
+                                ctypes.POINTER(I64)]),
         "sc_last_error": (ctypes.c_char_p, []),
         "sc_version": (ctypes.c_char_p, []),
     }
@@ -208,3 +229,43 @@ def sc_attn_plan_query(prefix_len, new_len, n_q_heads, n_kv_heads, target_items=
                                      ctypes.byref(n), items, n.value, splits))
     arr = np.frombuffer(items, dtype=np.int32)[: 8 * n.value].reshape(n.value, 8).copy()
     return arr, list(splits)
+
+
+def sc_pool_resize(pool, n_device_blocks):
+    _check(load().sc_pool_resize(pool, int(n_device_blocks)))
+
+
+def model_shape(n_layers, block_size, n_kv_heads, head_dim, dtype_bytes=2):
+    return sc_model_shape(n_layers, block_size, n_kv_heads, head_dim, dtype_bytes)
+
+
+def sc_plan_capacity(master, master_cache_bytes, worker_cache_bytes):
+    """Returns (sc_capacity, [K_i per worker])."""
+    n = len(worker_cache_bytes)
+    w = (ctypes.c_int64 * max(1, n))(*[int(x) for x in worker_cache_bytes])
+    k = (ctypes.c_int64 * max(1, n))()
+    out = sc_capacity()
+    _check(load().sc_plan_capacity(ctypes.byref(master), int(master_cache_bytes), w, n, k, ctypes.byref(out)))
+    return out, [int(k[i]) for i in range(n)]
+
+
+def sc_elastic_unit(master, worker):
+    mm, mw = ctypes.c_int64(), ctypes.c_int64()
+    _check(load().sc_elastic_unit(ctypes.byref(master), ctypes.byref(worker), ctypes.byref(mm), ctypes.byref(mw)))
+    return mm.value, mw.value
+
+
+def sc_scale_up(worker_blocks, worker_block_size, meu_worker, meu_master, request_len):
+    dw, dm = ctypes.c_int64(), ctypes.c_int64()
+    _check(load().sc_scale_up(int(worker_blocks), int(worker_block_size), int(meu_worker), int(meu_master),
+                              int(request_len), ctypes.byref(dw), ctypes.byref(dm)))
+    return dw.value, dm.value
+
+
+def sc_scale_down(worker_blocks, worker_block_size, meu_worker, meu_master, window_lens):
+    n = len(window_lens)
+    w = (ctypes.c_int64 * max(1, n))(*[int(x) for x in window_lens])
+    dw, dm = ctypes.c_int64(), ctypes.c_int64()
+    _check(load().sc_scale_down(int(worker_blocks), int(worker_block_size), int(meu_worker), int(meu_master),
+                                w, n, ctypes.byref(dw), ctypes.byref(dm)))
+    return dw.value, dm.value
