@@ -49,10 +49,12 @@ def attention_flops(wl):
     return 4.0 * wl.head_dim * wl.n_q_heads * pairs
 
 
-def fetch_payload_bytes(wl, device_tier_only=True):
-    """Prefix KV bytes moved by one layer's fetch (K and V)."""
+def fetch_payload_bytes(wl):
+    """Prefix KV bytes moved by one layer's fetch (K and V): every prefix
+    token outside the regular cache, whose blocks attention reads in place."""
     row = 2 * wl.n_kv_heads * wl.head_dim * 2
-    return row * int(np.sum(wl.prefix_len))
+    rc_keys = int(np.sum(wl.rc_blocks_per_seq())) * wl.block_size
+    return row * (int(np.sum(wl.prefix_len)) - rc_keys)
 
 
 def cpu_baseline(wl, dp, inputs, budget_s=15.0):
@@ -91,6 +93,9 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--rc-fraction", type=float, default=0.0,
+                    help="put this fraction of each sequence's full prefix blocks in the regular "
+                         "cache (read in place by attention, never fetched)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["attention", "fetch", "copy"], default=None,
                     help="run only one kernel of the path, --steps times over every layer "
@@ -109,7 +114,7 @@ def main():
     sc.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
 
-    wl = W.config(args.config)
+    wl = W.config(args.config, rc_fraction=args.rc_fraction)
     dp = DevicePool(sc, wl, fill="torch")
     L = wl.n_layers
     inputs = [W.layer_inputs_torch(wl, l, "cuda") for l in range(L)]
@@ -245,7 +250,8 @@ def main():
                          "kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
                          "prefix_len": [int(x) for x in wl.prefix_len][:16],
                          "new_len": [int(x) for x in wl.new_len][:16], "block_size": wl.block_size,
-                         "pool_blocks": wl.n_blocks, "host_tier_blocks": wl.n_host_blocks},
+                         "pool_blocks": wl.n_blocks, "host_tier_blocks": wl.n_host_blocks,
+                         "regular_cache_blocks": wl.n_rc_blocks},
               "roofline": roofline, "details": details}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, dp, inputs)

@@ -68,14 +68,19 @@ typedef struct sc_table sc_table;   /* opaque, library-owned */
  * Block ids [0, n_device_blocks) address the HBM tier (a device allocation
  * standing in for a co-located model's idle KV memory); ids
  * [n_device_blocks, n_device_blocks + n_host_blocks) address the host-pinned
- * tier, whose block k is id n_device_blocks + k.
+ * tier, whose block k is id n_device_blocks + k; ids
+ * [n_device_blocks + n_host_blocks, ... + n_rc_blocks) address the regular
+ * cache (§3.2 "Regular Cache"): full-layer blocks in the master's own HBM,
+ * which attention reads in place through the block table instead of
+ * fetching them (needs a power-of-two block_size of at least 16).
  *
  * device_base / host_base: when non-NULL the pool indexes caller-owned
  * memory of at least n_device_blocks * block_bytes (device memory on
  * `device`) and n_host_blocks * block_bytes (pinned host memory from
  * hipHostMalloc, mapped for device access) bytes, and never frees it.  When
  * NULL the library allocates the tier (hipMalloc / hipHostMalloc) and frees
- * it in sc_pool_destroy.
+ * it in sc_pool_destroy.  rc_base likewise for n_rc_blocks * block_bytes of
+ * device memory.
  */
 typedef struct {
   int32_t n_layers;
@@ -88,6 +93,8 @@ typedef struct {
   int32_t reserved;          /* must be 0 */
   void *device_base;         /* optional caller-owned HBM tier */
   void *host_base;           /* optional caller-owned pinned host tier */
+  int64_t n_rc_blocks;       /* regular-cache blocks (0: none) */
+  void *rc_base;             /* optional caller-owned regular-cache tier */
 } sc_pool_desc;
 
 typedef struct {
@@ -99,6 +106,8 @@ typedef struct {
   int64_t n_device_blocks;   /* HBM tier capacity (fixes the id split)   */
   int64_t n_host_blocks;
   int64_t device_blocks_lent;/* HBM blocks currently usable (sc_pool_resize), <= n_device_blocks */
+  void *rc_base;             /* regular-cache tier base (device address), or NULL */
+  int64_t n_rc_blocks;
 } sc_pool_layout;
 
 /* Active-layer buffer (the layer stream cache slot, §3.2): caller-owned
@@ -132,11 +141,17 @@ sc_status sc_pool_layout_get(const sc_pool *pool, sc_pool_layout *out);
  *                      t % block_size.  The new turn continues the last,
  *                      possibly partial, prefix block.
  *   block_ids[...]     pool block ids, each in range and used at most once
- *                      within the table.
+ *                      within the table.  Regular-cache ids may only be the
+ *                      leading entries of a sequence and only for blocks the
+ *                      prefix fills completely (R_b * block_size <= P_b): those
+ *                      R_b blocks are read in place by attention and never
+ *                      fetched, stored or appended to.
  * The table copies its index arrays to the device with hipMemcpyAsync on
  * `stream` (work issued on other streams must be ordered after it).
  * Errors: SC_ERR_INVALID (null pointer, batch <= 0, negative length, wrong
- * entry count, duplicate id), SC_ERR_RANGE (id outside the pool).
+ * entry count, duplicate id, a regular-cache id after a non-regular one or
+ * in a partially filled block), SC_ERR_RANGE (id outside the pool, or an HBM
+ * id beyond the blocks the pool lends, see sc_pool_resize).
  */
 sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids,
                           const int32_t *cu_blocks, const int32_t *prefix_len,
@@ -152,7 +167,8 @@ sc_status sc_table_totals(const sc_table *table, int64_t *total_q, int64_t *tota
  * rows cu_k[b] + t of dst->k and dst->v.  Token-exact: a partial last prefix
  * block copies P_b mod block_size rows; rows of new tokens are not written.
  * Host-tier blocks are read by the kernel over the host link (zero-copy).
- * The pool is only read.
+ * Regular-cache blocks are not copied (attention reads them in place), so
+ * their rows of dst keep whatever they held.  The pool is only read.
  * Errors: SC_ERR_INVALID (null), SC_ERR_RANGE (layer outside [0, n_layers)
  * or sum(P+N) > dst->capacity_tokens).
  */
@@ -189,10 +205,15 @@ sc_status sc_prefill_attn(const void *q, const void *k_active, const void *v_act
                           int32_t n_kv_heads, int32_t head_dim, float scale, void *out,
                           float *lse, void *stream);
 
-/* The same attention for every sequence of a table (packed varlen layout):
- * q, out [sum N][n_q_heads][head_dim]; kv = the active buffer filled by
- * sc_fetch_layer_kv + sc_append_new_kv; lse (nullable) [n_q_heads][sum N]. */
-sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, const void *q,
+/* The same attention for every sequence of a table (packed varlen layout)
+ * at layer `layer`: q, out [sum N][n_q_heads][head_dim]; kv = the active
+ * buffer filled by sc_fetch_layer_kv + sc_append_new_kv; lse (nullable)
+ * [n_q_heads][sum N].  Keys in the table's regular-cache blocks are read in
+ * place from layer `layer` of the pool's regular-cache tier (their rows of
+ * kv are not read); the partial results over those keys and over the rest
+ * are combined exactly by their log-sum-exp.
+ * Errors: as sc_prefill_attn, plus SC_ERR_RANGE (layer out of range). */
+sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, int32_t layer, const void *q,
                                  const sc_active *kv, int32_t n_q_heads, float scale,
                                  void *out, float *lse, void *stream);
 
@@ -249,18 +270,22 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
  * work, no allocation).  For a batch with the given lengths, returns in
  * *n_items the number of workgroup slots; when `items` is non-NULL it also
  * receives them as int32 octets
- *   {seq, kv_head, q0, n_queries, key_begin, key_end, split, 0}
+ *   {seq, kv_head, q0, n_queries, key_begin, key_end, split, paged}
  * (seq = -1 marks an idle padding slot; slot w runs on XCD w % 8), and when
  * `splits` is non-NULL it receives each sequence's key-split count.  Every
  * workgroup covers rows (queries [q0, q0 + n_queries) x the group of query
  * heads of kv_head) and keys [key_begin, key_end); the splits of one query
- * tile partition [0, P + q0 + n_queries).  `slots` is the number of
- * workgroups the device runs at once (<= 0: 512, i.e. 256 CUs x 2).
- * Errors: SC_ERR_INVALID (null, negative length, heads as in
- * sc_prefill_attn), SC_ERR_RANGE (items non-NULL and capacity too small).
+ * tile partition [0, P + q0 + n_queries).  rc_keys (nullable) gives each
+ * sequence's leading keys held in the regular cache, as a table with that
+ * many leading regular-cache blocks would: no workgroup straddles that
+ * boundary and paged = 1 marks those that read it.  `slots` is the number
+ * of workgroups the device runs at once (<= 0: 512, i.e. 256 CUs x 2).
+ * Errors: SC_ERR_INVALID (null, negative length, rc_keys outside [0, P],
+ * heads as in sc_prefill_attn), SC_ERR_RANGE (items non-NULL and capacity
+ * too small).
  */
 sc_status sc_attn_plan_query(int32_t batch, const int32_t *prefix_len, const int32_t *new_len,
-                             int32_t n_q_heads, int32_t n_kv_heads, int32_t slots,
+                             const int32_t *rc_keys, int32_t n_q_heads, int32_t n_kv_heads, int32_t slots,
                              int32_t *n_items, int32_t *items, int32_t capacity, int32_t *splits);
 
 /* ------------------------------------------------------------------------

@@ -26,6 +26,14 @@ pool block ids in token order; prefix token ``t`` lives in block
 position ``P_b + i`` (a partially filled last prefix block is filled up
 first).
 
+Regular cache (§3.2 "Regular Cache"): when the workers' memory cannot hold
+the whole context, the master keeps some blocks with all their layers in its
+own memory.  A table may list such blocks (ids at or above ``rc_first_id``)
+as the leading entries of a sequence, for blocks the prefix fills
+completely; their keys are used where they are and the KV Load skips them
+(:func:`regular_cache_rows`).  Attention still runs over every key, so the
+gathered K/V of :func:`gather_layer` defines its input either way.
+
 Values are handled as raw 16-bit patterns (numpy ``uint16``) so that every
 comparison is on bytes.
 
@@ -131,3 +139,20 @@ def store_layer(pool, block_ids, cu_blocks, prefix_len, new_len, layer, k_new, v
         out[blk, layer, 0, row] = k_new[src]
         out[blk, layer, 1, row] = v_new[src]
     return out
+
+
+def regular_cache_rows(block_ids, cu_blocks, prefix_len, new_len, block_size, rc_first_id):
+    """Rows of the packed active buffer whose keys live in the regular cache:
+    the tokens of each sequence's leading regular-cache blocks.  The KV Load
+    writes exactly the prefix rows outside this set."""
+    _, cu_k = seq_offsets(prefix_len, new_len)
+    rows = np.zeros(int(cu_k[-1]), dtype=bool)
+    for b, p in enumerate(prefix_len):
+        ids = np.asarray(block_ids[cu_blocks[b]:cu_blocks[b + 1]])
+        lead = 0
+        while lead < len(ids) and ids[lead] >= rc_first_id:
+            lead += 1
+        assert not np.any(ids[lead:] >= rc_first_id), "regular-cache blocks lead the table"
+        assert lead * block_size <= p, "regular-cache blocks are full prefix blocks"
+        rows[cu_k[b]:cu_k[b] + lead * block_size] = True
+    return rows

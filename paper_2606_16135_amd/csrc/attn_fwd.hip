@@ -230,14 +230,13 @@ __device__ __forceinline__ float settle_max(WaveState<D> &w, const f32x16 &s, u3
   return softmax_tile(s, pf, sl2, m_new);
 }
 
-template <int D>
-__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
+// One work item.  kPaged: its keys are read in place from the regular
+// cache; the two kinds of item are separate copies of the whole body so that
+// each is register-allocated on its own.
+template <int D, bool kPaged>
+__device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi, uint16_t *smem) {
   using G_ = Geo<D>;
   constexpr int NCH = G_::kChunksPerThread;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[G_::kSmem];
-
-  const WorkItem wi = a.items[blockIdx.x];
-  if (wi.seq < 0) return;
   const SeqDesc sd = a.seqs[wi.seq];
 
   const int tid = threadIdx.x;
@@ -297,7 +296,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
 
   // Staging: chunk c = tid + 512 i of a (K tile, V tile) pair; whether it is
   // a K or a V chunk is uniform over a wave.
-  int voff[NCH], lds_off[NCH];
+  int voff[NCH], lds_off[NCH], crow[NCH], ccol[NCH];
   bool is_v[NCH];
 #pragma unroll
   for (int i = 0; i < NCH; ++i) {
@@ -306,16 +305,56 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
     const int r = c / G_::kChunksPerRow, cc = c % G_::kChunksPerRow;
     voff[i] = (int)((r * kv_stride + cc * 8) * 2);
     lds_off[i] = is_v[i] ? 2 * G_::kTileK + r * G_::kLdsV + cc * 8 : r * G_::kLdsK + cc * 8;
+    crow[i] = r;
+    ccol[i] = wi.kvh * D + cc * 8;
   }
+  // Regular-cache item: key k of the sequence is row k mod B of local block
+  // rc_ids[rc_off + k / B], read in place.  A wave's chunk i covers 4 (D=128)
+  // or 8 (D=64) consecutive rows of a tile that start on a multiple of that
+  // count, and B >= 16 is a power of two, so those rows share one block: its
+  // index is wave-uniform and the load goes through a buffer resource over
+  // that block's layer slice.  The index of tile t + 1 is read while tile t
+  // is loaded (tiles of one chunk are loaded in order, one per call), so the
+  // data loads never wait on it.  Rows past the range read the clamped last
+  // block; they are masked.
+  const int32_t *rc_ids = kPaged ? a.rc_ids + sd.rc_off : nullptr;
+  const uint16_t *rc_layer = kPaged ? a.rc_base + a.rc_layer_elems : nullptr;
+  const int rc_mask = (1 << a.block_shift) - 1;
+  const uint32_t rc_slice_bytes = (uint32_t)(a.rc_half_elems * 4);
+  int rc_next[NCH];
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) rc_next[i] = 0;
+  // The index table is read through the constant address space: the host
+  // writes it before the launch and nothing writes it during the kernel, so
+  // the uniform index loads are scalar loads.
+  const __attribute__((address_space(4))) int32_t *rc_ids_c =
+      (const __attribute__((address_space(4))) int32_t *)rc_ids;
+  auto rc_block = [&](int t, int i) {
+    const int row0 = __builtin_amdgcn_readfirstlane(crow[i]);
+    return rc_ids_c[min(k_begin + t * KT + row0, k_end - 1) >> a.block_shift];
+  };
   // A negative tile index (prologue only) skips that half of the pair.
   u32x4 lr[NCH];
   auto stage_load = [&](int kj, int vj) {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       const int t = is_v[i] ? vj : kj;
-      if (t >= 0)
+      if (t < 0) continue;
+      if (kPaged) {
+        const int blk = __builtin_amdgcn_readfirstlane(t == 0 ? rc_block(0, i) : rc_next[i]);
+        rc_next[i] = rc_block(t + 1, i);
+        const uint16_t *base = rc_layer + (int64_t)blk * a.rc_block_elems;
+        const int row = (k_begin + t * KT + crow[i]) & rc_mask;
+        const int off = (int)((row * kv_stride + ccol[i] + (is_v[i] ? a.rc_half_elems : 0)) * 2);
+        lr[i] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(base), (short)0,
+                                                         (int)rc_slice_bytes, 0x00020000),
+                       off, 0, 0));
+      } else {
         lr[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc(is_v[i] ? vb : kb, t),
                                                                                  voff[i], 0, 0));
+      }
     }
   };
   // par_k / par_v: ring slots (tile parity) the K and V chunks go to.
@@ -469,6 +508,17 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
       *reinterpret_cast<f32x4 *>(po + dim) = x;
     }
   if (half == 0) a.part_lse[prow] = lse_val;
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t smem[Geo<D>::kSmem];
+  const WorkItem wi = a.items[blockIdx.x];
+  if (wi.seq < 0) return;
+  if (wi.paged)
+    attn_item<D, true>(a, wi, smem);
+  else
+    attn_item<D, false>(a, wi, smem);
 }
 
 // Split-key merge: D / 8 lanes per (token, head) row, 8 dims per lane.

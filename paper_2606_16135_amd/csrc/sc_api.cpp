@@ -98,7 +98,8 @@ int attn_slots(int device) {
 }
 
 void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N, int n_q_heads,
-                    int n_kv_heads, int slots, AttnPlan *plan) {
+                    int n_kv_heads, int slots, AttnPlan *plan, const std::vector<int32_t> &rc_keys,
+                    const std::vector<int32_t> &rc_off) {
   const int group = n_q_heads / n_kv_heads;
   const int rows_q = kAttnRows / group;
   const int batch = (int)P.size();
@@ -114,6 +115,9 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
     s.prefix = P[b];
     s.n_new = N[b];
     s.n_splits = 1;
+    s.rc_keys = rc_keys.empty() ? 0 : rc_keys[b];
+    s.rc_off = rc_off.empty() ? 0 : rc_off[b];
+    if (s.rc_keys > 0) plan->paged = true;
     cq += N[b];
     ck += (int64_t)P[b] + N[b];
     max_kv = std::max<int64_t>(max_kv, (int64_t)P[b] + N[b]);
@@ -127,10 +131,41 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
 
   // Key-split choice: every sequence is split into chunks of at most `chunk`
   // keys; try the chunk sizes that give 1..kMaxSplits splits to the longest
-  // sequence and keep the one with the shortest simulated schedule.
-  auto splits_for = [&](int64_t chunk, int b) {
+  // sequence and keep the one with the shortest simulated schedule.  The
+  // keys read in place from the regular cache [0, rc) and the keys of the
+  // active slot [rc, keys) never share an item.
+  struct Range {
+    int32_t k_begin, k_end, paged;
+  };
+  auto split_counts = [&](int64_t chunk, int b, int *s_rc, int *s_sl) {
+    const int64_t rc = rc_keys.empty() ? 0 : rc_keys[b];
     const int64_t kv = (int64_t)P[b] + N[b];
-    return (int)std::min<int64_t>(kMaxSplits, std::max<int64_t>(1, (kv + chunk - 1) / chunk));
+    *s_rc = rc > 0 ? (int)std::min<int64_t>(kMaxSplits - 1, std::max<int64_t>(1, (rc + chunk - 1) / chunk)) : 0;
+    *s_sl = (int)std::min<int64_t>(kMaxSplits - *s_rc, std::max<int64_t>(1, (kv - rc + chunk - 1) / chunk));
+  };
+  auto ranges_for = [&](int64_t chunk, int b, int keys, std::vector<Range> *out) {
+    int s_rc, s_sl;
+    split_counts(chunk, b, &s_rc, &s_sl);
+    const int rc = rc_keys.empty() ? 0 : rc_keys[b];
+    out->clear();
+    const int rc_t = (rc + kAttnKeyTile - 1) / kAttnKeyTile;
+    for (int sp = 0; sp < s_rc; ++sp) {
+      const int b0 = std::min(rc, (int)((int64_t)sp * rc_t / s_rc) * kAttnKeyTile);
+      const int b1 = std::min(rc, (int)((int64_t)(sp + 1) * rc_t / s_rc) * kAttnKeyTile);
+      out->push_back(Range{b0, std::max(b0, b1), 1});
+    }
+    const int len = keys - rc;
+    const int sl_t = (len + kAttnKeyTile - 1) / kAttnKeyTile;
+    for (int sp = 0; sp < s_sl; ++sp) {
+      const int b0 = rc + (int)((int64_t)sp * sl_t / s_sl) * kAttnKeyTile;
+      const int b1 = std::min(keys, rc + (int)((int64_t)(sp + 1) * sl_t / s_sl) * kAttnKeyTile);
+      out->push_back(Range{std::min(b0, keys), std::max(std::min(b0, keys), b1), 0});
+    }
+  };
+  auto splits_for = [&](int64_t chunk, int b) {
+    int s_rc, s_sl;
+    split_counts(chunk, b, &s_rc, &s_sl);
+    return s_rc + s_sl;
   };
   int64_t best_chunk = std::max<int64_t>(max_kv, 1), best_span = -1;
   size_t best_items = 0;
@@ -139,13 +174,12 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
     chunk = ((chunk + kAttnKeyTile - 1) / kAttnKeyTile) * kAttnKeyTile;
     if (s > 1 && chunk < kMinSplitKeys) break;
     std::vector<int64_t> costs;
+    std::vector<Range> rs;
     for (const TileDesc &t : tiles) {
-      const int S = splits_for(chunk, t.seq);
-      const int64_t ntile = (t.keys + kAttnKeyTile - 1) / kAttnKeyTile;
-      for (int sp = 0; sp < S; ++sp) {
-        const int64_t span = ((sp + 1) * ntile / S - sp * ntile / S) * kAttnKeyTile;
-        costs.push_back(span + kItemOverheadKeys + (S > 1 ? kMergeOverheadKeys : 0));
-      }
+      ranges_for(chunk, t.seq, t.keys, &rs);
+      const int S = (int)rs.size();
+      for (const Range &r : rs)
+        costs.push_back((r.k_end - r.k_begin) + kItemOverheadKeys + (S > 1 ? kMergeOverheadKeys : 0));
     }
     const size_t n = costs.size();
     const int64_t span = lpt_makespan(costs, slots);
@@ -171,23 +205,22 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
   std::vector<GroupItems> groups;
   size_t ti = 0;
   for (int b = 0; b < batch; ++b) {
-    const int S = plan->seqs[b].n_splits;
     for (int g = 0; g < n_kv_heads; ++g) {
       GroupItems gi;
+      std::vector<Range> rs;
       for (; ti < tiles.size() && tiles[ti].seq == b && tiles[ti].kvh == g; ++ti) {
         const TileDesc &t = tiles[ti];
-        const int ntile = (t.keys + kAttnKeyTile - 1) / kAttnKeyTile;
-        for (int s = 0; s < S; ++s) {
-          const int t0 = (int)((int64_t)s * ntile / S);
-          const int t1 = (int)((int64_t)(s + 1) * ntile / S);
+        ranges_for(best_chunk, b, t.keys, &rs);
+        for (int s = 0; s < (int)rs.size(); ++s) {
           WorkItem w{};
           w.seq = b;
           w.kvh = g;
           w.q0 = t.q0;
           w.nq = t.nq;
-          w.k_begin = t0 * kAttnKeyTile;
-          w.k_end = std::max(w.k_begin, std::min(t1 * kAttnKeyTile, t.keys));
+          w.k_begin = rs[s].k_begin;
+          w.k_end = rs[s].k_end;
           w.split = s;
+          w.paged = rs[s].paged;
           gi.cost += (w.k_end - w.k_begin) + kItemOverheadKeys;
           gi.items.push_back(w);
         }
@@ -307,10 +340,18 @@ sc_status single_plan(int device, int P, int N, int hq, int hkv, AttnPlan **out)
 // ready_flag / ready_value: optional device-side wait (overlapped stack);
 // after_fwd: optional event recorded once the forward kernel (the only one
 // that reads K/V) is enqueued.
+// rc: the table's regular cache (pool, layer, device block indices) for
+// plans with paged items; required exactly when plan.paged.
+struct RcView {
+  const sc_pool *pool = nullptr;
+  int layer = 0;
+  const int32_t *ids = nullptr;
+};
+
 sc_status run_attention(int device, const AttnPlan &plan, const void *q, const void *k, const void *v,
                         void *out, float *lse, int hq, int hkv, int head_dim, float scale,
                         hipStream_t stream, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
-                        hipEvent_t after_fwd = nullptr) {
+                        hipEvent_t after_fwd = nullptr, const RcView &rc = RcView()) {
   if (plan.n_items == 0) return SC_OK;
   // The kernel addresses one sequence's rows of one KV head with 32-bit
   // byte offsets.
@@ -341,6 +382,19 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
     if (st != SC_OK) return st;
     a.part_o = static_cast<float *>(ws);
     a.part_lse = a.part_o + rows * head_dim;
+  }
+  if (plan.paged) {
+    if (!rc.pool || !rc.ids || !rc.pool->rc_base)
+      return fail(SC_ERR_INVALID, "the table reads regular-cache blocks; the call needs the pool and layer");
+    const sc_pool_desc &pd = rc.pool->desc;
+    a.rc_base = reinterpret_cast<const uint16_t *>(rc.pool->rc_base);
+    a.rc_ids = rc.ids;
+    a.rc_block_elems = (int64_t)(rc.pool->block_bytes / 2);
+    a.rc_layer_elems = (int64_t)rc.layer * (int64_t)(rc.pool->slice_bytes / 2);
+    a.rc_half_elems = (int64_t)(rc.pool->slice_bytes / 4);
+    int sh = 0;
+    while ((1 << sh) < pd.block_size) ++sh;
+    a.block_shift = sh;
   }
   if (ready_flag) {
     a.ready_flag = ready_flag;
@@ -379,7 +433,7 @@ sc_status table_plan(sc_table *t, int hq, AttnPlan **out, int slots = 0) {
     return SC_OK;
   }
   AttnPlan &plan = t->plans[key];
-  plan_attention(t->P, t->N, hq, d.n_kv_heads, slots, &plan);
+  plan_attention(t->P, t->N, hq, d.n_kv_heads, slots, &plan, t->rc_keys, t->rc_off);
   st = upload_plan(&plan);
   if (st != SC_OK) {
     free_plan(&plan);
@@ -556,15 +610,21 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
   *out = nullptr;
   const sc_pool_desc &d = *desc;
   if (d.n_layers <= 0 || d.n_kv_heads <= 0 || d.block_size <= 0 || d.block_size > 256 ||
-      d.n_device_blocks < 0 || d.n_host_blocks < 0 || d.n_device_blocks + d.n_host_blocks <= 0 ||
-      d.reserved != 0)
+      d.n_device_blocks < 0 || d.n_host_blocks < 0 || d.n_rc_blocks < 0 ||
+      d.n_device_blocks + d.n_host_blocks + d.n_rc_blocks <= 0 || d.reserved != 0)
     return fail(SC_ERR_INVALID, "invalid pool description");
   if (d.head_dim != 64 && d.head_dim != 128)
     return fail(SC_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", d.head_dim);
-  if (d.n_device_blocks + d.n_host_blocks > INT32_MAX)
+  if (d.n_device_blocks + d.n_host_blocks + d.n_rc_blocks > INT32_MAX)
     return fail(SC_ERR_RANGE, "too many blocks for 32-bit block ids");
+  // Attention pages regular-cache keys in groups of up to 8 rows that must
+  // not straddle a block.
+  if (d.n_rc_blocks > 0 && (d.block_size < 16 || (d.block_size & (d.block_size - 1)) != 0))
+    return fail(SC_ERR_UNSUPPORTED, "a regular cache needs a power-of-two block size >= 16 (got %d)",
+                d.block_size);
   // Pools over caller-owned HBM without a host tier make no HIP call here.
-  const bool needs_hip = (d.n_device_blocks > 0 && !d.device_base) || d.n_host_blocks > 0;
+  const bool needs_hip = (d.n_device_blocks > 0 && !d.device_base) || d.n_host_blocks > 0 ||
+                         (d.n_rc_blocks > 0 && !d.rc_base);
   std::unique_ptr<DeviceGuard> guard;
   if (needs_hip) {
     guard.reset(new DeviceGuard(d.device));
@@ -609,16 +669,31 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
     }
     p->host_dev = static_cast<char *>(devp);
   }
+  if (d.n_rc_blocks > 0) {
+    if (d.rc_base) {
+      p->rc_base = static_cast<char *>(d.rc_base);
+    } else {
+      const size_t rc_bytes = (size_t)d.n_rc_blocks * p->block_bytes;
+      hipError_t e = hipMalloc(reinterpret_cast<void **>(&p->rc_base), rc_bytes);
+      if (e != hipSuccess) {
+        if (p->own_dev) (void)hipFree(p->dev_base);
+        if (p->own_host) (void)hipHostFree(p->host_base);
+        return fail(SC_ERR_OOM, "hipMalloc(%zu) for the regular cache: %s", rc_bytes, hipGetErrorString(e));
+      }
+      p->own_rc = true;
+    }
+  }
   *out = p.release();
   return SC_OK;
 }
 
 void sc_pool_destroy(sc_pool *pool) {
   if (!pool) return;
-  if (pool->own_dev || pool->own_host) {
+  if (pool->own_dev || pool->own_host || pool->own_rc) {
     DeviceGuard guard(pool->desc.device);
     if (pool->own_dev && pool->dev_base) (void)hipFree(pool->dev_base);
     if (pool->own_host && pool->host_base) (void)hipHostFree(pool->host_base);
+    if (pool->own_rc && pool->rc_base) (void)hipFree(pool->rc_base);
   }
   delete pool;
 }
@@ -648,6 +723,8 @@ sc_status sc_pool_layout_get(const sc_pool *pool, sc_pool_layout *out) {
   out->row_bytes = pool->row_bytes;
   out->n_device_blocks = pool->desc.n_device_blocks;
   out->n_host_blocks = pool->desc.n_host_blocks;
+  out->rc_base = pool->rc_base;
+  out->n_rc_blocks = pool->desc.n_rc_blocks;
   std::lock_guard<std::mutex> lk(const_cast<sc_pool *>(pool)->mu);
   out->device_blocks_lent = pool->dev_lent;
   return SC_OK;
@@ -661,7 +738,8 @@ sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids
   if (batch <= 0) return fail(SC_ERR_INVALID, "batch must be positive (got %d)", batch);
   const int bs = pool->desc.block_size;
   const int64_t n_dev = pool->desc.n_device_blocks;
-  const int64_t n_all = n_dev + pool->desc.n_host_blocks;
+  const int64_t n_rc0 = n_dev + pool->desc.n_host_blocks;   // first regular-cache id
+  const int64_t n_all = n_rc0 + pool->desc.n_rc_blocks;
   if (cu_blocks[0] != 0) return fail(SC_ERR_INVALID, "cu_blocks[0] must be 0");
   int64_t total_kv = 0;
   for (int b = 0; b < batch; ++b) {
@@ -695,6 +773,23 @@ sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids
     seen[id] = 1;
     if (id < n_dev) max_dev_id = std::max<int64_t>(max_dev_id, id);
   }
+  // Regular-cache blocks: the leading, completely filled prefix blocks only.
+  std::vector<int32_t> rc_keys(batch, 0), rc_off(batch, 0), rc_ids;
+  for (int b = 0; b < batch; ++b) {
+    const int32_t *ids = block_ids + cu_blocks[b];
+    const int n_b = cu_blocks[b + 1] - cu_blocks[b];
+    int r = 0;
+    while (r < n_b && ids[r] >= n_rc0) ++r;
+    for (int j = r; j < n_b; ++j)
+      if (ids[j] >= n_rc0)
+        return fail(SC_ERR_INVALID, "sequence %d: regular-cache block %d follows a non-regular block", b, ids[j]);
+    if ((int64_t)r * bs > prefix_len[b])
+      return fail(SC_ERR_INVALID, "sequence %d: regular-cache block %d is not filled by the prefix", b,
+                  ids[r - 1]);
+    rc_keys[b] = r * bs;
+    rc_off[b] = (int32_t)rc_ids.size();
+    for (int j = 0; j < r; ++j) rc_ids.push_back((int32_t)(ids[j] - n_rc0));
+  }
 
   std::unique_ptr<sc_table> t(new sc_table());
   t->pool = pool;
@@ -709,6 +804,9 @@ sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids
   }
   t->total_q = t->cu_q[batch];
   t->total_kv = t->cu_k[batch];
+  t->rc_keys = rc_keys;
+  t->rc_off = rc_off;
+  t->h_rc_ids = rc_ids;
 
   auto locate = [&](int32_t id, CopyItem *it) {
     it->tier = id >= n_dev ? 1 : 0;
@@ -719,7 +817,7 @@ sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids
   for (int b = 0; b < batch; ++b) {
     const int32_t *ids = block_ids + cu_blocks[b];
     const int P = prefix_len[b], N = new_len[b];
-    for (int j = 0; j * bs < P; ++j) {
+    for (int j = rc_keys[b] / bs; j * bs < P; ++j) {   // regular-cache blocks are read in place
       CopyItem it{};
       locate(ids[j], &it);
       it.act_row = t->cu_k[b] + (int64_t)j * bs;
@@ -763,7 +861,21 @@ sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids
     e = hipMemcpyAsync(t->d_items, all.data(), bytes, hipMemcpyHostToDevice, (hipStream_t)stream);
     if (e != hipSuccess) {
       (void)hipFree(t->d_items);
+      t->d_items = nullptr;
       return fail_hip(e, "table upload");
+    }
+  }
+  if (!t->h_rc_ids.empty()) {
+    const size_t bytes = t->h_rc_ids.size() * sizeof(int32_t);
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(&t->d_rc_ids), bytes);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(t->d_rc_ids, t->h_rc_ids.data(), bytes, hipMemcpyHostToDevice, (hipStream_t)stream);
+    if (e != hipSuccess) {
+      if (t->d_items) (void)hipFree(t->d_items);
+      if (t->d_rc_ids) (void)hipFree(t->d_rc_ids);
+      t->d_items = nullptr;
+      t->d_rc_ids = nullptr;
+      return fail_hip(e, "table upload (regular-cache ids)");
     }
   }
   {
@@ -789,28 +901,35 @@ void sc_table_destroy(sc_table *table) {
     auto it = table->pool->live_max_dev.find(table->max_dev_id);
     if (it != table->pool->live_max_dev.end()) table->pool->live_max_dev.erase(it);
   }
-  if (table->d_items || table->d_sync || !table->plans.empty()) {
+  if (table->d_items || table->d_sync || table->d_rc_ids || !table->plans.empty()) {
     DeviceGuard guard(table->pool->desc.device);
     if (table->d_items) (void)hipFree(table->d_items);
     if (table->d_sync) (void)hipFree(table->d_sync);
+    if (table->d_rc_ids) (void)hipFree(table->d_rc_ids);
     for (auto &kv : table->plans) free_plan(&kv.second);
   }
   delete table;
 }
 
 sc_status sc_attn_plan_query(int32_t batch, const int32_t *prefix_len, const int32_t *new_len,
-                             int32_t n_q_heads, int32_t n_kv_heads, int32_t slots, int32_t *n_items,
-                             int32_t *items, int32_t capacity, int32_t *splits) {
+                             const int32_t *rc_keys, int32_t n_q_heads, int32_t n_kv_heads, int32_t slots,
+                             int32_t *n_items, int32_t *items, int32_t capacity, int32_t *splits) {
   clear_error();
   if (batch <= 0 || !prefix_len || !new_len || !n_items) return fail(SC_ERR_INVALID, "null argument");
   sc_status st = check_heads(n_q_heads, n_kv_heads, 128);
   if (st != SC_OK) return st;
-  for (int b = 0; b < batch; ++b)
+  for (int b = 0; b < batch; ++b) {
     if (prefix_len[b] < 0 || new_len[b] < 0) return fail(SC_ERR_INVALID, "negative length");
+    if (rc_keys && (rc_keys[b] < 0 || rc_keys[b] > prefix_len[b]))
+      return fail(SC_ERR_INVALID, "sequence %d: regular-cache keys %d outside [0, %d]", b, rc_keys[b],
+                  prefix_len[b]);
+  }
+  std::vector<int32_t> rc;
+  if (rc_keys) rc.assign(rc_keys, rc_keys + batch);
   AttnPlan plan;
   plan_attention(std::vector<int32_t>(prefix_len, prefix_len + batch),
                  std::vector<int32_t>(new_len, new_len + batch), n_q_heads, n_kv_heads,
-                 slots > 0 ? slots : 512, &plan);
+                 slots > 0 ? slots : 512, &plan, rc, std::vector<int32_t>(rc.size(), 0));
   *n_items = plan.n_items;
   if (items) {
     if (capacity < plan.n_items) return fail(SC_ERR_RANGE, "capacity %d < %d items", capacity, plan.n_items);
@@ -884,11 +1003,14 @@ sc_status sc_prefill_attn(const void *q, const void *k_active, const void *v_act
                        scale, (hipStream_t)stream);
 }
 
-sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, const void *q, const sc_active *kv,
-                                 int32_t n_q_heads, float scale, void *out, float *lse, void *stream) {
+sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, int32_t layer, const void *q,
+                                 const sc_active *kv, int32_t n_q_heads, float scale, void *out, float *lse,
+                                 void *stream) {
   clear_error();
   if (!pool || !table) return fail(SC_ERR_INVALID, "null argument");
   if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
+  if (layer < 0 || layer >= pool->desc.n_layers)
+    return fail(SC_ERR_RANGE, "layer %d outside [0, %d)", layer, pool->desc.n_layers);
   sc_status st = check_active(table, kv);
   if (st != SC_OK) return st;
   if (table->total_q == 0) return SC_OK;
@@ -898,8 +1020,9 @@ sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, const voi
   st = table_plan(const_cast<sc_table *>(table), n_q_heads, &plan);
   if (st != SC_OK) return st;
   const sc_pool_desc &d = pool->desc;
+  RcView rc{pool, layer, table->d_rc_ids};
   return run_attention(d.device, *plan, q, kv->k, kv->v, out, lse, n_q_heads, d.n_kv_heads, d.head_dim, scale,
-                       (hipStream_t)stream);
+                       (hipStream_t)stream, nullptr, 0, nullptr, rc);
 }
 
 sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, const void *const *q_per_layer,
@@ -945,8 +1068,9 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
   hipStream_t xs = ss ? ss->copy : (hipStream_t)copy_stream;
   auto attn = [&](int l, const sc_active &slot, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
                   hipEvent_t after_fwd = nullptr) {
+    RcView rc{pool, l, table->d_rc_ids};
     return run_attention(d.device, *plan, q_per_layer[l], slot.k, slot.v, out_per_layer[l], nullptr, n_q_heads,
-                         d.n_kv_heads, d.head_dim, scale, cs, ready_flag, ready_value, after_fwd);
+                         d.n_kv_heads, d.head_dim, scale, cs, ready_flag, ready_value, after_fwd, rc);
   };
 
   if (mode == SC_STACK_ATTN_ONLY) {

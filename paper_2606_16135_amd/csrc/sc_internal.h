@@ -75,7 +75,9 @@ struct SeqDesc {
   int32_t prefix;     // P
   int32_t n_new;      // N
   int32_t n_splits;   // key splits of every query tile of this sequence
-  int32_t pad[3];
+  int32_t rc_keys;    // leading keys read in place from the regular cache
+  int32_t rc_off;     // first entry of the sequence in AttnArgs::rc_ids
+  int32_t pad;
 };
 static_assert(sizeof(SeqDesc) == 32, "SeqDesc layout");
 
@@ -86,10 +88,10 @@ struct WorkItem {
   int32_t kvh;
   int32_t q0;
   int32_t nq;
-  int32_t k_begin;    // multiple of the key tile
+  int32_t k_begin;
   int32_t k_end;
   int32_t split;
-  int32_t pad;
+  int32_t paged;      // 1: keys [k_begin, k_end) come from the regular cache in place
 };
 static_assert(sizeof(WorkItem) == 32, "WorkItem layout");
 
@@ -117,6 +119,16 @@ struct AttnArgs {
   const uint64_t *ready_flag;
   uint64_t ready_value;
   uint32_t *ready_timeout;
+  // Regular cache (paged items): block i of sequence s is local block
+  // rc_ids[seqs[s].rc_off + i] of the tier at rc_base, whose layer-l K rows
+  // start at rc_base + id * rc_block_elems + rc_layer_elems (V rows
+  // rc_half_elems further); block_shift = log2(block_size).
+  const uint16_t *rc_base;
+  const int32_t *rc_ids;
+  int64_t rc_block_elems;
+  int64_t rc_layer_elems;
+  int64_t rc_half_elems;
+  int32_t block_shift;
 };
 
 // Tile geometry the planner and the kernel agree on.
@@ -131,6 +143,7 @@ int kv_copy_vgprs();                // largest of the three copy kernels
 hipError_t launch_attn_merge(const AttnArgs &a, int head_dim, hipStream_t stream);
 
 struct AttnPlan {
+  bool paged = false;              // some items read the regular cache in place
   int group = 0;
   int rows_q = 0;
   int max_splits = 1;
@@ -145,8 +158,12 @@ struct AttnPlan {
 
 // Builds the work list for a batch (host only; no device work).
 // `slots` = workgroups the device runs at once (CUs x resident workgroups).
+// rc_keys[b] (may be empty = none) leading keys of sequence b are read in
+// place from the regular cache: they get items of their own (a split
+// boundary at rc_keys[b]).
 void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N, int n_q_heads,
-                    int n_kv_heads, int slots, AttnPlan *plan);
+                    int n_kv_heads, int slots, AttnPlan *plan, const std::vector<int32_t> &rc_keys = {},
+                    const std::vector<int32_t> &rc_off = {});
 int attn_slots(int device);
 
 }  // namespace sc
@@ -156,6 +173,8 @@ int attn_slots(int device);
 // ---------------------------------------------------------------------------
 struct sc_pool {
   sc_pool_desc desc;
+  char *rc_base = nullptr;        // regular-cache tier (device)
+  bool own_rc = false;
   // Elastic HBM tier (sc_pool_resize): ids [0, dev_lent) are usable; the
   // largest HBM id each live table references (-1: none), for the shrink check.
   int64_t dev_lent = 0;
@@ -174,6 +193,9 @@ struct sc_pool {
 struct sc_table {
   sc_pool *pool = nullptr;
   int64_t max_dev_id = -1;           // largest HBM block id in the table
+  std::vector<int32_t> rc_keys, rc_off; // per sequence: keys read in place, offset into rc ids
+  std::vector<int32_t> h_rc_ids;     // local regular-cache block index per leading block
+  int32_t *d_rc_ids = nullptr;
   int32_t batch = 0;
   std::vector<int32_t> P, N;
   std::vector<int64_t> cu_q, cu_k;

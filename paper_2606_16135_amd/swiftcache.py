@@ -51,14 +51,16 @@ class sc_pool_desc(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
                 ("n_device_blocks", ctypes.c_int64), ("n_host_blocks", ctypes.c_int64),
                 ("device", ctypes.c_int32), ("reserved", ctypes.c_int32),
-                ("device_base", ctypes.c_void_p), ("host_base", ctypes.c_void_p)]
+                ("device_base", ctypes.c_void_p), ("host_base", ctypes.c_void_p),
+                ("n_rc_blocks", ctypes.c_int64), ("rc_base", ctypes.c_void_p)]
 
 
 class sc_pool_layout(ctypes.Structure):
     _fields_ = [("device_base", ctypes.c_void_p), ("host_base", ctypes.c_void_p),
                 ("slice_bytes", ctypes.c_size_t), ("block_bytes", ctypes.c_size_t),
                 ("row_bytes", ctypes.c_size_t), ("n_device_blocks", ctypes.c_int64),
-                ("n_host_blocks", ctypes.c_int64), ("device_blocks_lent", ctypes.c_int64)]
+                ("n_host_blocks", ctypes.c_int64), ("device_blocks_lent", ctypes.c_int64),
+                ("rc_base", ctypes.c_void_p), ("n_rc_blocks", ctypes.c_int64)]
 
 
 class sc_model_shape(ctypes.Structure):
@@ -101,12 +103,12 @@ def load():
         "sc_fetch_layer_kv": (I32, [P, P, I32, ctypes.POINTER(sc_active), VP]),
         "sc_append_new_kv": (I32, [P, P, VP, VP, ctypes.POINTER(sc_active), VP]),
         "sc_prefill_attn": (I32, [VP, VP, VP, I32, I32, I32, I32, I32, F32, VP, VP, VP]),
-        "sc_prefill_attn_varlen": (I32, [P, P, VP, ctypes.POINTER(sc_active), I32, F32, VP, VP, VP]),
+        "sc_prefill_attn_varlen": (I32, [P, P, I32, VP, ctypes.POINTER(sc_active), I32, F32, VP, VP, VP]),
         "sc_store_layer_kv": (I32, [P, P, I32, VP, VP, VP]),
         "sc_prefill_stack": (I32, [P, P, I32, ctypes.POINTER(VP), ctypes.POINTER(VP),
                                    ctypes.POINTER(VP), ctypes.POINTER(VP),
                                    ctypes.POINTER(sc_active), I32, F32, ctypes.c_uint32, VP, VP]),
-        "sc_attn_plan_query": (I32, [I32, i32p, i32p, I32, I32, I32, i32p, i32p, I32, i32p]),
+        "sc_attn_plan_query": (I32, [I32, i32p, i32p, VP, I32, I32, I32, i32p, i32p, I32, i32p]),
         "sc_pool_resize": (I32, [P, I64]),
         "sc_plan_capacity": (I32, [ctypes.POINTER(sc_model_shape), I64, ctypes.POINTER(I64), I32,
                                    ctypes.POINTER(I64), ctypes.POINTER(sc_capacity)]),
@@ -141,9 +143,9 @@ def sc_version():
 
 
 def sc_pool_create(n_layers, n_kv_heads, head_dim, block_size, n_device_blocks, n_host_blocks=0,
-                   device=0, device_base=0, host_base=0):
+                   device=0, device_base=0, host_base=0, n_rc_blocks=0, rc_base=0):
     d = sc_pool_desc(n_layers, n_kv_heads, head_dim, block_size, n_device_blocks, n_host_blocks,
-                     device, 0, device_base or None, host_base or None)
+                     device, 0, device_base or None, host_base or None, n_rc_blocks, rc_base or None)
     h = ctypes.c_void_p()
     _check(load().sc_pool_create(ctypes.byref(d), ctypes.byref(h)))
     return h.value
@@ -200,8 +202,8 @@ def sc_prefill_attn(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_
                                   head_dim, scale, out, lse or None, stream or None))
 
 
-def sc_prefill_attn_varlen(pool, table, q, kv, n_q_heads, out, lse=0, scale=0.0, stream=0):
-    _check(load().sc_prefill_attn_varlen(pool, table, q, ctypes.byref(kv), n_q_heads, scale, out,
+def sc_prefill_attn_varlen(pool, table, layer, q, kv, n_q_heads, out, lse=0, scale=0.0, stream=0):
+    _check(load().sc_prefill_attn_varlen(pool, table, layer, q, ctypes.byref(kv), n_q_heads, scale, out,
                                          lse or None, stream or None))
 
 
@@ -215,17 +217,19 @@ def sc_prefill_stack(pool, table, q_ptrs, knew_ptrs, vnew_ptrs, out_ptrs, slots,
                                    compute_stream or None, copy_stream or None))
 
 
-def sc_attn_plan_query(prefix_len, new_len, n_q_heads, n_kv_heads, target_items=0):
+def sc_attn_plan_query(prefix_len, new_len, n_q_heads, n_kv_heads, target_items=0, rc_keys=None):
     """Returns (items [n][8] int32 list, splits per sequence)."""
     import numpy as np
     batch = len(prefix_len)
     n = ctypes.c_int32()
     P, N = _i32_array(prefix_len), _i32_array(new_len)
-    _check(load().sc_attn_plan_query(batch, P, N, n_q_heads, n_kv_heads, target_items,
+    rc_arr = _i32_array(rc_keys) if rc_keys is not None else None
+    rc = ctypes.cast(rc_arr, ctypes.c_void_p) if rc_arr is not None else None
+    _check(load().sc_attn_plan_query(batch, P, N, rc, n_q_heads, n_kv_heads, target_items,
                                      ctypes.byref(n), None, 0, None))
     items = (ctypes.c_int32 * (8 * max(1, n.value)))()
     splits = (ctypes.c_int32 * batch)()
-    _check(load().sc_attn_plan_query(batch, P, N, n_q_heads, n_kv_heads, target_items,
+    _check(load().sc_attn_plan_query(batch, P, N, rc, n_q_heads, n_kv_heads, target_items,
                                      ctypes.byref(n), items, n.value, splits))
     arr = np.frombuffer(items, dtype=np.int32)[: 8 * n.value].reshape(n.value, 8).copy()
     return arr, list(splits)

@@ -18,7 +18,8 @@ def from_u16(a, device):
 
 class DevicePool:
     """A workload's pool in caller-owned memory: a device tensor for the HBM
-    tier and a pinned host tensor for the host tier."""
+    tier, a pinned host tensor for the host tier and a device tensor for the
+    regular-cache tier."""
 
     def __init__(self, sc, wl, pool_u16=None, fill="numpy"):
         self.sc, self.wl = sc, wl
@@ -27,21 +28,28 @@ class DevicePool:
         self.host = None
         if wl.n_host_blocks:
             self.host = torch.empty(wl.n_host_blocks * be, dtype=torch.bfloat16).pin_memory()
+        self.rc = None
+        if wl.n_rc_blocks:
+            self.rc = torch.empty(wl.n_rc_blocks * be, dtype=torch.bfloat16, device="cuda")
         if pool_u16 is not None:
             flat = pool_u16.reshape(wl.n_blocks, be)
             self.dev.view(torch.int16)[: wl.n_device_blocks * be].copy_(
                 torch.from_numpy(flat[: wl.n_device_blocks].reshape(-1).view(np.int16)))
             if self.host is not None:
                 self.host.view(torch.int16).copy_(
-                    torch.from_numpy(flat[wl.n_device_blocks:].reshape(-1).view(np.int16)))
+                    torch.from_numpy(flat[wl.n_device_blocks:wl.rc_first_id].reshape(-1).view(np.int16)))
+            if self.rc is not None:
+                self.rc.view(torch.int16).copy_(
+                    torch.from_numpy(flat[wl.rc_first_id:].reshape(-1).view(np.int16)))
         elif fill == "torch":
             from paper_2606_16135_amd.workloads import fill_pool_torch
-            fill_pool_torch(wl, self.dev, self.host)
+            fill_pool_torch(wl, self.dev, self.host, rc_pool=self.rc)
         torch.cuda.synchronize()
         self.handle = sc.sc_pool_create(wl.n_layers, wl.n_kv_heads, wl.head_dim, wl.block_size,
                                         wl.n_device_blocks, wl.n_host_blocks, 0,
                                         self.dev.data_ptr(),
-                                        self.host.data_ptr() if self.host is not None else 0)
+                                        self.host.data_ptr() if self.host is not None else 0,
+                                        wl.n_rc_blocks, self.rc.data_ptr() if self.rc is not None else 0)
         self.table = sc.sc_table_create(self.handle, wl.block_ids, wl.cu_blocks, wl.prefix_len,
                                         wl.new_len, torch.cuda.current_stream().cuda_stream)
 
@@ -58,6 +66,9 @@ class DevicePool:
         if wl.n_host_blocks:
             h = self.host.view(torch.int16).view(wl.n_host_blocks, wl.n_layers, *shp)[:, layer].numpy()
             parts.append(h.copy())
+        if wl.n_rc_blocks:
+            r = self.rc.view(torch.int16).view(wl.n_rc_blocks, wl.n_layers, *shp)[:, layer].cpu().numpy()
+            parts.append(r)
         return np.concatenate(parts).view(np.uint16)[:, None]
 
     def full_u16(self):
@@ -67,6 +78,8 @@ class DevicePool:
             parts.append(self.dev.view(torch.int16)[: wl.n_device_blocks * wl.block_elems].cpu().numpy())
         if wl.n_host_blocks:
             parts.append(self.host.view(torch.int16).numpy().copy())
+        if wl.n_rc_blocks:
+            parts.append(self.rc.view(torch.int16).cpu().numpy())
         return np.concatenate(parts).view(np.uint16).reshape(wl.pool_shape())
 
     def close(self):

@@ -41,6 +41,7 @@ class Workload:
     cu_blocks: np.ndarray           # int32 [batch + 1]
     seed: int
     description: str = ""
+    n_rc_blocks: int = 0            # regular-cache tier (ids after the host tier)
 
     @property
     def batch(self):
@@ -48,7 +49,22 @@ class Workload:
 
     @property
     def n_blocks(self):
+        return self.n_device_blocks + self.n_host_blocks + self.n_rc_blocks
+
+    @property
+    def rc_first_id(self):
         return self.n_device_blocks + self.n_host_blocks
+
+    def rc_blocks_per_seq(self):
+        """Leading regular-cache entries of each sequence's table."""
+        out = np.zeros(self.batch, dtype=np.int32)
+        for b in range(self.batch):
+            ids = self.block_ids[self.cu_blocks[b]:self.cu_blocks[b + 1]]
+            r = 0
+            while r < len(ids) and ids[r] >= self.rc_first_id:
+                r += 1
+            out[b] = r
+        return out
 
     @property
     def total_q(self):
@@ -96,32 +112,52 @@ def _place(rng, total_blocks, needed):
 
 def make_workload(name, n_layers, n_q_heads, n_kv_heads, head_dim, prefix_len,
                   new_len, seed, block_size=16, pool_factor=4, host_fraction=0.0,
-                  description=""):
+                  description="", rc_fraction=0.0):
     """Build a workload with a seeded block placement.
 
-    The pool holds ``pool_factor`` times the blocks the batch needs; a
-    fraction ``host_fraction`` of the pool slots is the host-pinned tier (its
-    ids follow the device tier's).  Table entries are drawn without
-    replacement from all slots, so about ``host_fraction`` of the blocks of
-    each sequence land on the host tier."""
+    The donor pool holds ``pool_factor`` times the donor blocks the batch
+    needs; a fraction ``host_fraction`` of its slots is the host-pinned tier
+    (its ids follow the device tier's).  Table entries are drawn without
+    replacement from all donor slots, so about ``host_fraction`` of the
+    blocks of each sequence land on the host tier.
+
+    ``rc_fraction`` > 0 moves the first floor(rc_fraction * (P // B)) blocks
+    of each sequence -- blocks its prefix fills completely -- to a regular
+    cache tier (ids after the host tier, ``pool_factor`` times the blocks
+    placed there, seeded placement of their own)."""
     prefix_len = np.asarray(prefix_len, dtype=np.int32)
     new_len = np.asarray(new_len, dtype=np.int32)
     per_seq = np.array([_blocks_for(p, n, block_size) for p, n in zip(prefix_len, new_len)],
                        dtype=np.int64)
-    needed = int(per_seq.sum())
+    rc_seq = np.array([int(math.floor(rc_fraction * (int(p) // block_size))) for p in prefix_len],
+                      dtype=np.int64)
+    needed = int(per_seq.sum() - rc_seq.sum())
     total = max(needed, int(round(pool_factor * needed)))
     n_host = int(round(host_fraction * total))
     n_dev = total - n_host
     rng = np.random.default_rng(np.random.SeedSequence([seed, _tag_int("placement")]))
-    ids = _place(rng, total, needed)
+    donor = _place(rng, total, needed)
+    n_rc_needed = int(rc_seq.sum())
+    n_rc = max(n_rc_needed, int(round(pool_factor * n_rc_needed))) if n_rc_needed else 0
+    rc_ids = np.zeros(0, dtype=np.int32)
+    if n_rc_needed:
+        rng_rc = np.random.default_rng(np.random.SeedSequence([seed, _tag_int("placement-rc")]))
+        rc_ids = (_place(rng_rc, n_rc, n_rc_needed) + total).astype(np.int32)
+    parts, di, ri = [], 0, 0
+    for b in range(len(prefix_len)):
+        r, rest = int(rc_seq[b]), int(per_seq[b] - rc_seq[b])
+        parts += [rc_ids[ri:ri + r], donor[di:di + rest]]
+        ri, di = ri + r, di + rest
+    ids = np.concatenate(parts).astype(np.int32) if parts else donor
     cu = np.concatenate([[0], np.cumsum(per_seq)]).astype(np.int32)
     return Workload(name=name, n_layers=n_layers, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
                     head_dim=head_dim, block_size=block_size, prefix_len=prefix_len,
                     new_len=new_len, n_device_blocks=n_dev, n_host_blocks=n_host,
-                    block_ids=ids, cu_blocks=cu, seed=seed, description=description)
+                    block_ids=ids, cu_blocks=cu, seed=seed, description=description,
+                    n_rc_blocks=n_rc)
 
 
-def config(index, seed=None):
+def config(index, seed=None, rc_fraction=0.0):
     """The five benchmark shapes, numbered 1..5.
 
     1 tiny: 1 layer, 8/8 heads, D=64, prefix 256 (16 blocks) + new 64, pool of
@@ -135,43 +171,54 @@ def config(index, seed=None):
       1024, pool 4x.
     5 long context, 8B shape: prefix 131072, new 2048; pool 2x what is needed,
       half of it on the host-pinned tier.
+
+    ``rc_fraction`` > 0 gives each sequence a regular-cache tier for that
+    fraction of its full prefix blocks (see make_workload); the name and
+    description say so.
     """
     if seed is None:
         seed = SEED_BASE + index
+    kw = {}
     if index == 1:
-        p, n = [256], [64]
-        wl = make_workload("tiny-L1-H8-D64-P256-N64", 1, 8, 8, 64, p, n, seed,
-                           pool_factor=64 / 20, description="1 layer, 8/8 heads, D=64, P=256, N=64")
-        assert wl.n_blocks == 64
-        return wl
-    if index == 2:
-        return make_workload("llama3-8b-P8192-N512", 32, 32, 8, 128, [8192], [512], seed,
-                             description="32 layers, 32q/8kv heads, D=128, P=8192, N=512, batch 1")
-    if index == 3:
+        name, shape, p, n = "tiny-L1-H8-D64-P256-N64", (1, 8, 8, 64), [256], [64]
+        kw = dict(pool_factor=64 / 20)
+        desc = "1 layer, 8/8 heads, D=64, P=256, N=64"
+    elif index == 2:
+        name, shape, p, n = "llama3-8b-P8192-N512", (32, 32, 8, 128), [8192], [512]
+        desc = "32 layers, 32q/8kv heads, D=128, P=8192, N=512, batch 1"
+    elif index == 3:
         rng = np.random.default_rng(np.random.SeedSequence([seed, _tag_int("lengths")]))
-        p = np.floor(np.clip(rng.lognormal(math.log(4096.0), 0.8, size=16), 512, 32768))
-        n = rng.integers(64, 1024, size=16, endpoint=True)
-        return make_workload("llama3-8b-batch16-varlen", 32, 32, 8, 128, p.astype(np.int32),
-                             n.astype(np.int32), seed,
-                             description="32 layers, 32q/8kv, D=128, 16 conversations, "
-                                         "P~lognormal(ln4096,0.8) in [512,32768], N~U[64,1024]")
-    if index == 4:
-        return make_workload("qwen-14b-P32768-N1024", 48, 40, 8, 128, [32768], [1024], seed,
-                             description="48 layers, 40q/8kv heads, D=128, P=32768, N=1024")
-    if index == 5:
-        return make_workload("llama3-8b-P131072-N2048-hosttier", 32, 32, 8, 128, [131072], [2048],
-                             seed, pool_factor=2, host_fraction=0.5,
-                             description="32 layers, 32q/8kv, D=128, P=131072, N=2048, "
-                                         "pool 2x, half host-pinned")
-    raise ValueError(f"unknown config {index}")
+        p = np.floor(np.clip(rng.lognormal(math.log(4096.0), 0.8, size=16), 512, 32768)).astype(np.int32)
+        n = rng.integers(64, 1024, size=16, endpoint=True).astype(np.int32)
+        name, shape = "llama3-8b-batch16-varlen", (32, 32, 8, 128)
+        desc = ("32 layers, 32q/8kv, D=128, 16 conversations, "
+                "P~lognormal(ln4096,0.8) in [512,32768], N~U[64,1024]")
+    elif index == 4:
+        name, shape, p, n = "qwen-14b-P32768-N1024", (48, 40, 8, 128), [32768], [1024]
+        desc = "48 layers, 40q/8kv heads, D=128, P=32768, N=1024"
+    elif index == 5:
+        name, shape, p, n = "llama3-8b-P131072-N2048-hosttier", (32, 32, 8, 128), [131072], [2048]
+        kw = dict(pool_factor=2, host_fraction=0.5)
+        desc = "32 layers, 32q/8kv, D=128, P=131072, N=2048, pool 2x, half host-pinned"
+    else:
+        raise ValueError(f"unknown config {index}")
+    if rc_fraction:
+        name += f"-rc{rc_fraction:g}"
+        desc += f", regular cache for {rc_fraction:g} of the full prefix blocks"
+    wl = make_workload(name, *shape, p, n, seed, description=desc, rc_fraction=rc_fraction, **kw)
+    if index == 1 and not rc_fraction:
+        assert wl.n_blocks == 64
+    return wl
 
 
 def small_workload(seed, prefix_len, new_len, n_layers=2, n_q_heads=8, n_kv_heads=2,
-                   head_dim=64, block_size=16, pool_factor=2.0, host_fraction=0.0):
+                   head_dim=64, block_size=16, pool_factor=2.0, host_fraction=0.0, rc_fraction=0.0):
     """A custom small workload for parity edge cases."""
     return make_workload(f"small-{seed}", n_layers, n_q_heads, n_kv_heads, head_dim,
                          prefix_len, new_len, seed, block_size=block_size,
-                         pool_factor=pool_factor, host_fraction=host_fraction)
+                         pool_factor=pool_factor, host_fraction=host_fraction,
+                         rc_fraction=rc_fraction)
+
 
 
 # ----------------------------------------------------------------------------
@@ -223,11 +270,13 @@ def _torch_gen(wl, tag, device):
     return g
 
 
-def fill_pool_torch(wl, dev_pool, host_pool=None, chunk_blocks=256):
-    """Fill a device pool tensor (and the host-tier tensor, if any) in place.
+def fill_pool_torch(wl, dev_pool, host_pool=None, chunk_blocks=256, rc_pool=None):
+    """Fill a device pool tensor (and the host-tier and regular-cache
+    tensors, if any) in place.
 
     ``dev_pool`` is a bf16 tensor of ``n_device_blocks * block_elems``
-    elements; ``host_pool`` is a pinned CPU tensor for the host tier.
+    elements; ``host_pool`` is a pinned CPU tensor for the host tier;
+    ``rc_pool`` a device tensor of ``n_rc_blocks * block_elems`` elements.
     Referenced blocks get N(0,1) bf16 values, all others the NaN sentinel.
     Values are drawn on the device in chunks of blocks."""
     import torch
@@ -253,6 +302,16 @@ def fill_pool_torch(wl, dev_pool, host_pool=None, chunk_blocks=256):
             sel = host_used[i:i + chunk_blocks]
             vals = torch.randn((len(sel), be), generator=genh, device=device, dtype=torch.float32)
             hv[torch.from_numpy(sel)] = vals.to(torch.bfloat16).view(torch.int16).cpu()
+    if wl.n_rc_blocks:
+        assert rc_pool is not None
+        rv = rc_pool.view(torch.int16).view(wl.n_rc_blocks, be)
+        rv.fill_(BF16_NAN_SENTINEL)
+        rc_used = np.nonzero(used[wl.rc_first_id:])[0]
+        genr = _torch_gen(wl, "pool-rc", device)
+        for i in range(0, len(rc_used), chunk_blocks):
+            idx = torch.from_numpy(rc_used[i:i + chunk_blocks]).to(device)
+            vals = torch.randn((len(idx), be), generator=genr, device=device, dtype=torch.float32)
+            rv.index_copy_(0, idx, vals.to(torch.bfloat16).view(torch.int16))
 
 
 def layer_inputs_torch(wl, layer, device, q_scale=1.0):

@@ -1,7 +1,10 @@
 """GPU parity of every C-ABI call against the oracle, element by element, on
 seeded inputs small enough for the dense oracle: several key tiles and query
 tiles with ragged tails, head groups 1/4/5/8, head_dim 64/128, empty prefix,
-a batch with an empty new turn, split-key work, and a half host-pinned pool.
+a batch with an empty new turn, split-key work, a half host-pinned pool, and
+tables whose leading blocks sit in the regular-cache tier (read in place by
+attention; their active-buffer rows hold NaN patterns the kernel must not
+read).
 
 Fetch, append and store are compared byte for byte; attention to
 |gpu - oracle| <= 2e-2 + 1e-2 |oracle| on every element plus a relative-L2
@@ -32,11 +35,18 @@ def _case(name):
         "varlen_empty_turn": lambda: sw(108, [40, 77], [0, 33], 1, 8, 2, 128),
         "host_tier": lambda: sw(106, [200, 77], [20, 31], 2, 8, 2, 128, host_fraction=0.5),
         "g8_d64": lambda: sw(107, [64], [16], 1, 64, 8, 64),
+        # regular-cache tier: leading full prefix blocks read in place
+        "rc_varlen": lambda: sw(109, [1000, 40, 0, 300, 16], [30, 17, 50, 1, 5], 2, 16, 4, 64,
+                                rc_fraction=0.6),
+        "rc_split_d128": lambda: sw(110, [5000], [40], 1, 8, 2, 128, rc_fraction=0.5),
+        "rc_whole_prefix": lambda: sw(111, [256, 512], [64, 3], 1, 32, 8, 128, rc_fraction=1.0),
+        "rc_host": lambda: sw(112, [200, 77], [20, 31], 2, 8, 2, 128, host_fraction=0.5, rc_fraction=0.5),
     }[name]()
 
 
 CASES = ["cfg1", "g4_d128_ragged", "g5_d128", "g1_d64_P0", "g4_split_long", "varlen_batch",
-         "varlen_empty_turn", "host_tier", "g8_d64"]
+         "varlen_empty_turn", "host_tier", "g8_d64", "rc_varlen", "rc_split_d128", "rc_whole_prefix",
+         "rc_host"]
 
 
 def _oracle_layer(wl, pool_u16, layer, q, kn, vn):
@@ -56,6 +66,11 @@ def _prefix_rows(wl):
     return rows
 
 
+def _rc_rows(wl):
+    return ok.regular_cache_rows(wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, wl.block_size,
+                                 wl.rc_first_id)
+
+
 @pytest.mark.parametrize("name", CASES)
 @pytest.mark.parametrize("q_scale", [1.0, 8.0], ids=["flat", "peaky"])
 def test_layer_path_matches_oracle(name, q_scale):
@@ -73,21 +88,26 @@ def test_layer_path_matches_oracle(name, q_scale):
             sc.sc_fetch_layer_kv(dp.handle, dp.table, layer, act, stream)
             torch.cuda.synchronize()
             k_act, v_act, k_full, v_full, o_ref, lse_ref = _oracle_layer(wl, pool_u16, layer, q, kn, vn)
-            pre = _prefix_rows(wl)
+            rcr = _rc_rows(wl)
+            pre = _prefix_rows(wl) & ~rcr
             kg, vg = to_u16(k), to_u16(v)
-            # fetch: prefix rows bit-exact, other rows untouched
+            # fetch: prefix rows outside the regular cache bit-exact, other
+            # rows untouched (regular-cache rows keep the NaN fill, so
+            # attention below fails if it reads them from the slot)
             assert np.array_equal(kg[pre], k_act[pre]), f"{name} layer {layer}: K fetch"
             assert np.array_equal(vg[pre], v_act[pre]), f"{name} layer {layer}: V fetch"
             assert np.all(kg[~pre] == 0xFFFF) and np.all(vg[~pre] == 0xFFFF)
             sc.sc_append_new_kv(dp.handle, dp.table, knd.data_ptr(), vnd.data_ptr(), act, stream)
             torch.cuda.synchronize()
-            assert np.array_equal(to_u16(k), k_full), f"{name} layer {layer}: K append"
-            assert np.array_equal(to_u16(v), v_full), f"{name} layer {layer}: V append"
+            kg, vg = to_u16(k), to_u16(v)
+            assert np.array_equal(kg[~rcr], k_full[~rcr]), f"{name} layer {layer}: K append"
+            assert np.array_equal(vg[~rcr], v_full[~rcr]), f"{name} layer {layer}: V append"
+            assert np.all(kg[rcr] == 0xFFFF) and np.all(vg[rcr] == 0xFFFF)
 
             out = torch.full((wl.total_q, wl.n_q_heads, wl.head_dim), float("nan"),
                              dtype=torch.bfloat16, device="cuda")
             lse = torch.full((wl.n_q_heads, max(1, wl.total_q)), float("nan"), device="cuda")
-            sc.sc_prefill_attn_varlen(dp.handle, dp.table, qd.data_ptr(), act, wl.n_q_heads,
+            sc.sc_prefill_attn_varlen(dp.handle, dp.table, layer, qd.data_ptr(), act, wl.n_q_heads,
                                       out.data_ptr(), lse.data_ptr(), 0.0, stream)
             torch.cuda.synchronize()
             compare_attention(to_u16(out), o_ref, f"{name} layer {layer} varlen")
@@ -97,7 +117,7 @@ def test_layer_path_matches_oracle(name, q_scale):
             # of its exact value, so ln l is off by at most about 2^-9 plus
             # fp32 accumulation: 2^-8 bounds it.
             np.testing.assert_allclose(lse_g, lse_ref, atol=2.0 ** -8, rtol=1e-4)
-            if wl.batch == 1:
+            if wl.batch == 1 and not wl.n_rc_blocks:
                 out1 = torch.empty_like(out)
                 lse1 = torch.empty_like(lse)
                 sc.sc_prefill_attn(qd.data_ptr(), k.data_ptr(), v.data_ptr(), int(wl.prefix_len[0]),
@@ -109,7 +129,7 @@ def test_layer_path_matches_oracle(name, q_scale):
         dp.close()
 
 
-@pytest.mark.parametrize("name", ["cfg1", "host_tier", "varlen_batch"])
+@pytest.mark.parametrize("name", ["cfg1", "host_tier", "varlen_batch", "rc_host"])
 def test_store_matches_oracle(name):
     sc = require_gpu()
     import torch
@@ -139,7 +159,8 @@ def test_store_matches_oracle(name):
                 torch.cuda.synchronize()
                 kr, vr = ok.gather_layer(expect, wl2.block_ids, wl2.cu_blocks, wl2.prefix_len,
                                          wl2.new_len, layer)
-                assert np.array_equal(to_u16(k), kr) and np.array_equal(to_u16(v), vr)
+                f = ~_rc_rows(wl2)
+                assert np.array_equal(to_u16(k)[f], kr[f]) and np.array_equal(to_u16(v)[f], vr[f])
         finally:
             sc.sc_table_destroy(t2)
     finally:
@@ -167,14 +188,17 @@ def test_single_visible_key_returns_its_value_row_exactly():
 
 
 @pytest.mark.parametrize("mode", ["overlap", "serial"])
-@pytest.mark.parametrize("name", ["stack_g4", "stack_varlen_host"])
+@pytest.mark.parametrize("name", ["stack_g4", "stack_varlen_host", "stack_rc"])
 def test_layer_stack_matches_oracle(name, mode):
     sc = require_gpu()
     import torch
     if name == "stack_g4":
         wl = W.small_workload(201, [300], [70], 4, 32, 8, 128)
-    else:
+    elif name == "stack_varlen_host":
         wl = W.small_workload(202, [150, 0, 500], [20, 40, 7], 3, 8, 2, 64, host_fraction=0.5)
+    else:
+        wl = W.small_workload(203, [300, 700, 40], [70, 9, 33], 3, 32, 8, 128, host_fraction=0.3,
+                              rc_fraction=0.5)
     pool_u16 = W.pool_numpy(wl)
     dp = DevicePool(sc, wl, pool_u16)
     try:
@@ -215,6 +239,9 @@ def test_capacity_and_layer_errors():
         act = sc.active(k.data_ptr(), k.data_ptr(), wl.total_kv)
         with pytest.raises(sc.SwiftCacheError) as e:
             sc.sc_fetch_layer_kv(dp.handle, dp.table, 1, act)
+        assert e.value.status == sc.SC_ERR_RANGE
+        with pytest.raises(sc.SwiftCacheError) as e:
+            sc.sc_prefill_attn_varlen(dp.handle, dp.table, 1, k.data_ptr(), act, wl.n_q_heads, k.data_ptr())
         assert e.value.status == sc.SC_ERR_RANGE
     finally:
         dp.close()

@@ -88,6 +88,42 @@ def test_table_validation(sc, ids, cu, P, N, status):
         sc.sc_pool_destroy(p)
 
 
+def test_regular_cache_pool_validation(sc):
+    with pytest.raises(sc.SwiftCacheError) as e:      # paging needs a power-of-two block
+        sc.sc_pool_create(2, 2, 64, 24, 8, 0, 0, FAKE_BASE, 0, 4, FAKE_BASE)
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED
+    with pytest.raises(sc.SwiftCacheError) as e:      # smaller than a paged row group
+        sc.sc_pool_create(2, 2, 64, 8, 8, 0, 0, FAKE_BASE, 0, 4, FAKE_BASE)
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_pool_create(2, 2, 64, 16, 8, 0, 0, FAKE_BASE, 0, -1, FAKE_BASE)
+    assert e.value.status == sc.SC_ERR_INVALID
+    p = sc.sc_pool_create(2, 2, 64, 16, 0, 0, 0, 0, 0, 4, FAKE_BASE)   # a regular cache alone
+    try:
+        lay = sc.sc_pool_layout_get(p)
+        assert (lay.rc_base, lay.n_rc_blocks, lay.n_device_blocks) == (FAKE_BASE, 4, 0)
+    finally:
+        sc.sc_pool_destroy(p)
+
+
+# pool of 8 donor blocks (ids 0..7) and 4 regular-cache blocks (ids 8..11), B = 16
+@pytest.mark.parametrize("ids,cu,P,N,status", [
+    ([0, 8, 1], [0, 3], [33], [2], "INVALID"),       # regular-cache block after a donor block
+    ([8, 9, 10], [0, 3], [33], [2], "INVALID"),      # third block holds new-turn rows
+    ([8, 9, 10], [0, 3], [40], [0], "INVALID"),      # third block only partly filled
+    ([8, 12, 0], [0, 3], [33], [0], "RANGE"),        # id past the regular cache
+    ([8, 8, 0], [0, 3], [33], [0], "INVALID"),       # duplicate regular-cache id
+])
+def test_regular_cache_table_validation(sc, ids, cu, P, N, status):
+    p = sc.sc_pool_create(2, 2, 64, 16, 8, 0, 0, FAKE_BASE, 0, 4, FAKE_BASE)
+    try:
+        with pytest.raises(sc.SwiftCacheError) as e:
+            sc.sc_table_create(p, ids, cu, P, N)
+        assert e.value.status == getattr(sc, "SC_ERR_" + status)
+    finally:
+        sc.sc_pool_destroy(p)
+
+
 def test_attention_argument_validation(sc):
     with pytest.raises(sc.SwiftCacheError) as e:
         sc.sc_prefill_attn(1, 1, 1, 4, 4, 12, 8, 128, 1)
@@ -108,8 +144,9 @@ KEY_TILE = 32
 ROWS = 256
 
 
-def _check_plan(sc, P, N, hq, hkv, target):
-    items, splits = sc.sc_attn_plan_query(P, N, hq, hkv, target)
+def _check_plan(sc, P, N, hq, hkv, target, rc=None):
+    items, splits = sc.sc_attn_plan_query(P, N, hq, hkv, target, rc_keys=rc)
+    rc = [0] * len(P) if rc is None else rc
     group = hq // hkv
     rows_q = ROWS // group
     assert len(items) % 8 == 0
@@ -126,8 +163,15 @@ def _check_plan(sc, P, N, hq, hkv, target):
     # per query tile, the splits partition [0, P + q0 + nq)
     tiles = {}
     for it in real:
-        seq, kvh, q0, nq, kb, ke, s, _ = (int(x) for x in it)
-        assert kb % KEY_TILE == 0 and ke >= kb
+        seq, kvh, q0, nq, kb, ke, s, paged = (int(x) for x in it)
+        r = rc[seq]
+        # regular-cache items cover [0, r), the others [r, ...): tiles start
+        # on the key-tile grid of their own range
+        if paged:
+            assert ke <= r and kb % KEY_TILE == 0
+        else:
+            assert kb >= r and (kb - r) % KEY_TILE == 0
+        assert ke >= kb
         tiles.setdefault((seq, kvh, q0, nq), []).append((s, kb, ke))
     expect = set()
     for b, (p, n) in enumerate(zip(P, N)):
@@ -159,6 +203,30 @@ def _check_plan(sc, P, N, hq, hkv, target):
 ])
 def test_plan_covers_every_row_and_key_once(sc, P, N, hq, hkv, target):
     _check_plan(sc, P, N, hq, hkv, target)
+
+
+@pytest.mark.parametrize("P,N,rc,hq,hkv", [
+    ([8192], [512], [4096], 32, 8),
+    ([8192], [512], [8192], 32, 8),           # the whole prefix in the regular cache
+    ([5000], [40], [16], 8, 2),               # one block, off the key-tile grid
+    ([33, 0, 1000, 17], [5, 64, 1, 200], [32, 0, 496, 16], 16, 4),
+    ([131072], [2048], [65536], 32, 8),
+])
+def test_plan_with_regular_cache(sc, P, N, rc, hq, hkv):
+    items, splits = _check_plan(sc, P, N, hq, hkv, 768, rc)
+    for b, r in enumerate(rc):
+        mine = items[items[:, 0] == b]
+        if len(mine) == 0:
+            continue
+        assert bool(np.any(mine[:, 7] == 1)) == (r > 0)
+        if r > 0:
+            assert splits[b] >= 2               # partials over both ranges are merged
+
+
+def test_plan_rejects_regular_cache_beyond_prefix(sc):
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_attn_plan_query([100], [10], 8, 8, 0, rc_keys=[112])
+    assert e.value.status == sc.SC_ERR_INVALID
 
 
 def test_plan_random_batches(sc):

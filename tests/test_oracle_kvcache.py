@@ -139,3 +139,26 @@ def test_planted_kv_swap_is_caught():
     swapped = pool[:, :, ::-1].copy()
     k, _ = ok.gather_layer(swapped, ids, cu, prefix, new, 0)
     assert not np.array_equal(k[:8], dense[0][0, 0, :8])
+
+
+def test_regular_cache_rows_by_counting():
+    """Rows of leading regular-cache blocks, counted block by block: B rows
+    per leading regular-cache block at the start of each sequence, none
+    elsewhere; the fetched rows are the remaining prefix rows."""
+    bs, rc0 = 4, 100
+    prefix, new = [12, 9, 0, 8], [3, 2, 5, 0]
+    ids = np.array([100, 101, 7,  102, 3, 4,  5, 6,  103, 104], dtype=np.int32)
+    cu = np.array([0, 3, 6, 8, 10], dtype=np.int32)
+    rows = ok.regular_cache_rows(ids, cu, prefix, new, bs, rc0)
+    _, cu_k = ok.seq_offsets(prefix, new)
+    expect = np.zeros(int(cu_k[-1]), dtype=bool)
+    expect[0:8] = True                       # sequence 0: two blocks
+    expect[15:19] = True                     # sequence 1: one block
+    expect[31:39] = True                     # sequence 3: its whole prefix
+    assert np.array_equal(rows, expect)
+    assert rows.sum() == bs * 5
+    # a regular-cache block after a donor block, or one that new tokens share
+    with pytest.raises(AssertionError):
+        ok.regular_cache_rows(np.array([7, 100, 1], dtype=np.int32), np.array([0, 3]), [9], [2], bs, rc0)
+    with pytest.raises(AssertionError):
+        ok.regular_cache_rows(np.array([100, 101, 102], dtype=np.int32), np.array([0, 3]), [9], [2], bs, rc0)
