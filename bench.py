@@ -75,7 +75,7 @@ def cpu_baseline(wl, dp, inputs, budget_s=15.0):
         t0 = time.perf_counter()
         ka, va = ok.gather_layer(pool_l, wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, 0)
         kf, vf = ok.append_new(ka, va, kn, vn, wl.prefix_len, wl.new_len)
-        oa.attention(oa.bf16_bits_to_f64(q), oa.bf16_bits_to_f64(kf), oa.bf16_bits_to_f64(vf),
+        oa.attention(oa.bits_to_f64(q, wl.dtype), oa.bits_to_f64(kf, wl.dtype), oa.bits_to_f64(vf, wl.dtype),
                      wl.prefix_len, wl.new_len)
         t_layers.append(time.perf_counter() - t0)
         if sum(t_layers) >= budget_s:
@@ -96,6 +96,8 @@ def main():
     ap.add_argument("--rc-fraction", type=float, default=0.0,
                     help="put this fraction of each sequence's full prefix blocks in the regular "
                          "cache (read in place by attention, never fetched)")
+    ap.add_argument("--dtype", choices=["bf16", "f16"], default="bf16",
+                    help="element type of the pool, q, K, V and outputs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["attention", "fetch", "copy"], default=None,
                     help="run only one kernel of the path, --steps times over every layer "
@@ -114,14 +116,15 @@ def main():
     sc.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
 
-    wl = W.config(args.config, rc_fraction=args.rc_fraction)
+    wl = W.config(args.config, rc_fraction=args.rc_fraction, dtype=args.dtype)
+    td = W.torch_dtype(wl)
     dp = DevicePool(sc, wl, fill="torch")
     L = wl.n_layers
     inputs = [W.layer_inputs_torch(wl, l, "cuda") for l in range(L)]
-    outs = [torch.empty((wl.total_q, wl.n_q_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+    outs = [torch.empty((wl.total_q, wl.n_q_heads, wl.head_dim), dtype=td, device="cuda")
             for _ in range(L)]
-    slot_t = [(torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda"),
-               torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda"))
+    slot_t = [(torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=td, device="cuda"),
+               torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=td, device="cuda"))
               for _ in range(2)]
     slots = [sc.active(k.data_ptr(), v.data_ptr(), wl.total_kv) for k, v in slot_t]
     compute = torch.cuda.current_stream()
@@ -244,7 +247,7 @@ def main():
 
     result = {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
               "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 3),
-              "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+              "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
               "data": "synthetic",
               "config": {"workload": wl.name, "layers": L, "q_heads": wl.n_q_heads,
                          "kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,

@@ -53,6 +53,16 @@ typedef enum {
   SC_ERR_UNSUPPORTED = -5   /* shape the kernels are not built for           */
 } sc_status;
 
+/* Element type of every K/V, q, k_new, v_new and output element of a pool
+ * (and of the active buffers used with it): bf16, or IEEE fp16 as the paper
+ * serves its models (§5).  Attention accumulates in fp32 for both; the
+ * probabilities of the PV product and the output are rounded to the same
+ * type (round to nearest even). */
+typedef enum {
+  SC_DTYPE_BF16 = 0,
+  SC_DTYPE_F16 = 1
+} sc_dtype;
+
 typedef struct sc_pool sc_pool;     /* opaque, library-owned */
 typedef struct sc_table sc_table;   /* opaque, library-owned */
 
@@ -90,7 +100,7 @@ typedef struct {
   int64_t n_device_blocks;
   int64_t n_host_blocks;
   int32_t device;            /* HIP device ordinal */
-  int32_t reserved;          /* must be 0 */
+  int32_t dtype;             /* sc_dtype (0 = bf16) */
   void *device_base;         /* optional caller-owned HBM tier */
   void *host_base;           /* optional caller-owned pinned host tier */
   int64_t n_rc_blocks;       /* regular-cache blocks (0: none) */
@@ -108,10 +118,12 @@ typedef struct {
   int64_t device_blocks_lent;/* HBM blocks currently usable (sc_pool_resize), <= n_device_blocks */
   void *rc_base;             /* regular-cache tier base (device address), or NULL */
   int64_t n_rc_blocks;
+  int32_t dtype;             /* sc_dtype */
 } sc_pool_layout;
 
 /* Active-layer buffer (the layer stream cache slot, §3.2): caller-owned
- * device arrays K and V, each [capacity_tokens][n_kv_heads][head_dim] bf16. */
+ * device arrays K and V, each [capacity_tokens][n_kv_heads][head_dim] of the
+ * pool's element type. */
 typedef struct {
   void *k;
   void *v;
@@ -119,7 +131,7 @@ typedef struct {
 } sc_active;
 
 /* Create a pool (see sc_pool_desc).  Errors: SC_ERR_INVALID for a null
- * argument, non-positive sizes or reserved != 0; SC_ERR_UNSUPPORTED for a
+ * argument, non-positive sizes or an unknown dtype; SC_ERR_UNSUPPORTED for a
  * head_dim other than 64/128; SC_ERR_OOM when an allocation fails. */
 sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out);
 
@@ -178,7 +190,8 @@ sc_status sc_fetch_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
 /*
  * Append the new turn (§3.2: new entries are written into the active
  * buffer): rows cu_q[b] + i of k_new / v_new ([sum N][n_kv_heads][head_dim]
- * bf16, device) go to rows cu_k[b] + P_b + i of dst->k / dst->v.
+ * the pool's element type, device) go to rows cu_k[b] + P_b + i of dst->k /
+ * dst->v.
  * Errors: as sc_fetch_layer_kv.
  */
 sc_status sc_append_new_kv(sc_pool *pool, const sc_table *table, const void *k_new,
@@ -204,6 +217,15 @@ sc_status sc_prefill_attn(const void *q, const void *k_active, const void *v_act
                           int32_t prefix_len, int32_t new_len, int32_t n_q_heads,
                           int32_t n_kv_heads, int32_t head_dim, float scale, void *out,
                           float *lse, void *stream);
+
+/* The same with IEEE fp16 q, K, V and out (the paper's serving precision,
+ * §5): fp16 MFMA products, fp32 accumulation and softmax, probabilities
+ * rounded to fp16 for the PV product, output rounded to nearest even.
+ * Arguments and errors as sc_prefill_attn. */
+sc_status sc_prefill_attn_f16(const void *q, const void *k_active, const void *v_active,
+                              int32_t prefix_len, int32_t new_len, int32_t n_q_heads,
+                              int32_t n_kv_heads, int32_t head_dim, float scale, void *out,
+                              float *lse, void *stream);
 
 /* The same attention for every sequence of a table (packed varlen layout)
  * at layer `layer`: q, out [sum N][n_q_heads][head_dim]; kv = the active

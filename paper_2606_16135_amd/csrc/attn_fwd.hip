@@ -16,6 +16,9 @@
 // in the last-arriving workgroup would need device-scope fences, whose L2
 // write-back / invalidate stalls the other workgroups streaming K/V.
 //
+// q, K, V and out are bf16 or IEEE fp16 (Elem<DT> below); everything else
+// is the same for both types.
+//
 // Per key tile of 32 and per wave (32 rows):
 //   S^T (32 keys x 32 rows) = K_tile . Q^T         MFMA 32x32x16 bf16, fp32 out
 //   P = exp2(c S^T - m),  c = scale * log2(e)      online softmax, log2 domain
@@ -61,6 +64,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -71,10 +76,6 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 constexpr int kThreads = 512;            // 8 waves, 2 per SIMD
 constexpr int KT = kAttnKeyTile;
-// A lane's tile sum above this sends the wave through settle_max.  Every
-// probability is then below 2^20, so O and l stay far from fp32 overflow
-// for any sequence length; rows never pay for a max they do not need.
-constexpr float kSumLimit = 1048576.0f;
 // Polls of the ready flag before a workgroup gives up (about a second).
 constexpr int kReadySpinLimit = 1 << 22;
 static_assert(kAttnRows == 8 * 32, "eight waves of 32 rows");
@@ -100,19 +101,54 @@ struct Geo {
   static_assert(kChunksPerThread * kThreads == 2 * kTileChunks, "tile split");
 };
 
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 x) { return __builtin_bit_cast(bf16x8, x); }
+// Element type of q, K, V, the probabilities of the PV product and the
+// output: bf16 or IEEE fp16 (the paper's serving precision, §5).  Operands
+// travel as raw 16-bit patterns; only the MFMA, the packing of fp32 values
+// (round to nearest even) and the pair sum depend on the type.
+template <int DT>
+struct Elem;
 
-// Two floats to packed bf16 (round to nearest even), one v_cvt_pk_bf16_f32.
-__device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-  const bf16x2 p = {(__bf16)a, (__bf16)b};
-  return __builtin_bit_cast(uint32_t, p);
-}
+template <>
+struct Elem<SC_DTYPE_BF16> {
+  // A lane's tile sum above this sends the wave through settle_max.  Every
+  // probability is then below 2^20, so O and l stay far from fp32 overflow
+  // for any sequence length; rows never pay for a max they do not need.
+  static constexpr float kSumLimit = 1048576.0f;
+  static __device__ __forceinline__ f32x16 mfma(u32x4 a, u32x4 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                   0, 0, 0);
+  }
+  // Two floats to packed bf16, one v_cvt_pk_bf16_f32.
+  static __device__ __forceinline__ uint32_t pack(float a, float b) {
+    const bf16x2 p = {(__bf16)a, (__bf16)b};
+    return __builtin_bit_cast(uint32_t, p);
+  }
+  // Sum of the two halves of `p` added to `acc` (v_dot2c_f32_bf16 with 1, 1).
+  static __device__ __forceinline__ float add_pair(uint32_t p, float acc) {
+    const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p), one, acc, false);
+  }
+};
 
-// Sum of the two bf16 halves of `p` added to `acc` (v_dot2c_f32_bf16 with 1, 1).
-__device__ __forceinline__ float add_pair(uint32_t p, float acc) {
-  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p), one, acc, false);
-}
+template <>
+struct Elem<SC_DTYPE_F16> {
+  // As for bf16, but fp16 probabilities must also stay below its largest
+  // finite value (65504): with a tile sum of at most 2^15 every one does.
+  // A probability that overflowed to inf fails the same test.
+  static constexpr float kSumLimit = 32768.0f;
+  static __device__ __forceinline__ f32x16 mfma(u32x4 a, u32x4 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                  0, 0);
+  }
+  static __device__ __forceinline__ uint32_t pack(float a, float b) {
+    const f16x2 p = {(_Float16)a, (_Float16)b};
+    return __builtin_bit_cast(uint32_t, p);
+  }
+  static __device__ __forceinline__ float add_pair(uint32_t p, float acc) {
+    const f16x2 one = {(_Float16)1.0f, (_Float16)1.0f};
+    return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, p), one, acc, false);
+  }
+};
 
 // Max with the same lane of the other 32-lane half of the wave.
 __device__ __forceinline__ float max_with_other_half(float x) {
@@ -130,22 +166,21 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // S^T(tile) = K_tile . Q^T: D / 16 dependent MFMAs.
-template <int D>
-__device__ __forceinline__ void qk_tile(const uint16_t *sk, const bf16x8 (&qf)[D / 16], f32x16 &s, int lane) {
+template <int D, int DT>
+__device__ __forceinline__ void qk_tile(const uint16_t *sk, const u32x4 (&qf)[D / 16], f32x16 &s, int lane) {
   using G_ = Geo<D>;
 #pragma unroll
   for (int r = 0; r < 16; ++r) s[r] = 0.f;
   const uint16_t *krow = sk + (lane & 31) * G_::kLdsK + 8 * (lane >> 5);
 #pragma unroll
   for (int k = 0; k < D / 16; ++k)
-    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(*reinterpret_cast<const u32x4 *>(krow + 16 * k)),
-                                                qf[k], s, 0, 0, 0);
+    s = Elem<DT>::mfma(*reinterpret_cast<const u32x4 *>(krow + 16 * k), qf[k], s);
 }
 
 // O^T += V^T . P^T.  MFMA step t covers keys 16 t + [0, 16); k-slot e of a
 // lane in half `half` holds key 16 t + 4 half + (e < 4 ? e : e + 4), which
 // is accumulator element 8 t + e of S^T, i.e. pf[t] element e.
-template <int D>
+template <int D, int DT>
 __device__ __forceinline__ void pv_tile(const uint16_t *sv, const u32x4 (&pf)[2], f32x16 (&oacc)[D / 32],
                                         int lane) {
   using G_ = Geo<D>;
@@ -165,7 +200,7 @@ __device__ __forceinline__ void pv_tile(const uint16_t *sv, const u32x4 (&pf)[2]
       vw[1] = __builtin_bit_cast(u32x2, lo)[1];
       vw[2] = __builtin_bit_cast(u32x2, hi)[0];
       vw[3] = __builtin_bit_cast(u32x2, hi)[1];
-      oacc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vw), as_bf16x8(pf[t]), oacc[c], 0, 0, 0);
+      oacc[c] = Elem<DT>::mfma(vw, pf[t], oacc[c]);
     }
 }
 
@@ -189,23 +224,24 @@ __device__ __forceinline__ float tile_max(const f32x16 &s, float sl2) {
 
 // p = exp2(sl2 * s - m) for this lane's 16 keys, packed to bf16, and the sum
 // of the packed values (the weights the PV product uses).
+template <int DT>
 __device__ __forceinline__ float softmax_tile(const f32x16 &s, u32x4 (&pf)[2], float sl2, float m) {
   float r2[2] = {0.f, 0.f};
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int e = 0; e < 8; e += 2) {
-      const uint32_t w = pack_bf16(__builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * t + e], sl2, -m)),
+      const uint32_t w = Elem<DT>::pack(__builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * t + e], sl2, -m)),
                                    __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * t + e + 1], sl2, -m)));
       pf[t][e >> 1] = w;
-      r2[t] = add_pair(w, r2[t]);
+      r2[t] = Elem<DT>::add_pair(w, r2[t]);
     }
   return r2[0] + r2[1];
 }
 
 template <int D>
 struct WaveState {
-  bf16x8 qf[D / 16];
+  u32x4 qf[D / 16];   // raw 16-bit patterns
   f32x16 oacc[D / 32];
   f32x16 s[2];        // raw scores of the even / odd tiles
   u32x4 pf_prev[2];   // P(j-1) for the PV product
@@ -217,7 +253,7 @@ struct WaveState {
 // range: move every row's reference max to the true running max, rescale l
 // and O (O already holds PV(j-1), computed against the old reference), and
 // redo the tile's exponentials.  Returns the new tile sum.
-template <int D>
+template <int D, int DT>
 __device__ __forceinline__ float settle_max(WaveState<D> &w, const f32x16 &s, u32x4 (&pf)[2], float sl2) {
   const float m_new = fmaxf(w.m_run, tile_max(s, sl2));
   const float corr = __builtin_amdgcn_exp2f(w.m_run - m_new);
@@ -227,13 +263,13 @@ __device__ __forceinline__ float settle_max(WaveState<D> &w, const f32x16 &s, u3
   for (int c = 0; c < D / 32; ++c)
 #pragma unroll
     for (int r = 0; r < 16; ++r) w.oacc[c][r] *= corr;
-  return softmax_tile(s, pf, sl2, m_new);
+  return softmax_tile<DT>(s, pf, sl2, m_new);
 }
 
 // One work item.  kPaged: its keys are read in place from the regular
 // cache; the two kinds of item are separate copies of the whole body so that
 // each is register-allocated on its own.
-template <int D, bool kPaged>
+template <int D, int DT, bool kPaged>
 __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi, uint16_t *smem) {
   using G_ = Geo<D>;
   constexpr int NCH = G_::kChunksPerThread;
@@ -261,7 +297,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
     for (int k = 0; k < D / 16; ++k) {
       u32x4 x = {0u, 0u, 0u, 0u};
       if (valid) x = qp[2 * k + half];
-      w.qf[k] = as_bf16x8(x);
+      w.qf[k] = x;
     }
   }
   const float sl2 = a.scale_log2;   // scale * log2(e)
@@ -411,7 +447,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
     stage_store(true, false, 0, 0);
     stage_load(1, -1);
     lds_barrier();
-    qk_tile<D>(slot_k(0), w.qf, w.s[0], lane);
+    qk_tile<D, DT>(slot_k(0), w.qf, w.s[0], lane);
     stage_store(true, false, 1, 0);
     stage_load(2, 0);
     lds_barrier();
@@ -428,15 +464,15 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
       __builtin_assume(j >= 0);
       f32x16 &sc = w.s[PAR];
       u32x4 pf[2];
-      if (kQk) qk_tile<D>(slot_k(PAR ^ 1), w.qf, w.s[PAR ^ 1], lane);
-      if (kPv) pv_tile<D>(slot_v(PAR ^ 1), w.pf_prev, w.oacc, lane);
+      if (kQk) qk_tile<D, DT>(slot_k(PAR ^ 1), w.qf, w.s[PAR ^ 1], lane);
+      if (kPv) pv_tile<D, DT>(slot_v(PAR ^ 1), w.pf_prev, w.oacc, lane);
       if (kMask) apply_mask(sc, lim_of(j));
       if (kFirst) {
         const float tm = tile_max(sc, sl2);
         w.m_run = tm > -INFINITY ? tm : 0.f;
       }
-      float rs = softmax_tile(sc, pf, sl2, w.m_run);
-      if (!kFirst && __builtin_amdgcn_ballot_w64(!(rs <= kSumLimit))) rs = settle_max<D>(w, sc, pf, sl2);
+      float rs = softmax_tile<DT>(sc, pf, sl2, w.m_run);
+      if (!kFirst && __builtin_amdgcn_ballot_w64(!(rs <= Elem<DT>::kSumLimit))) rs = settle_max<D, DT>(w, sc, pf, sl2);
       w.l_run += rs;
       stage_store(true, true, PAR, PAR);
       stage_load(j + 3, j + 1);
@@ -467,7 +503,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
     if (n >= 2) {
       if ((n - 1) & 1) iterate(P1(), T(), F(), T(), F(), n - 1); else iterate(P0(), T(), F(), T(), F(), n - 1);
     }
-    pv_tile<D>(slot_v((n - 1) & 1), w.pf_prev, w.oacc, lane);
+    pv_tile<D, DT>(slot_v((n - 1) & 1), w.pf_prev, w.oacc, lane);
   }
 
   // Combine the two halves' denominators and normalise.
@@ -484,8 +520,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
       for (int g4 = 0; g4 < 4; ++g4) {
         const int dim = 32 * c + 8 * g4 + 4 * half;
         u32x2 pk;
-        pk[0] = pack_bf16(w.oacc[c][4 * g4 + 0] * inv, w.oacc[c][4 * g4 + 1] * inv);
-        pk[1] = pack_bf16(w.oacc[c][4 * g4 + 2] * inv, w.oacc[c][4 * g4 + 3] * inv);
+        pk[0] = Elem<DT>::pack(w.oacc[c][4 * g4 + 0] * inv, w.oacc[c][4 * g4 + 1] * inv);
+        pk[1] = Elem<DT>::pack(w.oacc[c][4 * g4 + 2] * inv, w.oacc[c][4 * g4 + 3] * inv);
         *reinterpret_cast<u32x2 *>(orow + dim) = pk;
       }
     if (a.lse != nullptr && half == 0) a.lse[(int64_t)h * a.total_q + sd.cu_q + qpos] = lse_val;
@@ -510,21 +546,21 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
   if (half == 0) a.part_lse[prow] = lse_val;
 }
 
-template <int D>
+template <int D, int DT>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t smem[Geo<D>::kSmem];
   const WorkItem wi = a.items[blockIdx.x];
   if (wi.seq < 0) return;
   if (wi.paged)
-    attn_item<D, true>(a, wi, smem);
+    attn_item<D, DT, true>(a, wi, smem);
   else
-    attn_item<D, false>(a, wi, smem);
+    attn_item<D, DT, false>(a, wi, smem);
 }
 
 // Split-key merge: D / 8 lanes per (token, head) row, 8 dims per lane.
 // Weights exp(lse_s - max) over the splits, weighted sum of the partials;
 // the loads of several splits are issued before they are used.
-template <int D>
+template <int D, int DT>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   constexpr int LPR = D / 8;
   constexpr int RPB = 256 / LPR;
@@ -577,7 +613,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   const float winv = wsum > 0.f ? 1.f / wsum : 0.f;
   u32x4 pk;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) pk[e] = pack_bf16(acc[2 * e] * winv, acc[2 * e + 1] * winv);
+  for (int e = 0; e < 4; ++e) pk[e] = Elem<DT>::pack(acc[2 * e] * winv, acc[2 * e + 1] * winv);
   *reinterpret_cast<u32x4 *>(a.out + row * D + sub * 8) = pk;
   if (a.lse != nullptr && sub == 0)
     a.lse[(int64_t)h * a.total_q + token] = wsum > 0.f ? mx + __logf(wsum) : -INFINITY;
@@ -587,18 +623,33 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 
 hipError_t launch_attn_fwd(const AttnArgs &a, int head_dim, int n_items, hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;
-  if (head_dim == 128)
-    hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(n_items), dim3(kThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(n_items), dim3(kThreads), 0, stream, a);
+  const dim3 grid(n_items), block(kThreads);
+  if (head_dim == 128) {
+    if (a.dtype == SC_DTYPE_F16)
+      hipLaunchKernelGGL((attn_fwd_kernel<128, SC_DTYPE_F16>), grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<128, SC_DTYPE_BF16>), grid, block, 0, stream, a);
+  } else {
+    if (a.dtype == SC_DTYPE_F16)
+      hipLaunchKernelGGL((attn_fwd_kernel<64, SC_DTYPE_F16>), grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<64, SC_DTYPE_BF16>), grid, block, 0, stream, a);
+  }
   return hipGetLastError();
 }
 
 int attn_fwd_vgprs(int head_dim) {
-  hipFuncAttributes at{};
-  const void *f = head_dim == 128 ? reinterpret_cast<const void *>(&attn_fwd_kernel<128>)
-                                  : reinterpret_cast<const void *>(&attn_fwd_kernel<64>);
-  return hipFuncGetAttributes(&at, f) == hipSuccess ? at.numRegs : -1;
+  // The largest of the two element types' kernels for this head_dim.
+  int m = -1;
+  for (const void *f : {head_dim == 128 ? reinterpret_cast<const void *>(&attn_fwd_kernel<128, SC_DTYPE_BF16>)
+                                        : reinterpret_cast<const void *>(&attn_fwd_kernel<64, SC_DTYPE_BF16>),
+                        head_dim == 128 ? reinterpret_cast<const void *>(&attn_fwd_kernel<128, SC_DTYPE_F16>)
+                                        : reinterpret_cast<const void *>(&attn_fwd_kernel<64, SC_DTYPE_F16>)}) {
+    hipFuncAttributes at{};
+    if (hipFuncGetAttributes(&at, f) != hipSuccess) return -1;
+    m = at.numRegs > m ? at.numRegs : m;
+  }
+  return m;
 }
 
 size_t attn_fwd_lds_bytes(int head_dim) {
@@ -608,11 +659,18 @@ size_t attn_fwd_lds_bytes(int head_dim) {
 hipError_t launch_attn_merge(const AttnArgs &a, int head_dim, hipStream_t stream) {
   const int64_t rows = (int64_t)a.total_q * a.n_q_heads;
   if (rows <= 0) return hipSuccess;
-  const unsigned blocks = (unsigned)((rows * (head_dim / 8) + 255) / 256);
-  if (head_dim == 128)
-    hipLaunchKernelGGL(attn_merge_kernel<128>, dim3(blocks), dim3(256), 0, stream, a);
-  else
-    hipLaunchKernelGGL(attn_merge_kernel<64>, dim3(blocks), dim3(256), 0, stream, a);
+  const dim3 grid((unsigned)((rows * (head_dim / 8) + 255) / 256)), block(256);
+  if (head_dim == 128) {
+    if (a.dtype == SC_DTYPE_F16)
+      hipLaunchKernelGGL((attn_merge_kernel<128, SC_DTYPE_F16>), grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL((attn_merge_kernel<128, SC_DTYPE_BF16>), grid, block, 0, stream, a);
+  } else {
+    if (a.dtype == SC_DTYPE_F16)
+      hipLaunchKernelGGL((attn_merge_kernel<64, SC_DTYPE_F16>), grid, block, 0, stream, a);
+    else
+      hipLaunchKernelGGL((attn_merge_kernel<64, SC_DTYPE_BF16>), grid, block, 0, stream, a);
+  }
   return hipGetLastError();
 }
 

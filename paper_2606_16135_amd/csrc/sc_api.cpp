@@ -349,7 +349,7 @@ struct RcView {
 };
 
 sc_status run_attention(int device, const AttnPlan &plan, const void *q, const void *k, const void *v,
-                        void *out, float *lse, int hq, int hkv, int head_dim, float scale,
+                        void *out, float *lse, int hq, int hkv, int head_dim, int dtype, float scale,
                         hipStream_t stream, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
                         hipEvent_t after_fwd = nullptr, const RcView &rc = RcView()) {
   if (plan.n_items == 0) return SC_OK;
@@ -373,6 +373,7 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
   a.n_kv_heads = hkv;
   a.group = plan.group;
   a.rows_q = plan.rows_q;
+  a.dtype = dtype;
   if (!(scale > 0.f)) scale = 1.f / std::sqrt((float)head_dim);
   a.scale_log2 = scale * 1.4426950408889634f;
   if (plan.max_splits > 1) {
@@ -590,6 +591,23 @@ sc_status do_store(sc_pool *p, const sc_table *t, int layer, const void *kn, con
   return e == hipSuccess ? SC_OK : fail_hip(e, "store launch");
 }
 
+sc_status prefill_attn_single(const void *q, const void *k_active, const void *v_active, int32_t prefix_len,
+                              int32_t new_len, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, int dtype,
+                              float scale, void *out, float *lse, void *stream) {
+  if (prefix_len < 0 || new_len < 0) return fail(SC_ERR_INVALID, "negative length");
+  sc_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
+  if (st != SC_OK) return st;
+  if (new_len == 0) return SC_OK;
+  if (!q || !k_active || !v_active || !out) return fail(SC_ERR_INVALID, "null argument");
+  int device = 0;
+  SC_HIP(hipGetDevice(&device));
+  AttnPlan *plan = nullptr;
+  st = single_plan(device, prefix_len, new_len, n_q_heads, n_kv_heads, &plan);
+  if (st != SC_OK) return st;
+  return run_attention(device, *plan, q, k_active, v_active, out, lse, n_q_heads, n_kv_heads, head_dim, dtype,
+                       scale, (hipStream_t)stream);
+}
+
 }  // namespace
 }  // namespace sc
 
@@ -611,7 +629,8 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
   const sc_pool_desc &d = *desc;
   if (d.n_layers <= 0 || d.n_kv_heads <= 0 || d.block_size <= 0 || d.block_size > 256 ||
       d.n_device_blocks < 0 || d.n_host_blocks < 0 || d.n_rc_blocks < 0 ||
-      d.n_device_blocks + d.n_host_blocks + d.n_rc_blocks <= 0 || d.reserved != 0)
+      d.n_device_blocks + d.n_host_blocks + d.n_rc_blocks <= 0 ||
+      (d.dtype != SC_DTYPE_BF16 && d.dtype != SC_DTYPE_F16))
     return fail(SC_ERR_INVALID, "invalid pool description");
   if (d.head_dim != 64 && d.head_dim != 128)
     return fail(SC_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", d.head_dim);
@@ -725,6 +744,7 @@ sc_status sc_pool_layout_get(const sc_pool *pool, sc_pool_layout *out) {
   out->n_host_blocks = pool->desc.n_host_blocks;
   out->rc_base = pool->rc_base;
   out->n_rc_blocks = pool->desc.n_rc_blocks;
+  out->dtype = pool->desc.dtype;
   std::lock_guard<std::mutex> lk(const_cast<sc_pool *>(pool)->mu);
   out->device_blocks_lent = pool->dev_lent;
   return SC_OK;
@@ -985,22 +1005,21 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
   return do_store(pool, table, layer, k_new, v_new, (hipStream_t)stream);
 }
 
+
 sc_status sc_prefill_attn(const void *q, const void *k_active, const void *v_active, int32_t prefix_len,
                           int32_t new_len, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, float scale,
                           void *out, float *lse, void *stream) {
   clear_error();
-  if (prefix_len < 0 || new_len < 0) return fail(SC_ERR_INVALID, "negative length");
-  sc_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
-  if (st != SC_OK) return st;
-  if (new_len == 0) return SC_OK;
-  if (!q || !k_active || !v_active || !out) return fail(SC_ERR_INVALID, "null argument");
-  int device = 0;
-  SC_HIP(hipGetDevice(&device));
-  AttnPlan *plan = nullptr;
-  st = single_plan(device, prefix_len, new_len, n_q_heads, n_kv_heads, &plan);
-  if (st != SC_OK) return st;
-  return run_attention(device, *plan, q, k_active, v_active, out, lse, n_q_heads, n_kv_heads, head_dim,
-                       scale, (hipStream_t)stream);
+  return prefill_attn_single(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_heads, head_dim,
+                             SC_DTYPE_BF16, scale, out, lse, stream);
+}
+
+sc_status sc_prefill_attn_f16(const void *q, const void *k_active, const void *v_active, int32_t prefix_len,
+                              int32_t new_len, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim, float scale,
+                              void *out, float *lse, void *stream) {
+  clear_error();
+  return prefill_attn_single(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_heads, head_dim,
+                             SC_DTYPE_F16, scale, out, lse, stream);
 }
 
 sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, int32_t layer, const void *q,
@@ -1021,8 +1040,8 @@ sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, int32_t l
   if (st != SC_OK) return st;
   const sc_pool_desc &d = pool->desc;
   RcView rc{pool, layer, table->d_rc_ids};
-  return run_attention(d.device, *plan, q, kv->k, kv->v, out, lse, n_q_heads, d.n_kv_heads, d.head_dim, scale,
-                       (hipStream_t)stream, nullptr, 0, nullptr, rc);
+  return run_attention(d.device, *plan, q, kv->k, kv->v, out, lse, n_q_heads, d.n_kv_heads, d.head_dim, d.dtype,
+                       scale, (hipStream_t)stream, nullptr, 0, nullptr, rc);
 }
 
 sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, const void *const *q_per_layer,
@@ -1070,7 +1089,7 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
                   hipEvent_t after_fwd = nullptr) {
     RcView rc{pool, l, table->d_rc_ids};
     return run_attention(d.device, *plan, q_per_layer[l], slot.k, slot.v, out_per_layer[l], nullptr, n_q_heads,
-                         d.n_kv_heads, d.head_dim, scale, cs, ready_flag, ready_value, after_fwd, rc);
+                         d.n_kv_heads, d.head_dim, d.dtype, scale, cs, ready_flag, ready_value, after_fwd, rc);
   };
 
   if (mode == SC_STACK_ATTN_ONLY) {

@@ -111,6 +111,7 @@ struct AttnArgs {
   int32_t n_kv_heads;
   int32_t group;
   int32_t rows_q;         // queries per workgroup tile
+  int32_t dtype;          // sc_dtype of q, K, V and out
   float scale_log2;       // softmax scale * log2(e)
   // Optional device-side dependency (overlapped layer stack): before reading
   // K/V, each workgroup waits until *ready_flag >= ready_value, polling at

@@ -26,6 +26,10 @@ SC_ERR_HIP = -3
 SC_ERR_RANGE = -4
 SC_ERR_UNSUPPORTED = -5
 
+SC_DTYPE_BF16 = 0
+SC_DTYPE_F16 = 1
+DTYPE_CODES = {"bf16": SC_DTYPE_BF16, "f16": SC_DTYPE_F16}
+
 SC_STACK_OVERLAP = 0
 SC_STACK_SERIAL = 1
 SC_STACK_ATTN_ONLY = 2
@@ -34,7 +38,7 @@ SC_STACK_NO_STORE = 4
 EXPORTED = [
     "sc_pool_create", "sc_pool_destroy", "sc_pool_layout_get", "sc_table_create",
     "sc_table_destroy", "sc_table_totals", "sc_fetch_layer_kv", "sc_append_new_kv",
-    "sc_prefill_attn", "sc_prefill_attn_varlen", "sc_store_layer_kv", "sc_prefill_stack",
+    "sc_prefill_attn", "sc_prefill_attn_f16", "sc_prefill_attn_varlen", "sc_store_layer_kv", "sc_prefill_stack",
     "sc_attn_plan_query", "sc_pool_resize", "sc_plan_capacity", "sc_elastic_unit", "sc_scale_up",
     "sc_scale_down", "sc_last_error", "sc_version",
 ]
@@ -50,7 +54,7 @@ class sc_pool_desc(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
                 ("n_device_blocks", ctypes.c_int64), ("n_host_blocks", ctypes.c_int64),
-                ("device", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("device", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("device_base", ctypes.c_void_p), ("host_base", ctypes.c_void_p),
                 ("n_rc_blocks", ctypes.c_int64), ("rc_base", ctypes.c_void_p)]
 
@@ -60,7 +64,8 @@ class sc_pool_layout(ctypes.Structure):
                 ("slice_bytes", ctypes.c_size_t), ("block_bytes", ctypes.c_size_t),
                 ("row_bytes", ctypes.c_size_t), ("n_device_blocks", ctypes.c_int64),
                 ("n_host_blocks", ctypes.c_int64), ("device_blocks_lent", ctypes.c_int64),
-                ("rc_base", ctypes.c_void_p), ("n_rc_blocks", ctypes.c_int64)]
+                ("rc_base", ctypes.c_void_p), ("n_rc_blocks", ctypes.c_int64),
+                ("dtype", ctypes.c_int32)]
 
 
 class sc_model_shape(ctypes.Structure):
@@ -103,6 +108,7 @@ def load():
         "sc_fetch_layer_kv": (I32, [P, P, I32, ctypes.POINTER(sc_active), VP]),
         "sc_append_new_kv": (I32, [P, P, VP, VP, ctypes.POINTER(sc_active), VP]),
         "sc_prefill_attn": (I32, [VP, VP, VP, I32, I32, I32, I32, I32, F32, VP, VP, VP]),
+        "sc_prefill_attn_f16": (I32, [VP, VP, VP, I32, I32, I32, I32, I32, F32, VP, VP, VP]),
         "sc_prefill_attn_varlen": (I32, [P, P, I32, VP, ctypes.POINTER(sc_active), I32, F32, VP, VP, VP]),
         "sc_store_layer_kv": (I32, [P, P, I32, VP, VP, VP]),
         "sc_prefill_stack": (I32, [P, P, I32, ctypes.POINTER(VP), ctypes.POINTER(VP),
@@ -143,9 +149,9 @@ def sc_version():
 
 
 def sc_pool_create(n_layers, n_kv_heads, head_dim, block_size, n_device_blocks, n_host_blocks=0,
-                   device=0, device_base=0, host_base=0, n_rc_blocks=0, rc_base=0):
+                   device=0, device_base=0, host_base=0, n_rc_blocks=0, rc_base=0, dtype=SC_DTYPE_BF16):
     d = sc_pool_desc(n_layers, n_kv_heads, head_dim, block_size, n_device_blocks, n_host_blocks,
-                     device, 0, device_base or None, host_base or None, n_rc_blocks, rc_base or None)
+                     device, dtype, device_base or None, host_base or None, n_rc_blocks, rc_base or None)
     h = ctypes.c_void_p()
     _check(load().sc_pool_create(ctypes.byref(d), ctypes.byref(h)))
     return h.value
@@ -200,6 +206,12 @@ def sc_prefill_attn(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_
                     out, lse=0, scale=0.0, stream=0):
     _check(load().sc_prefill_attn(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_heads,
                                   head_dim, scale, out, lse or None, stream or None))
+
+
+def sc_prefill_attn_f16(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_heads, head_dim,
+                        out, lse=0, scale=0.0, stream=0):
+    _check(load().sc_prefill_attn_f16(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_heads,
+                                      head_dim, scale, out, lse or None, stream or None))
 
 
 def sc_prefill_attn_varlen(pool, table, layer, q, kv, n_q_heads, out, lse=0, scale=0.0, stream=0):

@@ -7,13 +7,16 @@ import numpy as np
 import torch
 
 
+_TORCH_DTYPES = {"bf16": torch.bfloat16, "f16": torch.float16}
+
+
 def to_u16(t):
-    """bf16 tensor (any device) -> numpy uint16 bit patterns."""
+    """16-bit tensor (any device) -> numpy uint16 bit patterns."""
     return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def from_u16(a, device):
-    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device).view(torch.bfloat16)
+def from_u16(a, device, dtype="bf16"):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device).view(_TORCH_DTYPES[dtype])
 
 
 class DevicePool:
@@ -24,13 +27,13 @@ class DevicePool:
     def __init__(self, sc, wl, pool_u16=None, fill="numpy"):
         self.sc, self.wl = sc, wl
         be = wl.block_elems
-        self.dev = torch.empty(max(1, wl.n_device_blocks) * be, dtype=torch.bfloat16, device="cuda")
+        self.dev = torch.empty(max(1, wl.n_device_blocks) * be, dtype=_TORCH_DTYPES[wl.dtype], device="cuda")
         self.host = None
         if wl.n_host_blocks:
-            self.host = torch.empty(wl.n_host_blocks * be, dtype=torch.bfloat16).pin_memory()
+            self.host = torch.empty(wl.n_host_blocks * be, dtype=_TORCH_DTYPES[wl.dtype]).pin_memory()
         self.rc = None
         if wl.n_rc_blocks:
-            self.rc = torch.empty(wl.n_rc_blocks * be, dtype=torch.bfloat16, device="cuda")
+            self.rc = torch.empty(wl.n_rc_blocks * be, dtype=_TORCH_DTYPES[wl.dtype], device="cuda")
         if pool_u16 is not None:
             flat = pool_u16.reshape(wl.n_blocks, be)
             self.dev.view(torch.int16)[: wl.n_device_blocks * be].copy_(
@@ -49,7 +52,8 @@ class DevicePool:
                                         wl.n_device_blocks, wl.n_host_blocks, 0,
                                         self.dev.data_ptr(),
                                         self.host.data_ptr() if self.host is not None else 0,
-                                        wl.n_rc_blocks, self.rc.data_ptr() if self.rc is not None else 0)
+                                        wl.n_rc_blocks, self.rc.data_ptr() if self.rc is not None else 0,
+                                        sc.DTYPE_CODES[wl.dtype])
         self.table = sc.sc_table_create(self.handle, wl.block_ids, wl.cu_blocks, wl.prefix_len,
                                         wl.new_len, torch.cuda.current_stream().cuda_stream)
 
@@ -88,12 +92,13 @@ class DevicePool:
 
 
 def new_active(sc, wl, fill_bits=0xFFFF, extra=0):
-    """K and V active-layer buffers of sum(P+N) (+ extra) rows, filled with
-    the 16-bit pattern `fill_bits`, and their sc_active descriptor."""
+    """K and V active-layer buffers of sum(P+N) (+ extra) rows of the
+    workload's element type, filled with the 16-bit pattern `fill_bits`
+    (0xFFFF is a NaN in bf16 and fp16), and their sc_active descriptor."""
     cap = wl.total_kv + extra
     fill = int(np.uint16(fill_bits).view(np.int16))
     k = torch.full((cap, wl.n_kv_heads, wl.head_dim), fill, dtype=torch.int16, device="cuda")
     v = torch.full_like(k, fill)
-    k = k.view(torch.bfloat16)
-    v = v.view(torch.bfloat16)
+    k = k.view(_TORCH_DTYPES[wl.dtype])
+    v = v.view(_TORCH_DTYPES[wl.dtype])
     return k, v, sc.active(k.data_ptr(), v.data_ptr(), cap)

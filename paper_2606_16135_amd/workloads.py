@@ -11,9 +11,11 @@ and length distributions of those conversations: a long cached history
 (prefix) plus a short new turn, KV blocks of 16 tokens scattered over a donor
 pool in block-major layout.
 
-Values are N(0, 1) draws rounded to bf16 (round to nearest even) and kept as
-raw 16-bit patterns.  Pool blocks that no table references are filled with
-the bf16 quiet-NaN pattern 0x7FC0, so any stray read poisons attention.
+Values are N(0, 1) draws rounded to bf16 (or to IEEE fp16 for fp16
+workloads; round to nearest even) and kept as raw 16-bit patterns.  Pool
+blocks that no table references are filled with the element type's
+quiet-NaN pattern (bf16 0x7FC0, fp16 0x7E00), so any stray read poisons
+attention.
 """
 
 import dataclasses
@@ -22,6 +24,12 @@ import math
 import numpy as np
 
 BF16_NAN_SENTINEL = 0x7FC0
+F16_NAN_SENTINEL = 0x7E00
+DTYPES = ("bf16", "f16")
+
+
+def nan_sentinel(dtype):
+    return BF16_NAN_SENTINEL if dtype == "bf16" else F16_NAN_SENTINEL
 SEED_BASE = 26061613500
 
 
@@ -42,6 +50,7 @@ class Workload:
     seed: int
     description: str = ""
     n_rc_blocks: int = 0            # regular-cache tier (ids after the host tier)
+    dtype: str = "bf16"             # element type: "bf16" or "f16"
 
     @property
     def batch(self):
@@ -112,7 +121,7 @@ def _place(rng, total_blocks, needed):
 
 def make_workload(name, n_layers, n_q_heads, n_kv_heads, head_dim, prefix_len,
                   new_len, seed, block_size=16, pool_factor=4, host_fraction=0.0,
-                  description="", rc_fraction=0.0):
+                  description="", rc_fraction=0.0, dtype="bf16"):
     """Build a workload with a seeded block placement.
 
     The donor pool holds ``pool_factor`` times the donor blocks the batch
@@ -124,7 +133,10 @@ def make_workload(name, n_layers, n_q_heads, n_kv_heads, head_dim, prefix_len,
     ``rc_fraction`` > 0 moves the first floor(rc_fraction * (P // B)) blocks
     of each sequence -- blocks its prefix fills completely -- to a regular
     cache tier (ids after the host tier, ``pool_factor`` times the blocks
-    placed there, seeded placement of their own)."""
+    placed there, seeded placement of their own).  ``dtype`` is the element
+    type of every value ("bf16" or "f16")."""
+    if dtype not in DTYPES:
+        raise ValueError(f"unknown element type {dtype}")
     prefix_len = np.asarray(prefix_len, dtype=np.int32)
     new_len = np.asarray(new_len, dtype=np.int32)
     per_seq = np.array([_blocks_for(p, n, block_size) for p, n in zip(prefix_len, new_len)],
@@ -154,10 +166,10 @@ def make_workload(name, n_layers, n_q_heads, n_kv_heads, head_dim, prefix_len,
                     head_dim=head_dim, block_size=block_size, prefix_len=prefix_len,
                     new_len=new_len, n_device_blocks=n_dev, n_host_blocks=n_host,
                     block_ids=ids, cu_blocks=cu, seed=seed, description=description,
-                    n_rc_blocks=n_rc)
+                    n_rc_blocks=n_rc, dtype=dtype)
 
 
-def config(index, seed=None, rc_fraction=0.0):
+def config(index, seed=None, rc_fraction=0.0, dtype="bf16"):
     """The five benchmark shapes, numbered 1..5.
 
     1 tiny: 1 layer, 8/8 heads, D=64, prefix 256 (16 blocks) + new 64, pool of
@@ -173,8 +185,8 @@ def config(index, seed=None, rc_fraction=0.0):
       half of it on the host-pinned tier.
 
     ``rc_fraction`` > 0 gives each sequence a regular-cache tier for that
-    fraction of its full prefix blocks (see make_workload); the name and
-    description say so.
+    fraction of its full prefix blocks (see make_workload); ``dtype="f16"``
+    draws fp16 values; the name and description say so.
     """
     if seed is None:
         seed = SEED_BASE + index
@@ -205,19 +217,23 @@ def config(index, seed=None, rc_fraction=0.0):
     if rc_fraction:
         name += f"-rc{rc_fraction:g}"
         desc += f", regular cache for {rc_fraction:g} of the full prefix blocks"
-    wl = make_workload(name, *shape, p, n, seed, description=desc, rc_fraction=rc_fraction, **kw)
+    if dtype != "bf16":
+        name += f"-{dtype}"
+        desc += f", {dtype} values"
+    wl = make_workload(name, *shape, p, n, seed, description=desc, rc_fraction=rc_fraction, dtype=dtype, **kw)
     if index == 1 and not rc_fraction:
         assert wl.n_blocks == 64
     return wl
 
 
 def small_workload(seed, prefix_len, new_len, n_layers=2, n_q_heads=8, n_kv_heads=2,
-                   head_dim=64, block_size=16, pool_factor=2.0, host_fraction=0.0, rc_fraction=0.0):
+                   head_dim=64, block_size=16, pool_factor=2.0, host_fraction=0.0, rc_fraction=0.0,
+                   dtype="bf16"):
     """A custom small workload for parity edge cases."""
     return make_workload(f"small-{seed}", n_layers, n_q_heads, n_kv_heads, head_dim,
                          prefix_len, new_len, seed, block_size=block_size,
                          pool_factor=pool_factor, host_fraction=host_fraction,
-                         rc_fraction=rc_fraction)
+                         rc_fraction=rc_fraction, dtype=dtype)
 
 
 
@@ -237,24 +253,35 @@ def normal_bf16(rng, shape, scale=1.0):
     return f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32) * np.float32(scale))
 
 
+def normal_bits(rng, shape, dtype="bf16", scale=1.0):
+    """N(0, scale^2) draws rounded to the element type (nearest even), as
+    16-bit patterns.  numpy's float16 conversion rounds to nearest even."""
+    x = rng.standard_normal(shape, dtype=np.float32) * np.float32(scale)
+    if dtype == "bf16":
+        return f32_to_bf16_bits(x)
+    return x.astype(np.float16).view(np.uint16)
+
+
 def pool_numpy(wl):
-    """Pool contents as uint16 of shape ``wl.pool_shape()``: N(0,1) bf16 in
-    every referenced block, the NaN sentinel in every other block."""
+    """Pool contents as uint16 of shape ``wl.pool_shape()``: N(0,1) values of
+    the workload's element type in every referenced block, the NaN sentinel
+    in every other block."""
     rng = np.random.default_rng(wl.seed_for("pool"))
-    pool = np.full(wl.pool_shape(), BF16_NAN_SENTINEL, dtype=np.uint16)
+    pool = np.full(wl.pool_shape(), nan_sentinel(wl.dtype), dtype=np.uint16)
     used = np.unique(wl.block_ids)
-    pool[used] = normal_bf16(rng, (len(used),) + wl.pool_shape()[1:])
+    pool[used] = normal_bits(rng, (len(used),) + wl.pool_shape()[1:], wl.dtype)
     return pool
 
 
 def layer_inputs_numpy(wl, layer, q_scale=1.0):
     """q[sum N][H_q][D], k_new and v_new[sum N][H_kv][D] of one layer as
-    uint16 bf16 patterns.  ``q_scale`` > 1 makes the softmax peaky."""
+    uint16 patterns of the element type.  ``q_scale`` > 1 makes the softmax
+    peaky."""
     rng = np.random.default_rng(wl.seed_for(f"layer{layer}"))
     t = wl.total_q
-    q = normal_bf16(rng, (t, wl.n_q_heads, wl.head_dim), q_scale)
-    k = normal_bf16(rng, (t, wl.n_kv_heads, wl.head_dim))
-    v = normal_bf16(rng, (t, wl.n_kv_heads, wl.head_dim))
+    q = normal_bits(rng, (t, wl.n_q_heads, wl.head_dim), wl.dtype, q_scale)
+    k = normal_bits(rng, (t, wl.n_kv_heads, wl.head_dim), wl.dtype)
+    v = normal_bits(rng, (t, wl.n_kv_heads, wl.head_dim), wl.dtype)
     return q, k, v
 
 
@@ -262,6 +289,11 @@ def layer_inputs_numpy(wl, layer, q_scale=1.0):
 # torch generation on the device (large shapes).  torch is imported lazily so
 # that CPU-only users of this module do not need it.
 # ----------------------------------------------------------------------------
+
+def torch_dtype(wl):
+    import torch
+    return torch.bfloat16 if wl.dtype == "bf16" else torch.float16
+
 
 def _torch_gen(wl, tag, device):
     import torch
@@ -281,45 +313,49 @@ def fill_pool_torch(wl, dev_pool, host_pool=None, chunk_blocks=256, rc_pool=None
     Values are drawn on the device in chunks of blocks."""
     import torch
     device = dev_pool.device
+    td = torch_dtype(wl)
+    sentinel = nan_sentinel(wl.dtype)
     used = np.zeros(wl.n_blocks, dtype=bool)
     used[wl.block_ids] = True
     be = wl.block_elems
     gen = _torch_gen(wl, "pool-device", device)
     dv = dev_pool.view(torch.int16).view(wl.n_device_blocks, be)
-    dv.fill_(BF16_NAN_SENTINEL)
+    dv.fill_(sentinel)
     dev_used = np.nonzero(used[:wl.n_device_blocks])[0]
     for i in range(0, len(dev_used), chunk_blocks):
         idx = torch.from_numpy(dev_used[i:i + chunk_blocks]).to(device)
         vals = torch.randn((len(idx), be), generator=gen, device=device, dtype=torch.float32)
-        dv.index_copy_(0, idx, vals.to(torch.bfloat16).view(torch.int16))
+        dv.index_copy_(0, idx, vals.to(td).view(torch.int16))
     if wl.n_host_blocks:
         assert host_pool is not None
         hv = host_pool.view(torch.int16).view(wl.n_host_blocks, be)
-        hv.fill_(BF16_NAN_SENTINEL)
+        hv.fill_(sentinel)
         host_used = np.nonzero(used[wl.n_device_blocks:])[0]
         genh = _torch_gen(wl, "pool-host", device)
         for i in range(0, len(host_used), chunk_blocks):
             sel = host_used[i:i + chunk_blocks]
             vals = torch.randn((len(sel), be), generator=genh, device=device, dtype=torch.float32)
-            hv[torch.from_numpy(sel)] = vals.to(torch.bfloat16).view(torch.int16).cpu()
+            hv[torch.from_numpy(sel)] = vals.to(td).view(torch.int16).cpu()
     if wl.n_rc_blocks:
         assert rc_pool is not None
         rv = rc_pool.view(torch.int16).view(wl.n_rc_blocks, be)
-        rv.fill_(BF16_NAN_SENTINEL)
+        rv.fill_(sentinel)
         rc_used = np.nonzero(used[wl.rc_first_id:])[0]
         genr = _torch_gen(wl, "pool-rc", device)
         for i in range(0, len(rc_used), chunk_blocks):
             idx = torch.from_numpy(rc_used[i:i + chunk_blocks]).to(device)
             vals = torch.randn((len(idx), be), generator=genr, device=device, dtype=torch.float32)
-            rv.index_copy_(0, idx, vals.to(torch.bfloat16).view(torch.int16))
+            rv.index_copy_(0, idx, vals.to(td).view(torch.int16))
 
 
 def layer_inputs_torch(wl, layer, device, q_scale=1.0):
-    """Device bf16 tensors q[sum N][H_q][D], k_new, v_new[sum N][H_kv][D]."""
+    """Device tensors q[sum N][H_q][D], k_new, v_new[sum N][H_kv][D] of the
+    workload's element type."""
     import torch
     g = _torch_gen(wl, f"layer{layer}", device)
     t = wl.total_q
     q = (torch.randn((t, wl.n_q_heads, wl.head_dim), generator=g, device=device) * q_scale)
     k = torch.randn((t, wl.n_kv_heads, wl.head_dim), generator=g, device=device)
     v = torch.randn((t, wl.n_kv_heads, wl.head_dim), generator=g, device=device)
-    return q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
+    td = torch_dtype(wl)
+    return q.to(td), k.to(td), v.to(td)

@@ -29,15 +29,15 @@ def require_gpu():
     return sc
 
 
-def bits_to_f64(a):
-    from oracle.attention import bf16_bits_to_f64
-    return bf16_bits_to_f64(a)
+def bits_to_f64(a, dtype="bf16"):
+    from oracle.attention import bits_to_f64 as conv
+    return conv(a, dtype)
 
 
-def compare_attention(gpu_bits, ref, what=""):
+def compare_attention(gpu_bits, ref, what="", dtype="bf16"):
     """Element-wise |gpu - ref| <= ATOL + RTOL |ref| on every element, no NaN,
     and relative L2 below REL_L2.  Returns the error statistics."""
-    g = bits_to_f64(gpu_bits)
+    g = bits_to_f64(gpu_bits, dtype)
     assert np.all(np.isfinite(g)), f"{what}: non-finite output"
     err = np.abs(g - ref)
     bound = ATOL + RTOL * np.abs(ref)

@@ -1,6 +1,6 @@
-"""GPU parity at the five benchmark shapes (and two of them with half of each
-sequence's full prefix blocks in the regular cache), in the launch
-configuration the benchmark times: the whole layer stack runs once through sc_prefill_stack
+"""GPU parity at the five benchmark shapes (two of them also with half of each
+sequence's full prefix blocks in the regular cache, and the 8B shape also
+with fp16 values), in the launch configuration the benchmark times: the whole layer stack runs once through sc_prefill_stack
 (overlapped mode, two active slots, every layer fetched, appended, attended
 and stored), on the same seeded device-generated pool and inputs.
 
@@ -32,9 +32,13 @@ from _gpu_util import compare_attention, require_gpu, to_u16
 pytestmark = pytest.mark.gpu
 
 
-def _bits_to_f32(u16):
-    """bf16 bit patterns to float32 (exact), for the oracle's row sampler."""
-    return (u16.astype(np.uint32) << 16).view(np.float32)
+def _bits_to_float(u16, dtype):
+    """16-bit patterns to floats (exact), for the oracle's row sampler: bf16
+    to float32 (half the memory of float64 at these sizes), fp16 through
+    the oracle's float64 upcast."""
+    if dtype == "bf16":
+        return (u16.astype(np.uint32) << 16).view(np.float32)
+    return oa.f16_bits_to_f64(u16)
 
 
 def _sample_rows(wl, rng, per_seq_random=2):
@@ -61,14 +65,15 @@ def _sub_pool(dp, layer, ids):
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("cfg,rc", [(2, 0.0), (3, 0.0), (4, 0.0), (5, 0.0), (2, 0.5), (3, 0.5)],
-                         ids=["2", "3", "4", "5", "2-rc0.5", "3-rc0.5"])
-def test_benchmark_shape_stack_matches_oracle(cfg, rc):
+@pytest.mark.parametrize("cfg,rc,dtype", [(2, 0.0, "bf16"), (3, 0.0, "bf16"), (4, 0.0, "bf16"), (5, 0.0, "bf16"),
+                                          (2, 0.5, "bf16"), (3, 0.5, "bf16"), (2, 0.0, "f16")],
+                         ids=["2", "3", "4", "5", "2-rc0.5", "3-rc0.5", "2-f16"])
+def test_benchmark_shape_stack_matches_oracle(cfg, rc, dtype):
     sc = require_gpu()
     import torch
     from paper_2606_16135_amd.torch_pool import DevicePool
 
-    wl = W.config(cfg, rc_fraction=rc)
+    wl = W.config(cfg, rc_fraction=rc, dtype=dtype)
     rc_rows = ok.regular_cache_rows(wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, wl.block_size,
                                     wl.rc_first_id)
     L = wl.n_layers
@@ -81,10 +86,11 @@ def test_benchmark_shape_stack_matches_oracle(cfg, rc):
         snap = {l: _sub_pool(dp, l, ids) for l in check_layers}
 
         inputs = [W.layer_inputs_torch(wl, l, "cuda") for l in range(L)]
-        outs = [torch.empty((wl.total_q, wl.n_q_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+        td = W.torch_dtype(wl)
+        outs = [torch.empty((wl.total_q, wl.n_q_heads, wl.head_dim), dtype=td, device="cuda")
                 for _ in range(L)]
-        slot_t = [(torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda"),
-                   torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda"))
+        slot_t = [(torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=td, device="cuda"),
+                   torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=td, device="cuda"))
                   for _ in range(2)]
         slots = [sc.active(k.data_ptr(), v.data_ptr(), wl.total_kv) for k, v in slot_t]
         compute = torch.cuda.current_stream()
@@ -118,12 +124,12 @@ def test_benchmark_shape_stack_matches_oracle(cfg, rc):
 
             # attention, sampled rows of the stack's output
             rows = _sample_rows(wl, rng)
-            o_ref, _ = oa.attention_rows(_bits_to_f32(q), _bits_to_f32(k_full), _bits_to_f32(v_full),
-                                         wl.prefix_len, wl.new_len, rows)
+            o_ref, _ = oa.attention_rows(_bits_to_float(q, dtype), _bits_to_float(k_full, dtype),
+                                         _bits_to_float(v_full, dtype), wl.prefix_len, wl.new_len, rows)
             cu_q, _ = ok.seq_offsets(wl.prefix_len, wl.new_len)
             og = to_u16(outs[l])
             got = np.stack([og[cu_q[b] + i, h] for b, i, h in rows])
-            stats = compare_attention(got, o_ref, f"cfg {cfg} layer {l} ({len(rows)} rows)")
+            stats = compare_attention(got, o_ref, f"cfg {cfg} layer {l} ({len(rows)} rows)", dtype)
 
             # store: every referenced block of this layer
             expect = ok.store_layer(snap[l], local_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, 0, kn, vn)

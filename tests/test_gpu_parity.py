@@ -1,6 +1,6 @@
 """GPU parity of every C-ABI call against the oracle, element by element, on
 seeded inputs small enough for the dense oracle: several key tiles and query
-tiles with ragged tails, head groups 1/4/5/8, head_dim 64/128, empty prefix,
+tiles with ragged tails, head groups 1/4/5/8, head_dim 64/128, bf16 and fp16 values, empty prefix,
 a batch with an empty new turn, split-key work, a half host-pinned pool, and
 tables whose leading blocks sit in the regular-cache tier (read in place by
 attention; their active-buffer rows hold NaN patterns the kernel must not
@@ -41,20 +41,25 @@ def _case(name):
         "rc_split_d128": lambda: sw(110, [5000], [40], 1, 8, 2, 128, rc_fraction=0.5),
         "rc_whole_prefix": lambda: sw(111, [256, 512], [64, 3], 1, 32, 8, 128, rc_fraction=1.0),
         "rc_host": lambda: sw(112, [200, 77], [20, 31], 2, 8, 2, 128, host_fraction=0.5, rc_fraction=0.5),
+        # IEEE fp16 values (the paper's serving precision)
+        "f16_g4_d128_ragged": lambda: sw(121, [100], [77], 2, 32, 8, 128, dtype="f16"),
+        "f16_varlen": lambda: sw(122, [33, 0, 1000, 17], [5, 64, 1, 200], 2, 16, 4, 64, dtype="f16"),
+        "f16_g5_split_rc": lambda: sw(123, [5000, 300], [40, 20], 1, 40, 8, 128, rc_fraction=0.5, dtype="f16"),
+        "f16_host": lambda: sw(124, [200, 77], [20, 31], 1, 8, 2, 128, host_fraction=0.5, dtype="f16"),
     }[name]()
 
 
 CASES = ["cfg1", "g4_d128_ragged", "g5_d128", "g1_d64_P0", "g4_split_long", "varlen_batch",
          "varlen_empty_turn", "host_tier", "g8_d64", "rc_varlen", "rc_split_d128", "rc_whole_prefix",
-         "rc_host"]
+         "rc_host", "f16_g4_d128_ragged", "f16_varlen", "f16_g5_split_rc", "f16_host"]
 
 
 def _oracle_layer(wl, pool_u16, layer, q, kn, vn):
     k_act, v_act = ok.gather_layer(pool_u16, wl.block_ids, wl.cu_blocks, wl.prefix_len,
                                    wl.new_len, layer)
     k_full, v_full = ok.append_new(k_act, v_act, kn, vn, wl.prefix_len, wl.new_len)
-    o, lse = oa.attention(oa.bf16_bits_to_f64(q), oa.bf16_bits_to_f64(k_full),
-                          oa.bf16_bits_to_f64(v_full), wl.prefix_len, wl.new_len)
+    o, lse = oa.attention(oa.bits_to_f64(q, wl.dtype), oa.bits_to_f64(k_full, wl.dtype),
+                          oa.bits_to_f64(v_full, wl.dtype), wl.prefix_len, wl.new_len)
     return k_act, v_act, k_full, v_full, o, lse
 
 
@@ -83,7 +88,7 @@ def test_layer_path_matches_oracle(name, q_scale):
     try:
         for layer in range(wl.n_layers):
             q, kn, vn = W.layer_inputs_numpy(wl, layer, q_scale=q_scale)
-            qd, knd, vnd = (from_u16(x, "cuda") for x in (q, kn, vn))
+            qd, knd, vnd = (from_u16(x, "cuda", wl.dtype) for x in (q, kn, vn))
             k, v, act = new_active(sc, wl, fill_bits=0xFFFF)
             sc.sc_fetch_layer_kv(dp.handle, dp.table, layer, act, stream)
             torch.cuda.synchronize()
@@ -105,31 +110,33 @@ def test_layer_path_matches_oracle(name, q_scale):
             assert np.all(kg[rcr] == 0xFFFF) and np.all(vg[rcr] == 0xFFFF)
 
             out = torch.full((wl.total_q, wl.n_q_heads, wl.head_dim), float("nan"),
-                             dtype=torch.bfloat16, device="cuda")
+                             dtype=W.torch_dtype(wl), device="cuda")
             lse = torch.full((wl.n_q_heads, max(1, wl.total_q)), float("nan"), device="cuda")
             sc.sc_prefill_attn_varlen(dp.handle, dp.table, layer, qd.data_ptr(), act, wl.n_q_heads,
                                       out.data_ptr(), lse.data_ptr(), 0.0, stream)
             torch.cuda.synchronize()
-            compare_attention(to_u16(out), o_ref, f"{name} layer {layer} varlen")
+            compare_attention(to_u16(out), o_ref, f"{name} layer {layer} varlen", wl.dtype)
             lse_g = lse.cpu().numpy().astype(np.float64)[:, :wl.total_q]
-            # The kernel's denominator sums the bf16-rounded probabilities
-            # (the same weights that multiply V), each within 2^-9 relative
-            # of its exact value, so ln l is off by at most about 2^-9 plus
-            # fp32 accumulation: 2^-8 bounds it.
+            # The kernel's denominator sums the probabilities rounded to the
+            # element type (the same weights that multiply V), each within
+            # 2^-9 (bf16) or 2^-11 (fp16) relative of its exact value, so
+            # ln l is off by at most about 2^-9 plus fp32 accumulation:
+            # 2^-8 bounds it.
             np.testing.assert_allclose(lse_g, lse_ref, atol=2.0 ** -8, rtol=1e-4)
             if wl.batch == 1 and not wl.n_rc_blocks:
                 out1 = torch.empty_like(out)
                 lse1 = torch.empty_like(lse)
-                sc.sc_prefill_attn(qd.data_ptr(), k.data_ptr(), v.data_ptr(), int(wl.prefix_len[0]),
-                                   int(wl.new_len[0]), wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
-                                   out1.data_ptr(), lse1.data_ptr(), 0.0, stream)
+                single = sc.sc_prefill_attn if wl.dtype == "bf16" else sc.sc_prefill_attn_f16
+                single(qd.data_ptr(), k.data_ptr(), v.data_ptr(), int(wl.prefix_len[0]),
+                       int(wl.new_len[0]), wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                       out1.data_ptr(), lse1.data_ptr(), 0.0, stream)
                 torch.cuda.synchronize()
                 assert torch.equal(out1.view(torch.int16), out.view(torch.int16))
     finally:
         dp.close()
 
 
-@pytest.mark.parametrize("name", ["cfg1", "host_tier", "varlen_batch", "rc_host"])
+@pytest.mark.parametrize("name", ["cfg1", "host_tier", "varlen_batch", "rc_host", "f16_host"])
 def test_store_matches_oracle(name):
     sc = require_gpu()
     import torch
@@ -141,7 +148,7 @@ def test_store_matches_oracle(name):
         expect = pool_u16
         for layer in range(wl.n_layers):
             _, kn, vn = W.layer_inputs_numpy(wl, layer)
-            knd, vnd = from_u16(kn, "cuda"), from_u16(vn, "cuda")
+            knd, vnd = from_u16(kn, "cuda", wl.dtype), from_u16(vn, "cuda", wl.dtype)
             sc.sc_store_layer_kv(dp.handle, dp.table, layer, knd.data_ptr(), vnd.data_ptr(), stream)
             torch.cuda.synchronize()
             expect = ok.store_layer(expect, wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len,
@@ -167,19 +174,21 @@ def test_store_matches_oracle(name):
         dp.close()
 
 
-def test_single_visible_key_returns_its_value_row_exactly():
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_single_visible_key_returns_its_value_row_exactly(dtype):
     sc = require_gpu()
     import torch
     rng = np.random.default_rng(5)
+    single = sc.sc_prefill_attn if dtype == "bf16" else sc.sc_prefill_attn_f16
     for hq, hkv, d in [(8, 8, 64), (32, 8, 128), (40, 8, 128)]:
         n = 37
-        q = W.normal_bf16(rng, (n, hq, d))
-        k = W.normal_bf16(rng, (n, hkv, d))
-        v = W.normal_bf16(rng, (n, hkv, d))
-        qd, kd, vd = (from_u16(x, "cuda") for x in (q, k, v))
-        out = torch.empty((n, hq, d), dtype=torch.bfloat16, device="cuda")
-        sc.sc_prefill_attn(qd.data_ptr(), kd.data_ptr(), vd.data_ptr(), 0, n, hq, hkv, d, out.data_ptr(),
-                           0, 0.0, torch.cuda.current_stream().cuda_stream)
+        q = W.normal_bits(rng, (n, hq, d), dtype)
+        k = W.normal_bits(rng, (n, hkv, d), dtype)
+        v = W.normal_bits(rng, (n, hkv, d), dtype)
+        qd, kd, vd = (from_u16(x, "cuda", dtype) for x in (q, k, v))
+        out = torch.empty((n, hq, d), dtype=qd.dtype, device="cuda")
+        single(qd.data_ptr(), kd.data_ptr(), vd.data_ptr(), 0, n, hq, hkv, d, out.data_ptr(),
+               0, 0.0, torch.cuda.current_stream().cuda_stream)
         torch.cuda.synchronize()
         o = to_u16(out)
         g = hq // hkv
@@ -188,7 +197,7 @@ def test_single_visible_key_returns_its_value_row_exactly():
 
 
 @pytest.mark.parametrize("mode", ["overlap", "serial"])
-@pytest.mark.parametrize("name", ["stack_g4", "stack_varlen_host", "stack_rc"])
+@pytest.mark.parametrize("name", ["stack_g4", "stack_varlen_host", "stack_rc", "stack_f16_rc"])
 def test_layer_stack_matches_oracle(name, mode):
     sc = require_gpu()
     import torch
@@ -196,15 +205,17 @@ def test_layer_stack_matches_oracle(name, mode):
         wl = W.small_workload(201, [300], [70], 4, 32, 8, 128)
     elif name == "stack_varlen_host":
         wl = W.small_workload(202, [150, 0, 500], [20, 40, 7], 3, 8, 2, 64, host_fraction=0.5)
-    else:
+    elif name == "stack_rc":
         wl = W.small_workload(203, [300, 700, 40], [70, 9, 33], 3, 32, 8, 128, host_fraction=0.3,
                               rc_fraction=0.5)
+    else:
+        wl = W.small_workload(204, [400, 64], [50, 100], 3, 32, 8, 128, rc_fraction=0.5, dtype="f16")
     pool_u16 = W.pool_numpy(wl)
     dp = DevicePool(sc, wl, pool_u16)
     try:
         ins = [W.layer_inputs_numpy(wl, l) for l in range(wl.n_layers)]
-        dev = [[from_u16(x, "cuda") for x in t] for t in ins]
-        outs = [torch.full((wl.total_q, wl.n_q_heads, wl.head_dim), float("nan"), dtype=torch.bfloat16,
+        dev = [[from_u16(x, "cuda", wl.dtype) for x in t] for t in ins]
+        outs = [torch.full((wl.total_q, wl.n_q_heads, wl.head_dim), float("nan"), dtype=W.torch_dtype(wl),
                            device="cuda") for _ in range(wl.n_layers)]
         slots = [new_active(sc, wl) for _ in range(2)]
         copy = torch.cuda.Stream()
@@ -218,7 +229,7 @@ def test_layer_stack_matches_oracle(name, mode):
         for l in range(wl.n_layers):
             q, kn, vn = ins[l]
             *_, o_ref, _ = _oracle_layer(wl, pool_u16, l, q, kn, vn)
-            compare_attention(to_u16(outs[l]), o_ref, f"{name} {mode} layer {l}")
+            compare_attention(to_u16(outs[l]), o_ref, f"{name} {mode} layer {l}", wl.dtype)
             expect = ok.store_layer(expect, wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, l, kn, vn)
         assert np.array_equal(dp.full_u16(), expect)
     finally:

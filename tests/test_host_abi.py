@@ -57,6 +57,18 @@ def test_pool_validation(sc):
     assert e.value.status == sc.SC_ERR_INVALID
 
 
+def test_pool_element_type(sc):
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_pool_create(2, 2, 64, 16, 8, 0, 0, FAKE_BASE, 0, dtype=2)
+    assert e.value.status == sc.SC_ERR_INVALID
+    for code in (sc.SC_DTYPE_BF16, sc.SC_DTYPE_F16):
+        p = sc.sc_pool_create(2, 2, 64, 16, 8, 0, 0, FAKE_BASE, 0, dtype=code)
+        try:
+            assert sc.sc_pool_layout_get(p).dtype == code
+        finally:
+            sc.sc_pool_destroy(p)
+
+
 def test_pool_layout_follows_eq1(sc):
     p = sc.sc_pool_create(3, 8, 128, 16, 5, 0, 0, FAKE_BASE, 0)
     try:

@@ -215,6 +215,32 @@ def test_bf16_upcast_is_exact():
     assert vals[6] == 2.0 ** -133
 
 
+def test_f16_upcast_is_exact():
+    """Hand-decoded binary16 patterns, and every one of the 65536 patterns
+    against numpy's own float16 type (a library routine)."""
+    bits = np.array([0x3C00, 0xC000, 0x7BFF, 0x0001, 0x03FF, 0x0400, 0x8000, 0x7C00, 0xFC00, 0x3555],
+                    dtype=np.uint16)
+    v = oa.f16_bits_to_f64(bits)
+    assert v[0] == 1.0 and v[1] == -2.0
+    assert v[2] == 65504.0                        # largest finite
+    assert v[3] == 2.0 ** -24                     # smallest subnormal
+    assert v[4] == 1023 * 2.0 ** -24              # largest subnormal
+    assert v[5] == 2.0 ** -14                     # smallest normal
+    assert v[6] == 0.0 and math.copysign(1.0, v[6]) == -1.0
+    assert v[7] == math.inf and v[8] == -math.inf
+    assert v[9] == 1365 / 4096                    # 0x3555 = 1.0101010101b * 2^-2
+    allbits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    mine = oa.f16_bits_to_f64(allbits)
+    ref = allbits.view(np.float16).astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(mine[~nan]), np.signbit(ref[~nan]))
+    assert np.array_equal(oa.bits_to_f64(allbits[:100], "f16"), mine[:100])
+    with pytest.raises(ValueError):
+        oa.bits_to_f64(allbits[:4], "f32")
+
+
 # ---- planted mistakes: the pins above must catch them ---------------------
 
 def test_planted_diagonal_exclusion_is_caught(monkeypatch):
