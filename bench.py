@@ -98,6 +98,9 @@ def main():
                          "cache (read in place by attention, never fetched)")
     ap.add_argument("--dtype", choices=["bf16", "f16"], default="bf16",
                     help="element type of the pool, q, K, V and outputs")
+    ap.add_argument("--chunk-tokens", type=int, default=0,
+                    help="process the new turn in chunks of this many tokens over each fetched layer "
+                         "(0: the whole turn in one attention launch per layer)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["attention", "fetch", "copy"], default=None,
                     help="run only one kernel of the path, --steps times over every layer "
@@ -135,8 +138,12 @@ def main():
     op = [o.data_ptr() for o in outs]
 
     def stack(flags):
-        sc.sc_prefill_stack(dp.handle, dp.table, qp, kp, vp, op, slots, wl.n_q_heads, flags, 0.0,
-                            compute.cuda_stream, copy.cuda_stream)
+        if args.chunk_tokens > 0:
+            sc.sc_prefill_stack_chunked(dp.handle, dp.table, qp, kp, vp, op, slots, wl.n_q_heads, args.chunk_tokens,
+                                        flags, 0.0, compute.cuda_stream, copy.cuda_stream)
+        else:
+            sc.sc_prefill_stack(dp.handle, dp.table, qp, kp, vp, op, slots, wl.n_q_heads, flags, 0.0,
+                                compute.cuda_stream, copy.cuda_stream)
 
     if args.only is not None:
         # Profiling aid: one op over all layers, warmup then timed steps.
@@ -254,7 +261,7 @@ def main():
                          "prefix_len": [int(x) for x in wl.prefix_len][:16],
                          "new_len": [int(x) for x in wl.new_len][:16], "block_size": wl.block_size,
                          "pool_blocks": wl.n_blocks, "host_tier_blocks": wl.n_host_blocks,
-                         "regular_cache_blocks": wl.n_rc_blocks},
+                         "regular_cache_blocks": wl.n_rc_blocks, "chunk_tokens": args.chunk_tokens},
               "roofline": roofline, "details": details}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, dp, inputs)

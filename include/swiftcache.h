@@ -288,6 +288,25 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
                            uint32_t flags, void *compute_stream, void *copy_stream);
 
 /*
+ * The same layer stack with the new turn processed in chunks of at most
+ * chunk_tokens tokens per sequence (§8 names chunking the new turn for very
+ * long N): each layer's slot is fetched and appended once, then attention
+ * runs one launch per chunk c over that same slot, chunk c's queries
+ * (new tokens [c*C, min(N_b, (c+1)*C)) of each sequence) seeing the prefix
+ * and the earlier chunks.  The result equals sc_prefill_stack's (same
+ * definition; only the rounding order of the split-key merge differs);
+ * chunking bounds the split-key workspace and the length of any single
+ * launch to those of a C-token turn.  Arguments as sc_prefill_stack.
+ * Errors: as sc_prefill_stack, plus SC_ERR_INVALID (chunk_tokens <= 0).
+ */
+sc_status sc_prefill_stack_chunked(sc_pool *pool, const sc_table *table, int32_t n_layers,
+                                   const void *const *q_per_layer, const void *const *knew_per_layer,
+                                   const void *const *vnew_per_layer, void *const *out_per_layer,
+                                   const sc_active *slots /* [2] */, int32_t n_q_heads, float scale,
+                                   uint32_t flags, int32_t chunk_tokens, void *compute_stream,
+                                   void *copy_stream);
+
+/*
  * Host-only introspection of the attention work decomposition (no device
  * work, no allocation).  For a batch with the given lengths, returns in
  * *n_items the number of workgroup slots; when `items` is non-NULL it also

@@ -287,12 +287,15 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
   const bool valid = qi < wi.nq;
   const int qpos = wi.q0 + (valid ? qi : wi.nq - 1);
   const int h = wi.kvh * group + hg;
+  // qrow: the row in the plan's packed numbering (split partials, lse);
+  // io_row: the row of q and out (they differ for a chunk of a new turn).
   const int64_t qrow = (int64_t)(sd.cu_q + qpos) * a.n_q_heads + h;
+  const int64_t io_row = (int64_t)(sd.q_off + qpos) * a.n_q_heads + h;
 
   WaveState<D> w;
   // Q^T fragments (B operand): lane holds Q[row][16 k + 8 half .. + 7].
   {
-    const u32x4 *qp = reinterpret_cast<const u32x4 *>(a.q + qrow * D);
+    const u32x4 *qp = reinterpret_cast<const u32x4 *>(a.q + io_row * D);
 #pragma unroll
     for (int k = 0; k < D / 16; ++k) {
       u32x4 x = {0u, 0u, 0u, 0u};
@@ -513,7 +516,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
                         : l_tot > 0.f ? (w.m_run + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
   if (!valid) return;
   if (sd.n_splits == 1) {
-    uint16_t *orow = a.out + qrow * D;
+    uint16_t *orow = a.out + io_row * D;
 #pragma unroll
     for (int c = 0; c < D / 32; ++c)
 #pragma unroll
@@ -580,6 +583,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   }
   const int S = a.seqs[lo].n_splits;
   if (S <= 1) return;
+  const int64_t io_row = (int64_t)(a.seqs[lo].q_off + token - a.seqs[lo].cu_q) * a.n_q_heads + h;
   float ls[kAttnMaxSplits];
   float mx = -INFINITY;
 #pragma unroll
@@ -614,7 +618,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   u32x4 pk;
 #pragma unroll
   for (int e = 0; e < 4; ++e) pk[e] = Elem<DT>::pack(acc[2 * e] * winv, acc[2 * e + 1] * winv);
-  *reinterpret_cast<u32x4 *>(a.out + row * D + sub * 8) = pk;
+  *reinterpret_cast<u32x4 *>(a.out + io_row * D + sub * 8) = pk;
   if (a.lse != nullptr && sub == 0)
     a.lse[(int64_t)h * a.total_q + token] = wsum > 0.f ? mx + __logf(wsum) : -INFINITY;
 }

@@ -99,7 +99,8 @@ int attn_slots(int device) {
 
 void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N, int n_q_heads,
                     int n_kv_heads, int slots, AttnPlan *plan, const std::vector<int32_t> &rc_keys,
-                    const std::vector<int32_t> &rc_off) {
+                    const std::vector<int32_t> &rc_off, const std::vector<int32_t> &cu_k,
+                    const std::vector<int32_t> &q_off) {
   const int group = n_q_heads / n_kv_heads;
   const int rows_q = kAttnRows / group;
   const int batch = (int)P.size();
@@ -111,7 +112,8 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
   for (int b = 0; b < batch; ++b) {
     SeqDesc &s = plan->seqs[b];
     s.cu_q = (int32_t)cq;
-    s.cu_k = (int32_t)ck;
+    s.cu_k = cu_k.empty() ? (int32_t)ck : cu_k[b];
+    s.q_off = q_off.empty() ? (int32_t)cq : q_off[b];
     s.prefix = P[b];
     s.n_new = N[b];
     s.n_splits = 1;
@@ -421,20 +423,37 @@ sc_status check_heads(int hq, int hkv, int head_dim) {
   return SC_OK;
 }
 
-sc_status table_plan(sc_table *t, int hq, AttnPlan **out, int slots = 0) {
+// chunk_tokens > 0: the plan of chunk `chunk` of the new turn, i.e. new
+// tokens [chunk * C, min(N_b, (chunk + 1) * C)) of every sequence, which see
+// the prefix and the earlier chunks as their prefix (same active rows, q /
+// out rows offset by chunk * C within the sequence).
+sc_status table_plan(sc_table *t, int hq, AttnPlan **out, int slots = 0, int chunk_tokens = 0, int chunk = 0) {
   const sc_pool_desc &d = t->pool->desc;
   sc_status st = check_heads(hq, d.n_kv_heads, d.head_dim);
   if (st != SC_OK) return st;
   if (slots <= 0) slots = attn_slots(d.device);
   std::lock_guard<std::mutex> lk(t->mu);
-  auto key = std::make_pair(hq, slots);
+  auto key = std::make_tuple(hq, slots, chunk_tokens, chunk);
   auto it = t->plans.find(key);
   if (it != t->plans.end()) {
     *out = &it->second;
     return SC_OK;
   }
   AttnPlan &plan = t->plans[key];
-  plan_attention(t->P, t->N, hq, d.n_kv_heads, slots, &plan, t->rc_keys, t->rc_off);
+  if (chunk_tokens > 0) {
+    const size_t batch = t->P.size();
+    std::vector<int32_t> P(batch), N(batch), cu_k(batch), q_off(batch);
+    for (size_t b = 0; b < batch; ++b) {
+      const int64_t done = std::min<int64_t>(t->N[b], (int64_t)chunk * chunk_tokens);
+      P[b] = (int32_t)(t->P[b] + done);
+      N[b] = (int32_t)std::min<int64_t>(chunk_tokens, t->N[b] - done);
+      cu_k[b] = (int32_t)t->cu_k[b];
+      q_off[b] = (int32_t)(t->cu_q[b] + done);
+    }
+    plan_attention(P, N, hq, d.n_kv_heads, slots, &plan, t->rc_keys, t->rc_off, cu_k, q_off);
+  } else {
+    plan_attention(t->P, t->N, hq, d.n_kv_heads, slots, &plan, t->rc_keys, t->rc_off);
+  }
   st = upload_plan(&plan);
   if (st != SC_OK) {
     free_plan(&plan);
@@ -1044,11 +1063,18 @@ sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, int32_t l
                        scale, (hipStream_t)stream, nullptr, 0, nullptr, rc);
 }
 
-sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, const void *const *q_per_layer,
-                           const void *const *knew_per_layer, const void *const *vnew_per_layer,
-                           void *const *out_per_layer, const sc_active *slots, int32_t n_q_heads, float scale,
-                           uint32_t flags, void *compute_stream, void *copy_stream) {
-  clear_error();
+}  // extern "C"
+
+namespace sc {
+namespace {
+
+// The layer stack (sc_prefill_stack); chunk_tokens > 0 runs each layer's
+// attention as one launch per chunk of the new turn over the same fetched
+// slot (sc_prefill_stack_chunked).
+sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, const void *const *q_per_layer,
+                        const void *const *knew_per_layer, const void *const *vnew_per_layer,
+                        void *const *out_per_layer, const sc_active *slots, int32_t n_q_heads, float scale,
+                        uint32_t flags, int32_t chunk_tokens, void *compute_stream, void *copy_stream) {
   if (!pool || !table || !q_per_layer || !knew_per_layer || !vnew_per_layer || !out_per_layer || !slots)
     return fail(SC_ERR_INVALID, "null argument");
   if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
@@ -1078,18 +1104,36 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
     sc_status st = split_streams(d.device, &ss);
     if (st != SC_OK) return st;
   }
-  AttnPlan *plan = nullptr;
-  sc_status st = table_plan(const_cast<sc_table *>(table), n_q_heads, &plan,
-                            ss ? ss->attn_cus * kResidentPerCu : 0);
-  if (st != SC_OK) return st;
+  // One plan, or one per chunk of the new turn.
+  int n_chunks = 1;
+  if (chunk_tokens > 0) {
+    int64_t max_n = 0;
+    for (int32_t x : table->N) max_n = std::max<int64_t>(max_n, x);
+    n_chunks = (int)std::max<int64_t>(1, (max_n + chunk_tokens - 1) / chunk_tokens);
+  }
+  std::vector<AttnPlan *> plans(n_chunks, nullptr);
+  sc_status st = SC_OK;
+  for (int c = 0; c < n_chunks; ++c) {
+    st = table_plan(const_cast<sc_table *>(table), n_q_heads, &plans[c], ss ? ss->attn_cus * kResidentPerCu : 0,
+                    chunk_tokens > 0 ? chunk_tokens : 0, c);
+    if (st != SC_OK) return st;
+  }
   hipStream_t caller_cs = (hipStream_t)compute_stream;
   hipStream_t cs = ss ? ss->attn : caller_cs;
   hipStream_t xs = ss ? ss->copy : (hipStream_t)copy_stream;
+  // The first chunk waits for the slot; the slot-free event follows the
+  // last chunk's forward kernel.
   auto attn = [&](int l, const sc_active &slot, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
                   hipEvent_t after_fwd = nullptr) {
     RcView rc{pool, l, table->d_rc_ids};
-    return run_attention(d.device, *plan, q_per_layer[l], slot.k, slot.v, out_per_layer[l], nullptr, n_q_heads,
-                         d.n_kv_heads, d.head_dim, d.dtype, scale, cs, ready_flag, ready_value, after_fwd, rc);
+    for (int c = 0; c < n_chunks; ++c) {
+      sc_status r = run_attention(d.device, *plans[c], q_per_layer[l], slot.k, slot.v, out_per_layer[l], nullptr,
+                                  n_q_heads, d.n_kv_heads, d.head_dim, d.dtype, scale, cs,
+                                  c == 0 ? ready_flag : nullptr, ready_value,
+                                  c == n_chunks - 1 ? after_fwd : nullptr, rc);
+      if (r != SC_OK) return r;
+    }
+    return SC_OK;
   };
 
   if (mode == SC_STACK_ATTN_ONLY) {
@@ -1181,6 +1225,31 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
   st = body();
   for (auto &e : ev) (void)hipEventDestroy(e);
   return st;
+}
+
+}  // namespace
+}  // namespace sc
+
+extern "C" {
+
+sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, const void *const *q_per_layer,
+                           const void *const *knew_per_layer, const void *const *vnew_per_layer,
+                           void *const *out_per_layer, const sc_active *slots, int32_t n_q_heads, float scale,
+                           uint32_t flags, void *compute_stream, void *copy_stream) {
+  clear_error();
+  return prefill_stack(pool, table, n_layers, q_per_layer, knew_per_layer, vnew_per_layer, out_per_layer, slots,
+                       n_q_heads, scale, flags, 0, compute_stream, copy_stream);
+}
+
+sc_status sc_prefill_stack_chunked(sc_pool *pool, const sc_table *table, int32_t n_layers,
+                                   const void *const *q_per_layer, const void *const *knew_per_layer,
+                                   const void *const *vnew_per_layer, void *const *out_per_layer,
+                                   const sc_active *slots, int32_t n_q_heads, float scale, uint32_t flags,
+                                   int32_t chunk_tokens, void *compute_stream, void *copy_stream) {
+  clear_error();
+  if (chunk_tokens <= 0) return fail(SC_ERR_INVALID, "chunk_tokens must be positive (got %d)", chunk_tokens);
+  return prefill_stack(pool, table, n_layers, q_per_layer, knew_per_layer, vnew_per_layer, out_per_layer, slots,
+                       n_q_heads, scale, flags, chunk_tokens, compute_stream, copy_stream);
 }
 
 }  // extern "C"

@@ -77,7 +77,8 @@ struct SeqDesc {
   int32_t n_splits;   // key splits of every query tile of this sequence
   int32_t rc_keys;    // leading keys read in place from the regular cache
   int32_t rc_off;     // first entry of the sequence in AttnArgs::rc_ids
-  int32_t pad;
+  int32_t q_off;      // first row of the sequence's queries in q / out (== cu_q unless
+                      // the plan covers one chunk of the new turn)
 };
 static_assert(sizeof(SeqDesc) == 32, "SeqDesc layout");
 
@@ -161,10 +162,13 @@ struct AttnPlan {
 // `slots` = workgroups the device runs at once (CUs x resident workgroups).
 // rc_keys[b] (may be empty = none) leading keys of sequence b are read in
 // place from the regular cache: they get items of their own (a split
-// boundary at rc_keys[b]).
+// boundary at rc_keys[b]).  cu_k / q_off (may be empty = packed from P + N
+// and N): the sequence's first active-buffer row and first q / out row,
+// for plans over one chunk of a longer new turn.
 void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N, int n_q_heads,
                     int n_kv_heads, int slots, AttnPlan *plan, const std::vector<int32_t> &rc_keys = {},
-                    const std::vector<int32_t> &rc_off = {});
+                    const std::vector<int32_t> &rc_off = {}, const std::vector<int32_t> &cu_k = {},
+                    const std::vector<int32_t> &q_off = {});
 int attn_slots(int device);
 
 }  // namespace sc
@@ -206,7 +210,9 @@ struct sc_table {
   int32_t n_fetch = 0, n_append = 0, n_store = 0;
   int32_t n_fetch_host = 0;          // fetch items that read the host tier
   std::mutex mu;
-  std::map<std::pair<int, int>, sc::AttnPlan> plans;   // keyed by (n_q_heads, slots)
+  // keyed by (n_q_heads, slots, chunk tokens, chunk index); chunk tokens 0:
+  // the whole new turn
+  std::map<std::tuple<int, int, int, int>, sc::AttnPlan> plans;
   // Overlapped stack: [0] = count of layers whose active slot is filled
   // (written by the copy stream, polled by attention), [1] = time-out flag.
   uint64_t *d_sync = nullptr;

@@ -38,8 +38,8 @@ SC_STACK_NO_STORE = 4
 EXPORTED = [
     "sc_pool_create", "sc_pool_destroy", "sc_pool_layout_get", "sc_table_create",
     "sc_table_destroy", "sc_table_totals", "sc_fetch_layer_kv", "sc_append_new_kv",
-    "sc_prefill_attn", "sc_prefill_attn_f16", "sc_prefill_attn_varlen", "sc_store_layer_kv", "sc_prefill_stack",
-    "sc_attn_plan_query", "sc_pool_resize", "sc_plan_capacity", "sc_elastic_unit", "sc_scale_up",
+    "sc_prefill_attn", "sc_prefill_attn_f16", "sc_prefill_attn_varlen", "sc_store_layer_kv",
+    "sc_prefill_stack", "sc_prefill_stack_chunked", "sc_attn_plan_query", "sc_pool_resize", "sc_plan_capacity", "sc_elastic_unit", "sc_scale_up",
     "sc_scale_down", "sc_last_error", "sc_version",
 ]
 
@@ -114,6 +114,9 @@ def load():
         "sc_prefill_stack": (I32, [P, P, I32, ctypes.POINTER(VP), ctypes.POINTER(VP),
                                    ctypes.POINTER(VP), ctypes.POINTER(VP),
                                    ctypes.POINTER(sc_active), I32, F32, ctypes.c_uint32, VP, VP]),
+        "sc_prefill_stack_chunked": (I32, [P, P, I32, ctypes.POINTER(VP), ctypes.POINTER(VP),
+                                           ctypes.POINTER(VP), ctypes.POINTER(VP),
+                                           ctypes.POINTER(sc_active), I32, F32, ctypes.c_uint32, I32, VP, VP]),
         "sc_attn_plan_query": (I32, [I32, i32p, i32p, VP, I32, I32, I32, i32p, i32p, I32, i32p]),
         "sc_pool_resize": (I32, [P, I64]),
         "sc_plan_capacity": (I32, [ctypes.POINTER(sc_model_shape), I64, ctypes.POINTER(I64), I32,
@@ -285,3 +288,13 @@ def sc_scale_down(worker_blocks, worker_block_size, meu_worker, meu_master, wind
     _check(load().sc_scale_down(int(worker_blocks), int(worker_block_size), int(meu_worker), int(meu_master),
                                 w, n, ctypes.byref(dw), ctypes.byref(dm)))
     return dw.value, dm.value
+
+
+def sc_prefill_stack_chunked(pool, table, q_ptrs, knew_ptrs, vnew_ptrs, out_ptrs, slots, n_q_heads, chunk_tokens,
+                             flags=SC_STACK_OVERLAP, scale=0.0, compute_stream=0, copy_stream=0):
+    n = len(q_ptrs)
+    arr = ctypes.c_void_p * n
+    slot_arr = (sc_active * 2)(*slots)
+    _check(load().sc_prefill_stack_chunked(pool, table, n, arr(*q_ptrs), arr(*knew_ptrs), arr(*vnew_ptrs),
+                                           arr(*out_ptrs), slot_arr, n_q_heads, scale, flags, chunk_tokens,
+                                           compute_stream or None, copy_stream or None))

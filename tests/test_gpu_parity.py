@@ -236,6 +236,45 @@ def test_layer_stack_matches_oracle(name, mode):
         dp.close()
 
 
+@pytest.mark.parametrize("name,chunk,mode", [
+    ("g4_d128_ragged", 16, "overlap"), ("g4_d128_ragged", 100, "serial"), ("g4_d128_ragged", 1000, "overlap"),
+    ("varlen_batch", 48, "overlap"), ("varlen_empty_turn", 7, "overlap"), ("rc_varlen", 64, "overlap"),
+    ("f16_g5_split_rc", 9, "overlap"), ("host_tier", 13, "overlap"), ("g1_d64_P0", 33, "serial"),
+])
+def test_chunked_stack_matches_oracle(name, chunk, mode):
+    """The new turn in chunks over one fetched slot per layer: every output
+    row against the oracle's (unchunked) attention, and the pool after the
+    stores byte for byte."""
+    sc = require_gpu()
+    import torch
+    wl = _case(name)
+    pool_u16 = W.pool_numpy(wl)
+    dp = DevicePool(sc, wl, pool_u16)
+    try:
+        ins = [W.layer_inputs_numpy(wl, l, q_scale=8.0) for l in range(wl.n_layers)]
+        dev = [[from_u16(x, "cuda", wl.dtype) for x in t] for t in ins]
+        outs = [torch.full((wl.total_q, wl.n_q_heads, wl.head_dim), float("nan"), dtype=W.torch_dtype(wl),
+                           device="cuda") for _ in range(wl.n_layers)]
+        slots = [new_active(sc, wl) for _ in range(2)]
+        copy = torch.cuda.Stream()
+        flags = sc.SC_STACK_OVERLAP if mode == "overlap" else sc.SC_STACK_SERIAL
+        print(f"\n[chunked] {name} chunk {chunk} {mode}", flush=True)
+        sc.sc_prefill_stack_chunked(dp.handle, dp.table, [d[0].data_ptr() for d in dev],
+                                    [d[1].data_ptr() for d in dev], [d[2].data_ptr() for d in dev],
+                                    [o.data_ptr() for o in outs], [s[2] for s in slots], wl.n_q_heads, chunk,
+                                    flags, 0.0, torch.cuda.current_stream().cuda_stream, copy.cuda_stream)
+        torch.cuda.synchronize()
+        expect = pool_u16
+        for l in range(wl.n_layers):
+            q, kn, vn = ins[l]
+            *_, o_ref, _ = _oracle_layer(wl, pool_u16, l, q, kn, vn)
+            compare_attention(to_u16(outs[l]), o_ref, f"{name} chunk {chunk} layer {l}", wl.dtype)
+            expect = ok.store_layer(expect, wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, l, kn, vn)
+        assert np.array_equal(dp.full_u16(), expect)
+    finally:
+        dp.close()
+
+
 def test_capacity_and_layer_errors():
     sc = require_gpu()
     wl = W.config(1)

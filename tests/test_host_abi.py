@@ -136,6 +136,14 @@ def test_regular_cache_table_validation(sc, ids, cu, P, N, status):
         sc.sc_pool_destroy(p)
 
 
+def test_chunked_stack_rejects_bad_chunk(sc):
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_stack_chunked(FAKE_BASE, FAKE_BASE, [1], [1], [1], [1],
+                                    [sc.active(1, 1, 1), sc.active(1, 1, 1)], 8, 0)
+    assert e.value.status == sc.SC_ERR_INVALID
+    assert "chunk_tokens" in str(e.value)
+
+
 def test_attention_argument_validation(sc):
     with pytest.raises(sc.SwiftCacheError) as e:
         sc.sc_prefill_attn(1, 1, 1, 4, 4, 12, 8, 128, 1)
