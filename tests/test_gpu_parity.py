@@ -46,12 +46,19 @@ def _case(name):
         "f16_varlen": lambda: sw(122, [33, 0, 1000, 17], [5, 64, 1, 200], 2, 16, 4, 64, dtype="f16"),
         "f16_g5_split_rc": lambda: sw(123, [5000, 300], [40, 20], 1, 40, 8, 128, rc_fraction=0.5, dtype="f16"),
         "f16_host": lambda: sw(124, [200, 77], [20, 31], 1, 8, 2, 128, host_fraction=0.5, dtype="f16"),
+        # size extremes: largest block (with a regular cache), one-token
+        # blocks, many short sequences, the largest GQA group
+        "bs256_rc": lambda: sw(131, [700, 300], [30, 2], 1, 8, 2, 128, block_size=256, rc_fraction=0.5),
+        "bs1": lambda: sw(132, [50, 3], [9, 20], 1, 8, 8, 64, block_size=1),
+        "many_seqs": lambda: sw(133, list(range(0, 400, 10)), [1 + (7 * i) % 40 for i in range(40)], 1, 16, 4, 64),
+        "g16_d64": lambda: sw(134, [129], [100], 1, 32, 2, 64),
     }[name]()
 
 
 CASES = ["cfg1", "g4_d128_ragged", "g5_d128", "g1_d64_P0", "g4_split_long", "varlen_batch",
          "varlen_empty_turn", "host_tier", "g8_d64", "rc_varlen", "rc_split_d128", "rc_whole_prefix",
-         "rc_host", "f16_g4_d128_ragged", "f16_varlen", "f16_g5_split_rc", "f16_host"]
+         "rc_host", "f16_g4_d128_ragged", "f16_varlen", "f16_g5_split_rc", "f16_host", "bs256_rc", "bs1",
+         "many_seqs", "g16_d64"]
 
 
 def _oracle_layer(wl, pool_u16, layer, q, kn, vn):
@@ -273,6 +280,16 @@ def test_chunked_stack_matches_oracle(name, chunk, mode):
         assert np.array_equal(dp.full_u16(), expect)
     finally:
         dp.close()
+
+
+def test_sequence_beyond_32_bit_key_offsets_is_rejected():
+    """2^21 keys x 8 KV heads x 128 dims x 2 bytes = 4 GiB per sequence: the
+    kernel's 32-bit offsets cannot address it, so the call fails before
+    any launch (the buffers are never touched)."""
+    sc = require_gpu()
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn(16, 16, 16, 1 << 21, 1, 32, 8, 128, 16)
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED
 
 
 def test_capacity_and_layer_errors():
