@@ -10,7 +10,8 @@
 // the `group` query heads that share one KV head, and a range of keys.
 // Packing the heads of a group into the rows makes every K/V tile staged
 // through LDS serve all of them.  Long key ranges are split over several
-// workgroups (split-key): each writes a normalised fp32 partial output and
+// workgroups (split-key): each writes a normalised partial output (in the
+// element type; it is a convex combination of V rows) and
 // its log-sum-exp, and attn_merge_kernel combines them exactly
 // (o = sum_s exp(lse_s - lse) o_s).  The merge is a separate launch: merging
 // in the last-arriving workgroup would need device-scope fences, whose L2
@@ -128,6 +129,13 @@ struct Elem<SC_DTYPE_BF16> {
     const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p), one, acc, false);
   }
+  // Packed pair back to floats (exact).
+  static __device__ __forceinline__ f32x2 unpack(uint32_t p) {
+    f32x2 r;
+    r[0] = __builtin_bit_cast(float, p << 16);
+    r[1] = __builtin_bit_cast(float, p & 0xFFFF0000u);
+    return r;
+  }
 };
 
 template <>
@@ -147,6 +155,13 @@ struct Elem<SC_DTYPE_F16> {
   static __device__ __forceinline__ float add_pair(uint32_t p, float acc) {
     const f16x2 one = {(_Float16)1.0f, (_Float16)1.0f};
     return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, p), one, acc, false);
+  }
+  static __device__ __forceinline__ f32x2 unpack(uint32_t p) {
+    const f16x2 h = __builtin_bit_cast(f16x2, p);
+    f32x2 r;
+    r[0] = (float)h[0];
+    r[1] = (float)h[1];
+    return r;
   }
 };
 
@@ -533,18 +548,19 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
 
   // Split-key: write this split's normalised partial and its log-sum-exp.
   const int64_t prow = (int64_t)wi.split * a.total_q * a.n_q_heads + qrow;
-  float *po = a.part_o + prow * D;
+  // The partial is a convex combination of V rows, so it fits the element
+  // type's range; storing it in that type halves the split traffic for one
+  // extra rounding (2^-9 relative for bf16, 2^-11 for fp16).
+  uint16_t *po = a.part_o + prow * D;
 #pragma unroll
   for (int c = 0; c < D / 32; ++c)
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
       const int dim = 32 * c + 8 * g4 + 4 * half;
-      f32x4 x;
-      x[0] = w.oacc[c][4 * g4 + 0] * inv;
-      x[1] = w.oacc[c][4 * g4 + 1] * inv;
-      x[2] = w.oacc[c][4 * g4 + 2] * inv;
-      x[3] = w.oacc[c][4 * g4 + 3] * inv;
-      *reinterpret_cast<f32x4 *>(po + dim) = x;
+      u32x2 pk;
+      pk[0] = Elem<DT>::pack(w.oacc[c][4 * g4 + 0] * inv, w.oacc[c][4 * g4 + 1] * inv);
+      pk[1] = Elem<DT>::pack(w.oacc[c][4 * g4 + 2] * inv, w.oacc[c][4 * g4 + 3] * inv);
+      *reinterpret_cast<u32x2 *>(po + dim) = pk;
     }
   if (half == 0) a.part_lse[prow] = lse_val;
 }
@@ -593,25 +609,25 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   }
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
-  const float *po = a.part_o + row * D + sub * 8;
+  const uint16_t *po = a.part_o + row * D + sub * 8;
 #pragma unroll
   for (int s0 = 0; s0 < kAttnMaxSplits; s0 += 4) {
     if (s0 >= S) break;
-    f32x4 x[4][2];
+    u32x4 x[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      if (s0 + u < S) {
-        const f32x4 *p = reinterpret_cast<const f32x4 *>(po + (int64_t)(s0 + u) * rows * D);
-        x[u][0] = p[0];
-        x[u][1] = p[1];
-      }
+      if (s0 + u < S) x[u] = *reinterpret_cast<const u32x4 *>(po + (int64_t)(s0 + u) * rows * D);
 #pragma unroll
     for (int u = 0; u < 4; ++u)
       if (s0 + u < S) {
         const float wgt = ls[s0 + u] == -INFINITY ? 0.f : __expf(ls[s0 + u] - mx);
         wsum += wgt;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] += wgt * x[u][e >> 2][e & 3];
+        for (int e = 0; e < 4; ++e) {
+          const f32x2 v = Elem<DT>::unpack(x[u][e]);
+          acc[2 * e] += wgt * v[0];
+          acc[2 * e + 1] += wgt * v[1];
+        }
       }
   }
   const float winv = wsum > 0.f ? 1.f / wsum : 0.f;

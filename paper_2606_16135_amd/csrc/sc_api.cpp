@@ -381,10 +381,10 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
   if (plan.max_splits > 1) {
     const size_t rows = (size_t)plan.max_splits * plan.total_q * hq;
     void *ws = nullptr;
-    sc_status st = get_workspace(device, stream, rows * ((size_t)head_dim + 1) * sizeof(float), &ws);
+    sc_status st = get_workspace(device, stream, rows * ((size_t)head_dim * sizeof(uint16_t) + sizeof(float)), &ws);
     if (st != SC_OK) return st;
-    a.part_o = static_cast<float *>(ws);
-    a.part_lse = a.part_o + rows * head_dim;
+    a.part_o = static_cast<uint16_t *>(ws);
+    a.part_lse = reinterpret_cast<float *>(a.part_o + rows * head_dim);
   }
   if (plan.paged) {
     if (!rc.pool || !rc.ids || !rc.pool->rc_base)

@@ -104,7 +104,7 @@ struct AttnArgs {
   float *lse;             // nullable, [Hq][total_q]
   const WorkItem *items;
   const SeqDesc *seqs;
-  float *part_o;          // [max_splits][total_q][Hq][D] fp32, normalised partial outputs
+  uint16_t *part_o;       // [max_splits][total_q][Hq][D] normalised partial outputs, element type
   float *part_lse;        // [max_splits][total_q][Hq]
   int32_t n_seqs;
   int32_t total_q;
