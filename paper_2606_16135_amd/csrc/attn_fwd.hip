@@ -49,12 +49,15 @@
 // the exponent range, which the limit bounds.  No per-tile row max is
 // computed on the common path.
 //
-// K and V tiles each live in a 2-entry LDS ring (slot = tile parity).
-// Iteration j reads K(j+1) and V(j-1), writes K(j+2) and V(j) from registers
-// loaded in iteration j-1, loads K(j+3) and V(j+1), and ends with one
-// workgroup barrier that orders LDS only (global loads stay in flight
-// across it).  The loop is unrolled by two so that slots and score
-// registers are fixed at compile time.
+// K and V tiles each live in a 4-entry LDS ring (slot = tile mod 4).
+// Iteration j reads K(j+1) and V(j-1), writes K(j+3) and V(j+1) from
+// registers loaded in iteration j-1 and loads K(j+4) and V(j+2).  Because a
+// tile is written two iterations before it is read, only every second
+// iteration ends with a workgroup barrier (one that orders LDS only; global
+// loads stay in flight across it), which halves the barrier waits and lets
+// the waves drift apart by up to an iteration.  The loop is unrolled by two
+// so that the barrier placement and the score registers are fixed at
+// compile time.
 #include "sc_internal.h"
 
 #include <cmath>
@@ -98,7 +101,8 @@ struct Geo {
   static constexpr int kLdsV = D + 32;
   static constexpr int kTileK = KT * kLdsK;
   static constexpr int kTileV = KT * kLdsV;
-  static constexpr int kSmem = 2 * kTileK + 2 * kTileV;
+  static constexpr int kSlots = 4;   // ring entries per operand (K and V)
+  static constexpr int kSmem = kSlots * (kTileK + kTileV);
   static_assert(kChunksPerThread * kThreads == 2 * kTileChunks, "tile split");
 };
 
@@ -358,7 +362,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
     const int c = tid + kThreads * i - (is_v[i] ? G_::kTileChunks : 0);
     const int r = c / G_::kChunksPerRow, cc = c % G_::kChunksPerRow;
     voff[i] = (int)((r * kv_stride + cc * 8) * 2);
-    lds_off[i] = is_v[i] ? 2 * G_::kTileK + r * G_::kLdsV + cc * 8 : r * G_::kLdsK + cc * 8;
+    lds_off[i] = is_v[i] ? G_::kSlots * G_::kTileK + r * G_::kLdsV + cc * 8 : r * G_::kLdsK + cc * 8;
     crow[i] = r;
     ccol[i] = wi.kvh * D + cc * 8;
   }
@@ -389,7 +393,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
   };
   // A negative tile index (prologue only) skips that half of the pair.
   u32x4 lr[NCH];
-  auto stage_load = [&](int kj, int vj) {
+  auto stage_load = [&](u32x4 (&lr)[NCH], int kj, int vj) {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       const int t = is_v[i] ? vj : kj;
@@ -411,18 +415,20 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
       }
     }
   };
-  // par_k / par_v: ring slots (tile parity) the K and V chunks go to.
-  auto stage_store = [&](bool k_on, bool v_on, int par_k, int par_v) {
+  // kt / vt: the tiles the K and V chunks hold (ring slot = tile mod 4); a
+  // negative tile skips that half.
+  auto stage_store = [&](const u32x4 (&lr)[NCH], int kt, int vt) {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
-      if (is_v[i] ? v_on : k_on) {
-        const int slot_off = is_v[i] ? par_v * G_::kTileV : par_k * G_::kTileK;
+      const int t = is_v[i] ? vt : kt;
+      if (t >= 0) {
+        const int slot_off = is_v[i] ? (t & 3) * G_::kTileV : (t & 3) * G_::kTileK;
         *reinterpret_cast<u32x4 *>(smem + lds_off[i] + slot_off) = lr[i];
       }
     }
   };
-  auto slot_k = [&](int par) { return smem + par * G_::kTileK; };
-  auto slot_v = [&](int par) { return smem + 2 * G_::kTileK + par * G_::kTileV; };
+  auto slot_k = [&](int t) { return smem + (t & 3) * G_::kTileK; };
+  auto slot_v = [&](int t) { return smem + G_::kSlots * G_::kTileK + (t & 3) * G_::kTileV; };
 
   // First tile that needs the mask, the same for the whole workgroup: it
   // reaches past the key range or past the diagonal of the first query.
@@ -459,20 +465,28 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
   }
 
   if (n > 0 && !timed_out) {
-    // Prologue: K(0) into the ring, then QK(0); K(1) goes in and K(2), V(0)
-    // are loaded for iteration 0.
-    stage_load(0, -1);
-    stage_store(true, false, 0, 0);
-    stage_load(1, -1);
+    // Prologue: K(0), K(1), K(2) and V(0) into the rings (their loads in
+    // flight together), K(3) and V(1) loaded for iteration 0, then QK(0).
+    {
+      u32x4 lb[NCH], lc[NCH];
+      stage_load(lr, 0, 0);
+      stage_load(lb, 1, -1);
+      stage_load(lc, 2, -1);
+      stage_store(lr, 0, 0);
+      stage_store(lb, 1, -1);
+      stage_store(lc, 2, -1);
+      stage_load(lr, 3, 1);
+    }
     lds_barrier();
     qk_tile<D, DT>(slot_k(0), w.qf, w.s[0], lane);
-    stage_store(true, false, 1, 0);
-    stage_load(2, 0);
-    lds_barrier();
 
     // Iteration j (tile parity PAR): QK(j+1) and PV(j-1) on the MFMA pipe,
-    // softmax(j) on the VALU, then K(j+2), V(j) into the ring and K(j+3),
-    // V(j+1) from memory.  Tile j's scores live in s[PAR].
+    // softmax(j) on the VALU, then K(j+3), V(j+1) into the rings and K(j+4),
+    // V(j+2) from memory.  Tile j's scores live in s[PAR].  The rings hold
+    // four tiles, so a workgroup barrier is needed only after even
+    // iterations: the two iterations between barriers read K(j+1), V(j-1)
+    // written at least one barrier earlier and write the two slots read
+    // last before that barrier.
     auto iterate = [&](auto par_tag, auto mask_tag, auto qk_tag, auto pv_tag, auto first_tag, int j) {
       constexpr int PAR = decltype(par_tag)::value;
       constexpr bool kMask = decltype(mask_tag)::value;
@@ -482,8 +496,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
       __builtin_assume(j >= 0);
       f32x16 &sc = w.s[PAR];
       u32x4 pf[2];
-      if (kQk) qk_tile<D, DT>(slot_k(PAR ^ 1), w.qf, w.s[PAR ^ 1], lane);
-      if (kPv) pv_tile<D, DT>(slot_v(PAR ^ 1), w.pf_prev, w.oacc, lane);
+      if (kQk) qk_tile<D, DT>(slot_k(j + 1), w.qf, w.s[PAR ^ 1], lane);
+      if (kPv) pv_tile<D, DT>(slot_v(j - 1), w.pf_prev, w.oacc, lane);
       if (kMask) apply_mask(sc, lim_of(j));
       if (kFirst) {
         const float tm = tile_max(sc, sl2);
@@ -492,9 +506,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
       float rs = softmax_tile<DT>(sc, pf, sl2, w.m_run);
       if (!kFirst && __builtin_amdgcn_ballot_w64(!(rs <= Elem<DT>::kSumLimit))) rs = settle_max<D, DT>(w, sc, pf, sl2);
       w.l_run += rs;
-      stage_store(true, true, PAR, PAR);
-      stage_load(j + 3, j + 1);
-      lds_barrier();
+      stage_store(lr, j + 3, j + 1);
+      stage_load(lr, j + 4, j + 2);
+      if (PAR == 0) lds_barrier();
       w.pf_prev[0] = pf[0];
       w.pf_prev[1] = pf[1];
     };
@@ -517,11 +531,13 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
     };
     steady(F(), min(j_mask, n - 1));
     steady(T(), n - 1);
-    // j = n - 1: PV(n-2) and softmax(n-1), then drain PV(n-1).
+    // j = n - 1: PV(n-2) and softmax(n-1), then drain PV(n-1) (V(n-1) was
+    // written in iteration n-2; whichever of n-2, n-1 is even ended with a
+    // barrier).
     if (n >= 2) {
       if ((n - 1) & 1) iterate(P1(), T(), F(), T(), F(), n - 1); else iterate(P0(), T(), F(), T(), F(), n - 1);
     }
-    pv_tile<D, DT>(slot_v((n - 1) & 1), w.pf_prev, w.oacc, lane);
+    pv_tile<D, DT>(slot_v(n - 1), w.pf_prev, w.oacc, lane);
   }
 
   // Combine the two halves' denominators and normalise.

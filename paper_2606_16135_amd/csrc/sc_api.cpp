@@ -542,9 +542,13 @@ size_t copy_lds_reserve(int device, int head_dim) {
   if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device) == hipSuccess &&
       hipDeviceGetAttribute(&lds_block, hipDeviceAttributeMaxSharedMemoryPerBlock, device) == hipSuccess &&
       lds_cu > 0) {
-    const size_t cand = ((size_t)lds_cu / (kCopyBesideAttn + 1) + 1024 + 255) & ~(size_t)255;
-    if (cand <= (size_t)lds_block && kCopyBesideAttn * cand + attn_fwd_lds_bytes(head_dim) <= (size_t)lds_cu)
-      r = cand;
+    // kCopyBesideAttn of these fit in the LDS an attention workgroup leaves
+    // free, one more does not.
+    const size_t attn = attn_fwd_lds_bytes(head_dim);
+    if (attn < (size_t)lds_cu) {
+      const size_t cand = (((size_t)lds_cu - attn) / (kCopyBesideAttn + 1) + 1024 + 255) & ~(size_t)255;
+      if (cand <= (size_t)lds_block && kCopyBesideAttn * cand + attn <= (size_t)lds_cu) r = cand;
+    }
   }
   g_reserve[key] = r;
   return r;
