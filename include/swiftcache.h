@@ -289,10 +289,10 @@ sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layer
 
 /*
  * The same layer stack with the new turn processed in chunks of at most
- * chunk_tokens tokens per sequence (§8 names chunking the new turn for very
- * long N): each layer's slot is fetched and appended once, then attention
- * runs one launch per chunk c over that same slot, chunk c's queries
- * (new tokens [c*C, min(N_b, (c+1)*C)) of each sequence) seeing the prefix
+ * chunk_tokens tokens per sequence, for very long new turns (the paper does
+ * not describe chunking): each layer's slot is fetched and appended once,
+ * then attention runs one launch per chunk c over that same slot, chunk c's
+ * queries (new tokens [c*C, min(N_b, (c+1)*C)) of each sequence) seeing the prefix
  * and the earlier chunks.  The result equals sc_prefill_stack's (same
  * definition; only the rounding order of the split-key merge differs);
  * chunking bounds the split-key workspace and the length of any single
