@@ -10,11 +10,16 @@
 // the active buffer, so each item is one contiguous range on both sides.
 //
 // HBM-bound: every lane moves 16-byte chunks with kUnroll loads in flight
-// before the matching stores.  Both sides are streamed once per call, so
-// loads and stores are non-temporal and do not evict the attention's K/V
-// working set from L2 (measured on MI355X: about 6% faster than cached
-// stores for the fetch pattern).  Host-tier blocks are read or written
-// through their device-visible pinned mapping, over the host link.
+// before the matching stores, through buffer resources over the item's two
+// ranges.  Both sides are streamed once per call: the loads are
+// system-coherent and non-temporal (sc0 sc1 nt: no cache keeps the source),
+// the stores non-temporal (nt), so neither evicts the attention's K/V
+// working set from L2.  Measured on MI355X against non-temporal loads, the
+// fetch of the 8B shape runs about 7% faster (11.9 vs 12.8 us per layer);
+// against cached stores, non-temporal stores about 6% faster.  The data a
+// copy reads was written by earlier kernels, whose completion wrote it back
+// beyond the caches.  Host-tier blocks are read or written through their
+// device-visible pinned mapping, over the host link.
 #include "sc_internal.h"
 
 namespace sc {
@@ -22,6 +27,9 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kUnroll = 8;
+// Buffer instruction cache-policy bits on gfx950: sc0 = 1, nt = 2, sc1 = 16.
+constexpr int kLoadPolicy = 1 | 2 | 16;
+constexpr int kStorePolicy = 2;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
@@ -44,19 +52,24 @@ __device__ __forceinline__ void copy_rows(const CopyArgs &a) {
     src = (is_v ? a.new_v : a.new_k) + it.src_row * a.row_bytes;
     dst = a.tier_base[it.tier] + it.pool_off + a.layer_off + half_off;
   }
-  const u32x4 *s = reinterpret_cast<const u32x4 *>(src);
-  u32x4 *d = reinterpret_cast<u32x4 *>(dst);
+  // One item is at most 256 rows of one KV layer (under 4 MiB), so 32-bit
+  // byte offsets cover it.
+  const int bytes = (int)(nchunks * 16);
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(src), (short)0, bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(dst, (short)0, bytes, 0x00020000);
   for (int64_t base = 0; base < nchunks; base += (int64_t)kThreads * kUnroll) {
     u32x4 r[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t idx = base + u * kThreads + threadIdx.x;
-      if (idx < nchunks) r[u] = __builtin_nontemporal_load(s + idx);
+      if (idx < nchunks)
+        r[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(idx * 16), 0, kLoadPolicy));
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t idx = base + u * kThreads + threadIdx.x;
-      if (idx < nchunks) __builtin_nontemporal_store(r[u], d + idx);
+      if (idx < nchunks) __builtin_amdgcn_raw_buffer_store_b128(r[u], rd, (int)(idx * 16), 0, kStorePolicy);
     }
   }
 }

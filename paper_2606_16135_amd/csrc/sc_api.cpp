@@ -657,6 +657,11 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
     return fail(SC_ERR_INVALID, "invalid pool description");
   if (d.head_dim != 64 && d.head_dim != 128)
     return fail(SC_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", d.head_dim);
+  // The copy kernels address one block's K (or V) rows of a layer with
+  // 32-bit byte offsets.
+  if ((int64_t)d.block_size * d.n_kv_heads * d.head_dim * 2 >= ((int64_t)1 << 31))
+    return fail(SC_ERR_UNSUPPORTED, "block_size x n_kv_heads x head_dim too large (%d x %d x %d)", d.block_size,
+                d.n_kv_heads, d.head_dim);
   if (d.n_device_blocks + d.n_host_blocks + d.n_rc_blocks > INT32_MAX)
     return fail(SC_ERR_RANGE, "too many blocks for 32-bit block ids");
   // Attention pages regular-cache keys in groups of up to 8 rows that must

@@ -57,6 +57,13 @@ def test_pool_validation(sc):
     assert e.value.status == sc.SC_ERR_INVALID
 
 
+def test_pool_rejects_blocks_beyond_32_bit_offsets(sc):
+    # 256 tokens x 2^16 KV heads x 128 dims x 2 bytes = 4 GiB of K per block and layer
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_pool_create(1, 1 << 16, 128, 256, 8, 0, 0, FAKE_BASE, 0)
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED
+
+
 def test_pool_element_type(sc):
     with pytest.raises(sc.SwiftCacheError) as e:
         sc.sc_pool_create(2, 2, 64, 16, 8, 0, 0, FAKE_BASE, 0, dtype=2)
