@@ -5,7 +5,8 @@
 // All three move whole token rows (n_kv_heads * head_dim bf16 = row_bytes)
 // between a block of the block-major pool (§3.4) and a packed buffer, so one
 // body serves them: workgroup 2*i copies item i's K rows, workgroup 2*i+1
-// its V rows.  A block slice of one layer is contiguous in the pool (K half
+// its V rows (a grid capped below 2 * n_items, as the overlapped layer stack
+// launches it beside attention, strides over the item halves).  A block slice of one layer is contiguous in the pool (K half
 // then V half, Eq. 1), and consecutive rows of a sequence are contiguous in
 // the active buffer, so each item is one contiguous range on both sides.
 //
@@ -34,9 +35,9 @@ constexpr int kStorePolicy = 2;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 template <int MODE>
-__device__ __forceinline__ void copy_rows(const CopyArgs &a) {
-  const int item_idx = blockIdx.x >> 1;
-  const int is_v = blockIdx.x & 1;
+__device__ __forceinline__ void copy_rows(const CopyArgs &a, int g) {
+  const int item_idx = g >> 1;
+  const int is_v = g & 1;
   const CopyItem it = a.items[item_idx];
   const int64_t nchunks = ((int64_t)it.nrows * a.row_bytes) >> 4;
   const int64_t half_off = is_v ? a.v_half_off : 0;
@@ -75,9 +76,15 @@ __device__ __forceinline__ void copy_rows(const CopyArgs &a) {
 }
 
 // One kernel symbol per direction, so that profiles tell them apart.
-__global__ __launch_bounds__(kThreads) void kv_fetch_kernel(CopyArgs a) { copy_rows<COPY_FETCH>(a); }
-__global__ __launch_bounds__(kThreads) void kv_append_kernel(CopyArgs a) { copy_rows<COPY_APPEND>(a); }
-__global__ __launch_bounds__(kThreads) void kv_store_kernel(CopyArgs a) { copy_rows<COPY_STORE>(a); }
+// Workgroup g copies half g & 1 of item g >> 1; a grid smaller than
+// 2 * n_items walks the halves with a stride of the grid size.
+template <int MODE>
+__device__ __forceinline__ void copy_all(const CopyArgs &a) {
+  for (int g = blockIdx.x; g < 2 * a.n_items; g += gridDim.x) copy_rows<MODE>(a, g);
+}
+__global__ __launch_bounds__(kThreads) void kv_fetch_kernel(CopyArgs a) { copy_all<COPY_FETCH>(a); }
+__global__ __launch_bounds__(kThreads) void kv_append_kernel(CopyArgs a) { copy_all<COPY_APPEND>(a); }
+__global__ __launch_bounds__(kThreads) void kv_store_kernel(CopyArgs a) { copy_all<COPY_STORE>(a); }
 
 }  // namespace
 
@@ -92,9 +99,10 @@ int kv_copy_vgprs() {
   return m;
 }
 
-hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_reserve) {
+hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_reserve, int max_groups) {
   if (a.n_items <= 0) return hipSuccess;
-  const dim3 grid(2 * a.n_items), block(kThreads);
+  const int groups = max_groups > 0 && max_groups < 2 * a.n_items ? max_groups : 2 * a.n_items;
+  const dim3 grid(groups), block(kThreads);
   if (a.mode == COPY_FETCH)
     hipLaunchKernelGGL(kv_fetch_kernel, grid, block, lds_reserve, stream, a);
   else if (a.mode == COPY_APPEND)

@@ -554,6 +554,36 @@ size_t copy_lds_reserve(int device, int head_dim) {
   return r;
 }
 
+// Width of the copy grids beside attention.  Every copy workgroup that
+// shares a CU with attention slows that CU's attention waves (issue slots,
+// the vector memory path), so the overlapped stack launches the fewest
+// copy workgroups that still finish a layer's fetch, append and store in
+// about half of the attention they hide behind; they then loop over the
+// items.  Measured on the 8B shape (32 MiB fetched per layer beside ~84 us
+// of attention): 1024 workgroups (one per item half) cost 10-11% over
+// attention alone, 256 cost 8.6%, 128 cost 7.4%, 64 cost 17% (the copies
+// no longer finish in time).  A copy workgroup beside attention moves about
+// kCopyGroupBps; attention runs at about kAttnFlops.  Never fewer than half
+// the CUs, never more than the items need.
+constexpr double kCopyGroupBps = 6.5e9;
+constexpr double kAttnFlops = 0.9e15;
+
+int copy_groups_beside_attention(int device, const sc_table *t, int n_q_heads, int head_dim) {
+  double pairs = 0.0;
+  for (int32_t b = 0; b < t->batch; ++b)
+    pairs += (double)t->N[b] * t->P[b] + 0.5 * (double)t->N[b] * (t->N[b] + 1);
+  const double flops = 4.0 * head_dim * n_q_heads * pairs;
+  int64_t rows = 0;
+  for (const CopyItem &it : t->h_items) rows += it.nrows;
+  const double bytes = 2.0 * (double)rows * (double)t->pool->row_bytes;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || cus <= 0) return 0;
+  if (flops <= 0.0) return 0;
+  const double need = 2.0 * bytes * kAttnFlops / (kCopyGroupBps * flops);
+  if (need > 1e9) return 0;
+  return std::max(cus / 2, (int)std::ceil(need));
+}
+
 CopyArgs copy_args(const sc_pool *p, const sc_table *t, int mode) {
   CopyArgs a{};
   a.mode = mode;
@@ -584,33 +614,33 @@ sc_status check_active(const sc_table *t, const sc_active *dst) {
 }
 
 sc_status do_fetch(sc_pool *p, const sc_table *t, int layer, const sc_active *dst, hipStream_t s,
-                   size_t lds_reserve = 0) {
+                   size_t lds_reserve = 0, int max_groups = 0) {
   CopyArgs a = copy_args(p, t, COPY_FETCH);
   a.layer_off = (int64_t)layer * (int64_t)p->slice_bytes;
   a.act_k = static_cast<char *>(dst->k);
   a.act_v = static_cast<char *>(dst->v);
-  hipError_t e = launch_kv_copy(a, s, lds_reserve);
+  hipError_t e = launch_kv_copy(a, s, lds_reserve, max_groups);
   return e == hipSuccess ? SC_OK : fail_hip(e, "fetch launch");
 }
 
 sc_status do_append(sc_pool *p, const sc_table *t, const void *kn, const void *vn, const sc_active *dst,
-                    hipStream_t s, size_t lds_reserve = 0) {
+                    hipStream_t s, size_t lds_reserve = 0, int max_groups = 0) {
   CopyArgs a = copy_args(p, t, COPY_APPEND);
   a.new_k = static_cast<const char *>(kn);
   a.new_v = static_cast<const char *>(vn);
   a.act_k = static_cast<char *>(dst->k);
   a.act_v = static_cast<char *>(dst->v);
-  hipError_t e = launch_kv_copy(a, s, lds_reserve);
+  hipError_t e = launch_kv_copy(a, s, lds_reserve, max_groups);
   return e == hipSuccess ? SC_OK : fail_hip(e, "append launch");
 }
 
 sc_status do_store(sc_pool *p, const sc_table *t, int layer, const void *kn, const void *vn, hipStream_t s,
-                   size_t lds_reserve = 0) {
+                   size_t lds_reserve = 0, int max_groups = 0) {
   CopyArgs a = copy_args(p, t, COPY_STORE);
   a.layer_off = (int64_t)layer * (int64_t)p->slice_bytes;
   a.new_k = static_cast<const char *>(kn);
   a.new_v = static_cast<const char *>(vn);
-  hipError_t e = launch_kv_copy(a, s, lds_reserve);
+  hipError_t e = launch_kv_copy(a, s, lds_reserve, max_groups);
   return e == hipSuccess ? SC_OK : fail_hip(e, "store launch");
 }
 
@@ -1195,6 +1225,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   hipEvent_t *ready = ev, *free_ = ev + 2, start = ev[4], done = ev[5];
   // Host-tier fetches already run on their own CUs (split streams).
   const size_t reserve = ss ? 0 : copy_lds_reserve(d.device, d.head_dim);
+  const int groups = ss ? 0 : copy_groups_beside_attention(d.device, table, n_q_heads, d.head_dim);
   auto body = [&]() -> sc_status {
     // Both streams start after everything already queued on the caller's
     // compute stream.
@@ -1205,15 +1236,17 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
       const int s = l & 1;
       if (l >= 2) SC_HIP(hipStreamWaitEvent(xs, free_[s], 0));
       sc_status r;
-      if ((r = do_fetch(pool, table, l, &slots[s], xs, reserve)) != SC_OK) return r;
-      if ((r = do_append(pool, table, knew_per_layer[l], vnew_per_layer[l], &slots[s], xs, reserve)) != SC_OK)
+      if ((r = do_fetch(pool, table, l, &slots[s], xs, reserve, groups)) != SC_OK) return r;
+      if ((r = do_append(pool, table, knew_per_layer[l], vnew_per_layer[l], &slots[s], xs, reserve, groups)) !=
+          SC_OK)
         return r;
       if (device_wait) {
         SC_HIP(hipStreamWriteValue64(xs, sync, base + l + 1, 0));
       } else {
         SC_HIP(hipEventRecord(ready[s], xs));
       }
-      if (do_st && (r = do_store(pool, table, l, knew_per_layer[l], vnew_per_layer[l], xs, reserve)) != SC_OK)
+      if (do_st &&
+          (r = do_store(pool, table, l, knew_per_layer[l], vnew_per_layer[l], xs, reserve, groups)) != SC_OK)
         return r;
       if (device_wait) {
         if ((r = attn(l, slots[s], sync, base + l + 1, free_[s])) != SC_OK) return r;

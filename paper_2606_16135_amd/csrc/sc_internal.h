@@ -64,7 +64,8 @@ struct CopyArgs {
 
 // lds_reserve: bytes of LDS each copy workgroup reserves without using them
 // (limits how many copy workgroups share a CU with attention; 0 = none).
-hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_reserve = 0);
+// max_groups > 0 caps the grid; the workgroups then loop over the items.
+hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_reserve = 0, int max_groups = 0);
 
 // ---------------------------------------------------------------------------
 // Attention work decomposition
