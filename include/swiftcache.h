@@ -13,7 +13,9 @@
  *
  * Conventions shared by every call
  * --------------------------------
- *  - Element type of every KV, q and output tensor: bf16 (raw 16-bit).
+ *  - Element type of every KV, q and output tensor: the pool's sc_dtype,
+ *    bf16 by default or IEEE fp16 (raw 16-bit patterns either way);
+ *    sc_prefill_attn is bf16, sc_prefill_attn_f16 its fp16 twin.
  *  - Device pointers are HIP device addresses on the pool's device.  Host
  *    arrays (block tables, lengths) are read synchronously during the call
  *    and may be freed when it returns.
@@ -68,7 +70,8 @@ typedef struct sc_table sc_table;   /* opaque, library-owned */
 
 /*
  * Donor pool description.  Eq. 1 (§3.2) gives the bytes of one block of one
- * layer: slice_bytes = 2 * block_size * n_kv_heads * head_dim * 2 (bf16).
+ * layer: slice_bytes = 2 * block_size * n_kv_heads * head_dim * 2 (16-bit
+ * elements).
  * Block-major layout (§3.4), with Eq. 1's K/V factor made explicit and the
  * K half first:
  *     pool[n_blocks][n_layers][2][block_size][n_kv_heads][head_dim]
