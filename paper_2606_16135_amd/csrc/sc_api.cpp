@@ -1213,9 +1213,16 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
     base = t->sync_gen;
     t->sync_gen += (uint64_t)n_layers + 1;
   }
+  // free_[s] only orders a write after a read of slot s (the next fetch into
+  // it after the forward kernel that read it); no data flows through it, so
+  // it is recorded without the system-scope release, whose cache write-back
+  // (the split-key partials the forward kernel just wrote) measured ~7 us
+  // between every forward kernel and its merge.
   hipEvent_t ev[6] = {};
-  for (auto &e : ev) {
-    hipError_t he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+  for (int i = 0; i < 6; ++i) {
+    const bool war_only = i == 2 || i == 3;
+    hipError_t he = hipEventCreateWithFlags(
+        &ev[i], war_only ? (hipEventDisableTiming | hipEventDisableSystemFence) : hipEventDisableTiming);
     if (he != hipSuccess) {
       for (auto &x : ev)
         if (x) (void)hipEventDestroy(x);
