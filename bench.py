@@ -17,7 +17,8 @@ Prints one JSON line.  `value` = new-turn tokens per second through the
 whole stack.  `roofline` is for the attention kernel (MFMA-bound), timed
 with HIP events on its own stream; `details` adds the fetch kernel's HBM
 bandwidth, the attention-only and serial stack times, and the overlap
-overhead.  `cpu_baseline` times the CPU oracle on a bounded sample of the
+overhead, plus a plain 1 GiB device-to-device copy's bandwidth as context
+for the fetch.  `cpu_baseline` times the CPU oracle on a bounded sample of the
 same workload (a few layers, extrapolated to the stack).
 """
 
@@ -224,6 +225,22 @@ def main():
     t_fetch = f0.elapsed_time(f1) / (reps * L) * 1e-3          # seconds per layer
     fetch_gbs = 2.0 * fetch_payload_bytes(wl) / t_fetch / 1e9
 
+    # Context for the fetch: a plain contiguous 1 GiB device-to-device copy
+    # (torch copy_, the runtime's copy kernel) on the same stream, read +
+    # write bytes per second.
+    csrc = torch.empty(1 << 29, dtype=torch.int16, device="cuda").fill_(1)
+    cdst = torch.empty_like(csrc)
+    with torch.cuda.stream(copy):
+        cdst.copy_(csrc)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record(copy)
+        for _ in range(5):
+            cdst.copy_(csrc)
+        c1.record(copy)
+    torch.cuda.synchronize()
+    copy_gbs = 2.0 * csrc.numel() * 2 * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del csrc, cdst
+
     flops = attention_flops(wl)
     t_attn_layer = t_attn_only / L * 1e-3
     achieved_tflops = flops / t_attn_layer / 1e12
@@ -253,6 +270,7 @@ def main():
                      "serial": round(t_serial, 3)},
         "overlap_overhead": round(t_overlap / t_attn_only - 1.0, 4),
         "fetch": {"us_per_layer": round(t_fetch * 1e6, 2), "hbm_gbs": round(fetch_gbs, 1),
+                  "device_copy_1gib_gbs": round(copy_gbs, 1),
                   "frac_of_hbm_peak": round(fetch_gbs / HBM_PEAK_GBS, 4),
                   "payload_bytes_per_layer": fetch_payload_bytes(wl)},
         "elastic": elastic,
