@@ -276,13 +276,20 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
  * only, over whatever the slots hold: the reference point for the overlap
  * overhead), optionally | SC_STACK_NO_STORE.  `copy` may be NULL unless
  * SC_STACK_OVERLAP is set.
+ * SC_STACK_TEST_NEVER_READY (with SC_STACK_OVERLAP only, for tests of the
+ * failure path): every attention kernel waits for a slot count the copy
+ * stream never reaches and gives up after a few hundred polls, so its rows
+ * come out NaN and sc_table_stack_status reports the time-out; every kernel
+ * still exits.  SC_ERR_UNSUPPORTED if this stack would use the stream-level
+ * wait (no device-side wait to time out).
  */
 enum {
   SC_STACK_OVERLAP = 0,
   SC_STACK_SERIAL = 1,
   SC_STACK_ATTN_ONLY = 2,
   SC_STACK_MODE_MASK = 3,
-  SC_STACK_NO_STORE = 4
+  SC_STACK_NO_STORE = 4,
+  SC_STACK_TEST_NEVER_READY = 8
 };
 sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers,
                            const void *const *q_per_layer, const void *const *knew_per_layer,
@@ -418,6 +425,16 @@ sc_status sc_scale_down(int64_t worker_blocks, int32_t worker_block_size, int64_
                         int64_t *worker_delta, int64_t *master_delta);
 
 /* Message of the last failed call on this thread ("" if none). */
+/*
+ * Whether an attention workgroup of an overlapped stack on this table gave
+ * up its device-side wait for a slot (and wrote NaN rows) since the table
+ * was created or the flag was last cleared.  Reads device memory
+ * synchronously: call it only after the streams passed to the stack have
+ * been synchronised.  *timed_out = 0 or 1; clear != 0 resets the flag.
+ * A table that never ran an overlapped stack reports 0.
+ */
+sc_status sc_table_stack_status(const sc_table *table, int32_t *timed_out, int32_t clear);
+
 const char *sc_last_error(void);
 
 /* Library version string. */

@@ -80,8 +80,6 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 constexpr int kThreads = 512;            // 8 waves, 2 per SIMD
 constexpr int KT = kAttnKeyTile;
-// Polls of the ready flag before a workgroup gives up (about a second).
-constexpr int kReadySpinLimit = 1 << 22;
 static_assert(kAttnRows == 8 * 32, "eight waves of 32 rows");
 static_assert(KT == 32, "one 32-key MFMA block per tile");
 
@@ -451,7 +449,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
     if (tid == 0) {
       int spins = 0, late = 0;
       while (__hip_atomic_load(a.ready_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < a.ready_value) {
-        if (++spins > kReadySpinLimit) {
+        if (++spins > a.ready_spin_limit) {
           late = 1;
           __hip_atomic_store(a.ready_timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           break;

@@ -353,7 +353,8 @@ struct RcView {
 sc_status run_attention(int device, const AttnPlan &plan, const void *q, const void *k, const void *v,
                         void *out, float *lse, int hq, int hkv, int head_dim, int dtype, float scale,
                         hipStream_t stream, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
-                        hipEvent_t after_fwd = nullptr, const RcView &rc = RcView()) {
+                        hipEvent_t after_fwd = nullptr, const RcView &rc = RcView(),
+                        int spin_limit = kAttnReadySpinLimit) {
   if (plan.n_items == 0) return SC_OK;
   // The kernel addresses one sequence's rows of one KV head with 32-bit
   // byte offsets.
@@ -403,6 +404,7 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
     a.ready_flag = ready_flag;
     a.ready_value = ready_value;
     a.ready_timeout = reinterpret_cast<uint32_t *>(const_cast<uint64_t *>(ready_flag + 1));
+    a.ready_spin_limit = spin_limit;
   }
   hipError_t e = launch_attn_fwd(a, head_dim, plan.n_items, stream);
   if (e != hipSuccess) return fail_hip(e, "attn_fwd launch");
@@ -1026,6 +1028,22 @@ sc_status sc_table_totals(const sc_table *table, int64_t *total_q, int64_t *tota
   return SC_OK;
 }
 
+sc_status sc_table_stack_status(const sc_table *table, int32_t *timed_out, int32_t clear) {
+  clear_error();
+  if (!table || !timed_out) return fail(SC_ERR_INVALID, "null argument");
+  *timed_out = 0;
+  if (!table->d_sync) return SC_OK;
+  sc::DeviceGuard guard(table->pool->desc.device);
+  uint64_t flag = 0;
+  SC_HIP(hipMemcpy(&flag, table->d_sync + 1, sizeof(flag), hipMemcpyDeviceToHost));
+  *timed_out = flag != 0 ? 1 : 0;
+  if (clear && flag != 0) {
+    const uint64_t zero = 0;
+    SC_HIP(hipMemcpy(table->d_sync + 1, &zero, sizeof(zero), hipMemcpyHostToDevice));
+  }
+  return SC_OK;
+}
+
 sc_status sc_fetch_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer, const sc_active *dst,
                             void *stream) {
   clear_error();
@@ -1119,9 +1137,13 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
   if (n_layers <= 0 || n_layers > pool->desc.n_layers)
     return fail(SC_ERR_RANGE, "n_layers %d outside [1, %d]", n_layers, pool->desc.n_layers);
-  if (flags & ~(uint32_t)(SC_STACK_MODE_MASK | SC_STACK_NO_STORE)) return fail(SC_ERR_INVALID, "unknown flags");
+  if (flags & ~(uint32_t)(SC_STACK_MODE_MASK | SC_STACK_NO_STORE | SC_STACK_TEST_NEVER_READY))
+    return fail(SC_ERR_INVALID, "unknown flags");
   const uint32_t mode = flags & SC_STACK_MODE_MASK;
   if (mode > SC_STACK_ATTN_ONLY) return fail(SC_ERR_INVALID, "unknown stack mode");
+  const bool never_ready = (flags & SC_STACK_TEST_NEVER_READY) != 0;
+  if (never_ready && mode != SC_STACK_OVERLAP)
+    return fail(SC_ERR_INVALID, "SC_STACK_TEST_NEVER_READY needs SC_STACK_OVERLAP");
   const bool do_st = !(flags & SC_STACK_NO_STORE);
   const int n_slots = mode == SC_STACK_SERIAL ? 1 : 2;
   for (int s = 0; s < n_slots; ++s) {
@@ -1162,14 +1184,18 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   hipStream_t xs = ss ? ss->copy : (hipStream_t)copy_stream;
   // The first chunk waits for the slot; the slot-free event follows the
   // last chunk's forward kernel.
+  // A forced time-out (tests of the failure path) waits for a count the
+  // copy stream never reaches, with a spin limit of a few hundred polls.
+  const uint64_t never = never_ready ? (uint64_t)1 << 40 : 0;
+  const int spin_limit = never_ready ? kAttnTestSpinLimit : kAttnReadySpinLimit;
   auto attn = [&](int l, const sc_active &slot, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
                   hipEvent_t after_fwd = nullptr) {
     RcView rc{pool, l, table->d_rc_ids};
     for (int c = 0; c < n_chunks; ++c) {
       sc_status r = run_attention(d.device, *plans[c], q_per_layer[l], slot.k, slot.v, out_per_layer[l], nullptr,
                                   n_q_heads, d.n_kv_heads, d.head_dim, d.dtype, scale, cs,
-                                  c == 0 ? ready_flag : nullptr, ready_value,
-                                  c == n_chunks - 1 ? after_fwd : nullptr, rc);
+                                  c == 0 ? ready_flag : nullptr, ready_value + (ready_flag ? never : 0),
+                                  c == n_chunks - 1 ? after_fwd : nullptr, rc, spin_limit);
       if (r != SC_OK) return r;
     }
     return SC_OK;
@@ -1200,6 +1226,8 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   // (attention of the layer that last used slot s has read it).
   // Disjoint CU sets (host tier) never block each other.
   const bool device_wait = ss != nullptr || copy_fits_beside_attention(d.head_dim);
+  if (never_ready && !device_wait)
+    return fail(SC_ERR_UNSUPPORTED, "this stack waits on stream events; there is no device wait to time out");
   uint64_t *sync = nullptr, base = 0;
   if (device_wait) {
     std::lock_guard<std::mutex> lk(const_cast<sc_table *>(table)->mu);

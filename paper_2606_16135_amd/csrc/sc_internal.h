@@ -117,11 +117,12 @@ struct AttnArgs {
   float scale_log2;       // softmax scale * log2(e)
   // Optional device-side dependency (overlapped layer stack): before reading
   // K/V, each workgroup waits until *ready_flag >= ready_value, polling at
-  // most kReadySpinLimit times; on time-out it sets *ready_timeout and
+  // most ready_spin_limit times; on time-out it sets *ready_timeout and
   // writes NaN rows instead of results.  ready_flag == nullptr: no wait.
   const uint64_t *ready_flag;
   uint64_t ready_value;
   uint32_t *ready_timeout;
+  int32_t ready_spin_limit;
   // Regular cache (paged items): block i of sequence s is local block
   // rc_ids[seqs[s].rc_off + i] of the tier at rc_base, whose layer-l K rows
   // start at rc_base + id * rc_block_elems + rc_layer_elems (V rows
@@ -138,6 +139,10 @@ struct AttnArgs {
 constexpr int kAttnRows = 256;   // (query, head) rows per workgroup
 constexpr int kAttnKeyTile = 32; // keys per LDS tile
 constexpr int kAttnMaxSplits = 16; // key splits per sequence (merge kernel bound)
+// Polls of the ready flag before an attention workgroup gives up (about a
+// second), and the limit a forced time-out uses.
+constexpr int kAttnReadySpinLimit = 1 << 22;
+constexpr int kAttnTestSpinLimit = 256;
 
 hipError_t launch_attn_fwd(const AttnArgs &a, int head_dim, int n_items, hipStream_t stream);
 size_t attn_fwd_lds_bytes(int head_dim);

@@ -34,10 +34,11 @@ SC_STACK_OVERLAP = 0
 SC_STACK_SERIAL = 1
 SC_STACK_ATTN_ONLY = 2
 SC_STACK_NO_STORE = 4
+SC_STACK_TEST_NEVER_READY = 8
 
 EXPORTED = [
     "sc_pool_create", "sc_pool_destroy", "sc_pool_layout_get", "sc_table_create",
-    "sc_table_destroy", "sc_table_totals", "sc_fetch_layer_kv", "sc_append_new_kv",
+    "sc_table_destroy", "sc_table_totals", "sc_table_stack_status", "sc_fetch_layer_kv", "sc_append_new_kv",
     "sc_prefill_attn", "sc_prefill_attn_f16", "sc_prefill_attn_varlen", "sc_store_layer_kv",
     "sc_prefill_stack", "sc_prefill_stack_chunked", "sc_attn_plan_query", "sc_pool_resize", "sc_plan_capacity", "sc_elastic_unit", "sc_scale_up",
     "sc_scale_down", "sc_last_error", "sc_version",
@@ -105,6 +106,7 @@ def load():
         "sc_table_create": (I32, [P, I32, i32p, i32p, i32p, i32p, VP, ctypes.POINTER(P)]),
         "sc_table_destroy": (None, [P]),
         "sc_table_totals": (I32, [P, ctypes.POINTER(I64), ctypes.POINTER(I64)]),
+        "sc_table_stack_status": (I32, [P, ctypes.POINTER(I32), I32]),
         "sc_fetch_layer_kv": (I32, [P, P, I32, ctypes.POINTER(sc_active), VP]),
         "sc_append_new_kv": (I32, [P, P, VP, VP, ctypes.POINTER(sc_active), VP]),
         "sc_prefill_attn": (I32, [VP, VP, VP, I32, I32, I32, I32, I32, F32, VP, VP, VP]),
@@ -187,6 +189,14 @@ def sc_table_totals(table):
     tq, tk = ctypes.c_int64(), ctypes.c_int64()
     _check(load().sc_table_totals(table, ctypes.byref(tq), ctypes.byref(tk)))
     return tq.value, tk.value
+
+
+def sc_table_stack_status(table, clear=False):
+    """True when an overlapped stack's attention gave up waiting for a slot
+    (call after synchronising the stack's streams)."""
+    t = ctypes.c_int32()
+    _check(load().sc_table_stack_status(table, ctypes.byref(t), 1 if clear else 0))
+    return bool(t.value)
 
 
 def active(k_ptr, v_ptr, capacity_tokens):

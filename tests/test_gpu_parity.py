@@ -243,6 +243,52 @@ def test_layer_stack_matches_oracle(name, mode):
         dp.close()
 
 
+def test_forced_slot_wait_timeout_is_reported_and_recoverable():
+    """The failure path of the overlapped stack's device-side slot wait,
+    forced from the host: with SC_STACK_TEST_NEVER_READY every attention
+    kernel waits for a slot count the copy stream never reaches, gives up
+    after a few hundred polls and writes NaN rows; every kernel exits, the
+    table reports the time-out, and after clearing the flag a normal stack
+    on the same table is correct again."""
+    sc = require_gpu()
+    import torch
+    wl = W.small_workload(205, [300, 41], [70, 9], 3, 32, 8, 128)
+    pool_u16 = W.pool_numpy(wl)
+    dp = DevicePool(sc, wl, pool_u16)
+    try:
+        ins = [W.layer_inputs_numpy(wl, l) for l in range(wl.n_layers)]
+        dev = [[from_u16(x, "cuda", wl.dtype) for x in t] for t in ins]
+        outs = [torch.zeros((wl.total_q, wl.n_q_heads, wl.head_dim), dtype=W.torch_dtype(wl), device="cuda")
+                for _ in range(wl.n_layers)]
+        slots = [new_active(sc, wl) for _ in range(2)]
+        copy = torch.cuda.Stream()
+        cs = torch.cuda.current_stream().cuda_stream
+
+        def run(flags):
+            sc.sc_prefill_stack(dp.handle, dp.table, [d[0].data_ptr() for d in dev],
+                                [d[1].data_ptr() for d in dev], [d[2].data_ptr() for d in dev],
+                                [o.data_ptr() for o in outs], [s[2] for s in slots], wl.n_q_heads,
+                                flags, 0.0, cs, copy.cuda_stream)
+            torch.cuda.synchronize()
+
+        assert not sc.sc_table_stack_status(dp.table)
+        run(sc.SC_STACK_OVERLAP | sc.SC_STACK_NO_STORE | sc.SC_STACK_TEST_NEVER_READY)
+        for l, o in enumerate(outs):
+            assert bool(torch.isnan(o.float()).all()), f"layer {l}: rows written despite the time-out"
+        assert sc.sc_table_stack_status(dp.table, clear=True)
+        assert not sc.sc_table_stack_status(dp.table)
+        run(sc.SC_STACK_OVERLAP | sc.SC_STACK_NO_STORE)
+        assert not sc.sc_table_stack_status(dp.table)
+        for l in range(wl.n_layers):
+            q, kn, vn = ins[l]
+            *_, o_ref, _ = _oracle_layer(wl, pool_u16, l, q, kn, vn)
+            compare_attention(to_u16(outs[l]), o_ref, f"after recovery, layer {l}", wl.dtype)
+        with pytest.raises(sc.SwiftCacheError):
+            run(sc.SC_STACK_SERIAL | sc.SC_STACK_TEST_NEVER_READY)
+    finally:
+        dp.close()
+
+
 @pytest.mark.parametrize("name,chunk,mode", [
     ("g4_d128_ragged", 16, "overlap"), ("g4_d128_ragged", 100, "serial"), ("g4_d128_ragged", 1000, "overlap"),
     ("varlen_batch", 48, "overlap"), ("varlen_empty_turn", 7, "overlap"), ("rc_varlen", 64, "overlap"),

@@ -151,6 +151,12 @@ def test_chunked_stack_rejects_bad_chunk(sc):
     assert "chunk_tokens" in str(e.value)
 
 
+def test_stack_status_validation(sc):
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_table_stack_status(None)
+    assert e.value.status == sc.SC_ERR_INVALID
+
+
 def test_attention_argument_validation(sc):
     with pytest.raises(sc.SwiftCacheError) as e:
         sc.sc_prefill_attn(1, 1, 1, 4, 4, 12, 8, 128, 1)
