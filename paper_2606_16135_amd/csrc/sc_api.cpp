@@ -309,12 +309,14 @@ void free_plan(AttnPlan *plan) {
   plan->d_seqs = nullptr;
 }
 
-// Plans for single-sequence calls, keyed by (device, P, N, Hq, Hkv).
+// Plans for single-sequence calls, keyed by (device, P, N, Hq, Hkv).  The
+// caller holds g_plan_mu from the lookup until its kernels are enqueued, so
+// an eviction (which drains the device first) never frees a plan that
+// another thread is about to launch with.
 std::mutex g_plan_mu;
 std::map<std::tuple<int, int, int, int, int>, std::unique_ptr<AttnPlan>> g_single_plans;
 
 sc_status single_plan(int device, int P, int N, int hq, int hkv, AttnPlan **out) {
-  std::lock_guard<std::mutex> lk(g_plan_mu);
   auto key = std::make_tuple(device, P, N, hq, hkv);
   auto it = g_single_plans.find(key);
   if (it != g_single_plans.end()) {
@@ -657,6 +659,7 @@ sc_status prefill_attn_single(const void *q, const void *k_active, const void *v
   int device = 0;
   SC_HIP(hipGetDevice(&device));
   AttnPlan *plan = nullptr;
+  std::lock_guard<std::mutex> lk(g_plan_mu);
   st = single_plan(device, prefix_len, new_len, n_q_heads, n_kv_heads, &plan);
   if (st != SC_OK) return st;
   return run_attention(device, *plan, q, k_active, v_active, out, lse, n_q_heads, n_kv_heads, head_dim, dtype,
