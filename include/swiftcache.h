@@ -276,6 +276,12 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
  * only, over whatever the slots hold: the reference point for the overlap
  * overhead), optionally | SC_STACK_NO_STORE.  `copy` may be NULL unless
  * SC_STACK_OVERLAP is set.
+ * SC_STACK_DEBUG_POISON (overlapped or serial): before each layer's fetch
+ * the slot it fills is overwritten with quiet-NaN patterns (bf16 0x7FC0,
+ * fp16 0x7E00), on the stream that then fetches into it, so an attention
+ * that read a slot before its fetch and append had landed (a lost ordering)
+ * would produce NaN rows instead of another layer's plausible values.
+ * Costs one slot-sized fill per layer; for tests.
  * SC_STACK_TEST_NEVER_READY (with SC_STACK_OVERLAP only, for tests of the
  * failure path): every attention kernel waits for a slot count the copy
  * stream never reaches and gives up after a few hundred polls, so its rows
@@ -289,7 +295,8 @@ enum {
   SC_STACK_ATTN_ONLY = 2,
   SC_STACK_MODE_MASK = 3,
   SC_STACK_NO_STORE = 4,
-  SC_STACK_TEST_NEVER_READY = 8
+  SC_STACK_TEST_NEVER_READY = 8,
+  SC_STACK_DEBUG_POISON = 16
 };
 sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers,
                            const void *const *q_per_layer, const void *const *knew_per_layer,

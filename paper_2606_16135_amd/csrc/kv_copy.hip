@@ -86,7 +86,25 @@ __global__ __launch_bounds__(kThreads) void kv_fetch_kernel(CopyArgs a) { copy_a
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(CopyArgs a) { copy_all<COPY_APPEND>(a); }
 __global__ __launch_bounds__(kThreads) void kv_store_kernel(CopyArgs a) { copy_all<COPY_STORE>(a); }
 
+// Fills n16 16-byte chunks with a repeated 16-bit pattern (the debug
+// poisoning of an active slot before it is refilled).
+__global__ __launch_bounds__(kThreads) void kv_fill_kernel(u32x4 *p, int64_t n16, uint32_t pattern2) {
+  const u32x4 v = {pattern2, pattern2, pattern2, pattern2};
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n16; i += (int64_t)gridDim.x * kThreads)
+    p[i] = v;
+}
+
 }  // namespace
+
+hipError_t launch_kv_fill(void *p, size_t bytes, uint16_t pattern, hipStream_t stream) {
+  const int64_t n16 = (int64_t)(bytes / 16);
+  if (n16 <= 0) return hipSuccess;
+  const int64_t want = (n16 + kThreads - 1) / kThreads;
+  const unsigned blocks = (unsigned)(want < 4096 ? want : 4096);
+  hipLaunchKernelGGL(kv_fill_kernel, dim3(blocks), dim3(kThreads), 0, stream, static_cast<u32x4 *>(p), n16,
+                     (uint32_t)pattern * 0x10001u);
+  return hipGetLastError();
+}
 
 int kv_copy_vgprs() {
   int m = 0;

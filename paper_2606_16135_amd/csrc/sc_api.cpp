@@ -1140,11 +1140,15 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
   if (n_layers <= 0 || n_layers > pool->desc.n_layers)
     return fail(SC_ERR_RANGE, "n_layers %d outside [1, %d]", n_layers, pool->desc.n_layers);
-  if (flags & ~(uint32_t)(SC_STACK_MODE_MASK | SC_STACK_NO_STORE | SC_STACK_TEST_NEVER_READY))
+  if (flags & ~(uint32_t)(SC_STACK_MODE_MASK | SC_STACK_NO_STORE | SC_STACK_TEST_NEVER_READY |
+                          SC_STACK_DEBUG_POISON))
     return fail(SC_ERR_INVALID, "unknown flags");
   const uint32_t mode = flags & SC_STACK_MODE_MASK;
   if (mode > SC_STACK_ATTN_ONLY) return fail(SC_ERR_INVALID, "unknown stack mode");
   const bool never_ready = (flags & SC_STACK_TEST_NEVER_READY) != 0;
+  const bool poison = (flags & SC_STACK_DEBUG_POISON) != 0;
+  if (poison && mode == SC_STACK_ATTN_ONLY)
+    return fail(SC_ERR_INVALID, "SC_STACK_DEBUG_POISON needs a stack that fetches");
   if (never_ready && mode != SC_STACK_OVERLAP)
     return fail(SC_ERR_INVALID, "SC_STACK_TEST_NEVER_READY needs SC_STACK_OVERLAP");
   const bool do_st = !(flags & SC_STACK_NO_STORE);
@@ -1211,8 +1215,17 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
     }
     return SC_OK;
   }
+  // Debug poisoning: NaN patterns over a slot's K and V before it is refilled.
+  auto poison_slot = [&](const sc_active &slot, hipStream_t s) -> sc_status {
+    const size_t bytes = (size_t)table->total_kv * pool->row_bytes;
+    const uint16_t nan16 = d.dtype == SC_DTYPE_F16 ? 0x7E00 : 0x7FC0;
+    hipError_t e = launch_kv_fill(slot.k, bytes, nan16, s);
+    if (e == hipSuccess) e = launch_kv_fill(slot.v, bytes, nan16, s);
+    return e == hipSuccess ? SC_OK : fail_hip(e, "slot poison launch");
+  };
   if (mode == SC_STACK_SERIAL) {
     for (int l = 0; l < n_layers; ++l) {
+      if (poison && (st = poison_slot(slots[0], cs)) != SC_OK) return st;
       if ((st = do_fetch(pool, table, l, &slots[0], cs)) != SC_OK) return st;
       if ((st = do_append(pool, table, knew_per_layer[l], vnew_per_layer[l], &slots[0], cs)) != SC_OK) return st;
       if ((st = attn(l, slots[0])) != SC_OK) return st;
@@ -1274,6 +1287,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
       const int s = l & 1;
       if (l >= 2) SC_HIP(hipStreamWaitEvent(xs, free_[s], 0));
       sc_status r;
+      if (poison && (r = poison_slot(slots[s], xs)) != SC_OK) return r;
       if ((r = do_fetch(pool, table, l, &slots[s], xs, reserve, groups)) != SC_OK) return r;
       if ((r = do_append(pool, table, knew_per_layer[l], vnew_per_layer[l], &slots[s], xs, reserve, groups)) !=
           SC_OK)

@@ -66,6 +66,8 @@ struct CopyArgs {
 // (limits how many copy workgroups share a CU with attention; 0 = none).
 // max_groups > 0 caps the grid; the workgroups then loop over the items.
 hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_reserve = 0, int max_groups = 0);
+// bytes (a multiple of 16, 16-byte aligned p) filled with a 16-bit pattern.
+hipError_t launch_kv_fill(void *p, size_t bytes, uint16_t pattern, hipStream_t stream);
 
 // ---------------------------------------------------------------------------
 // Attention work decomposition

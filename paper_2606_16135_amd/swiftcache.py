@@ -35,6 +35,7 @@ SC_STACK_SERIAL = 1
 SC_STACK_ATTN_ONLY = 2
 SC_STACK_NO_STORE = 4
 SC_STACK_TEST_NEVER_READY = 8
+SC_STACK_DEBUG_POISON = 16
 
 EXPORTED = [
     "sc_pool_create", "sc_pool_destroy", "sc_pool_layout_get", "sc_table_create",

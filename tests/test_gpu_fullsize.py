@@ -2,7 +2,10 @@
 sequence's full prefix blocks in the regular cache, and the 8B shape also
 with fp16 values), in the launch configuration the benchmark times: the whole layer stack runs once through sc_prefill_stack
 (overlapped mode, two active slots, every layer fetched, appended, attended
-and stored), on the same seeded device-generated pool and inputs.
+and stored), on the same seeded device-generated pool and inputs.  Two more
+runs (8B and varlen shapes) add SC_STACK_DEBUG_POISON: every slot is
+overwritten with NaN patterns before it is refilled, so an attention that
+ran ahead of its slot's fetch and append would leave NaN rows.
 
 Checked on layers {0, L/2, L-1} against the oracle, which works from a host
 snapshot of those layers taken before the stack ran:
@@ -65,10 +68,13 @@ def _sub_pool(dp, layer, ids):
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("cfg,rc,dtype", [(2, 0.0, "bf16"), (3, 0.0, "bf16"), (4, 0.0, "bf16"), (5, 0.0, "bf16"),
-                                          (2, 0.5, "bf16"), (3, 0.5, "bf16"), (2, 0.0, "f16")],
-                         ids=["2", "3", "4", "5", "2-rc0.5", "3-rc0.5", "2-f16"])
-def test_benchmark_shape_stack_matches_oracle(cfg, rc, dtype):
+@pytest.mark.parametrize("cfg,rc,dtype,poison", [(2, 0.0, "bf16", False), (3, 0.0, "bf16", False),
+                                                 (4, 0.0, "bf16", False), (5, 0.0, "bf16", False),
+                                                 (2, 0.5, "bf16", False), (3, 0.5, "bf16", False),
+                                                 (2, 0.0, "f16", False), (2, 0.0, "bf16", True),
+                                                 (3, 0.0, "bf16", True)],
+                         ids=["2", "3", "4", "5", "2-rc0.5", "3-rc0.5", "2-f16", "2-poison", "3-poison"])
+def test_benchmark_shape_stack_matches_oracle(cfg, rc, dtype, poison):
     sc = require_gpu()
     import torch
     from paper_2606_16135_amd.torch_pool import DevicePool
@@ -97,7 +103,8 @@ def test_benchmark_shape_stack_matches_oracle(cfg, rc, dtype):
         copy = torch.cuda.Stream()
         sc.sc_prefill_stack(dp.handle, dp.table, [i[0].data_ptr() for i in inputs],
                             [i[1].data_ptr() for i in inputs], [i[2].data_ptr() for i in inputs],
-                            [o.data_ptr() for o in outs], slots, wl.n_q_heads, sc.SC_STACK_OVERLAP, 0.0,
+                            [o.data_ptr() for o in outs], slots, wl.n_q_heads,
+                            sc.SC_STACK_OVERLAP | (sc.SC_STACK_DEBUG_POISON if poison else 0), 0.0,
                             compute.cuda_stream, copy.cuda_stream)
         torch.cuda.synchronize()
         print(f"[fullsize] cfg {cfg}: stack done", flush=True)

@@ -203,9 +203,13 @@ def test_single_visible_key_returns_its_value_row_exactly(dtype):
             assert np.array_equal(o[0, h], v[0, h // g]), (hq, hkv, d, h)
 
 
-@pytest.mark.parametrize("mode", ["overlap", "serial"])
+@pytest.mark.parametrize("mode", ["overlap", "serial", "overlap-poison"])
 @pytest.mark.parametrize("name", ["stack_g4", "stack_varlen_host", "stack_rc", "stack_f16_rc"])
 def test_layer_stack_matches_oracle(name, mode):
+    """The whole layer stack against the oracle, layer by layer, and the pool
+    after every store.  "overlap-poison" overwrites each slot with NaN
+    patterns before it is refilled, so an attention that ran ahead of its
+    slot's fetch and append would leave NaN rows."""
     sc = require_gpu()
     import torch
     if name == "stack_g4":
@@ -226,7 +230,8 @@ def test_layer_stack_matches_oracle(name, mode):
                            device="cuda") for _ in range(wl.n_layers)]
         slots = [new_active(sc, wl) for _ in range(2)]
         copy = torch.cuda.Stream()
-        flags = sc.SC_STACK_OVERLAP if mode == "overlap" else sc.SC_STACK_SERIAL
+        flags = {"overlap": sc.SC_STACK_OVERLAP, "serial": sc.SC_STACK_SERIAL,
+                 "overlap-poison": sc.SC_STACK_OVERLAP | sc.SC_STACK_DEBUG_POISON}[mode]
         sc.sc_prefill_stack(dp.handle, dp.table, [d[0].data_ptr() for d in dev],
                             [d[1].data_ptr() for d in dev], [d[2].data_ptr() for d in dev],
                             [o.data_ptr() for o in outs], [s[2] for s in slots], wl.n_q_heads, flags,
@@ -310,7 +315,8 @@ def test_chunked_stack_matches_oracle(name, chunk, mode):
                            device="cuda") for _ in range(wl.n_layers)]
         slots = [new_active(sc, wl) for _ in range(2)]
         copy = torch.cuda.Stream()
-        flags = sc.SC_STACK_OVERLAP if mode == "overlap" else sc.SC_STACK_SERIAL
+        flags = {"overlap": sc.SC_STACK_OVERLAP, "serial": sc.SC_STACK_SERIAL,
+                 "overlap-poison": sc.SC_STACK_OVERLAP | sc.SC_STACK_DEBUG_POISON}[mode]
         print(f"\n[chunked] {name} chunk {chunk} {mode}", flush=True)
         sc.sc_prefill_stack_chunked(dp.handle, dp.table, [d[0].data_ptr() for d in dev],
                                     [d[1].data_ptr() for d in dev], [d[2].data_ptr() for d in dev],
