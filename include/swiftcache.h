@@ -337,7 +337,8 @@ sc_status sc_prefill_stack_chunked(sc_pool *pool, const sc_table *table, int32_t
  * sequence's leading keys held in the regular cache, as a table with that
  * many leading regular-cache blocks would: no workgroup straddles that
  * boundary and paged = 1 marks those that read it.  `slots` is the number
- * of workgroups the device runs at once (<= 0: 512, i.e. 256 CUs x 2).
+ * of workgroups the device runs at once (<= 0: 256, one per CU of an MI355X,
+ * as the library plans its own calls).
  * Errors: SC_ERR_INVALID (null, negative length, rc_keys outside [0, P],
  * heads as in sc_prefill_attn), SC_ERR_RANGE (items non-NULL and capacity
  * too small).

@@ -61,8 +61,17 @@ constexpr int kXcds = 8;                 // MI355X: workgroup w is dispatched to
 constexpr int kMinSplitKeys = 512;
 constexpr int kMaxSplits = kAttnMaxSplits;
 constexpr int kResidentPerCu = 1;        // one 8-wave workgroup per CU (LDS ring, 2 waves per SIMD)
+constexpr int kQueryDefaultSlots = 256 * kResidentPerCu;   // MI355X: 256 CUs
 constexpr int64_t kItemOverheadKeys = 128;  // prologue + epilogue, in keys
-constexpr int64_t kMergeOverheadKeys = 64;  // partial write + merge-kernel share, in keys
+constexpr int64_t kMergeOverheadKeys = 64;  // partial write of a split item, in keys
+// The merge kernel runs after the forward kernel, so its time adds to the
+// schedule: a launch plus a term proportional to the partial rows it reads
+// and the output rows it writes.  Calibrated on MI355X, where a key of one
+// workgroup's range costs ~33 ns: the 8B shape's merge (16384 rows, 4
+// splits) takes ~5.8 us, the 16-conversation batch's (~520k row-splits)
+// ~33 us.
+constexpr int64_t kMergeLaunchKeys = 45;
+constexpr int64_t kMergeRowSplitsPerKey = 600;  // (rows x (splits + 1)) per key of merge time
 
 struct TileDesc {
   int32_t seq, kvh, q0, nq, keys;
@@ -184,7 +193,13 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
         costs.push_back((r.k_end - r.k_begin) + kItemOverheadKeys + (S > 1 ? kMergeOverheadKeys : 0));
     }
     const size_t n = costs.size();
-    const int64_t span = lpt_makespan(costs, slots);
+    int64_t row_splits = 0;
+    for (int b = 0; b < batch; ++b) {
+      const int S = splits_for(chunk, b);
+      if (S > 1) row_splits += (int64_t)N[b] * n_q_heads * (S + 1);
+    }
+    const int64_t merge = row_splits > 0 ? kMergeLaunchKeys + row_splits / kMergeRowSplitsPerKey : 0;
+    const int64_t span = lpt_makespan(costs, slots) + merge;
     if (best_span < 0 || span < best_span || (span == best_span && n < best_items)) {
       best_span = span;
       best_chunk = chunk;
@@ -1012,7 +1027,7 @@ sc_status sc_attn_plan_query(int32_t batch, const int32_t *prefix_len, const int
   AttnPlan plan;
   plan_attention(std::vector<int32_t>(prefix_len, prefix_len + batch),
                  std::vector<int32_t>(new_len, new_len + batch), n_q_heads, n_kv_heads,
-                 slots > 0 ? slots : 512, &plan, rc, std::vector<int32_t>(rc.size(), 0));
+                 slots > 0 ? slots : kQueryDefaultSlots, &plan, rc, std::vector<int32_t>(rc.size(), 0));
   *n_items = plan.n_items;
   if (items) {
     if (capacity < plan.n_items) return fail(SC_ERR_RANGE, "capacity %d < %d items", capacity, plan.n_items);
