@@ -273,3 +273,22 @@ def test_plan_random_batches(sc):
         hkv = int(rng.choice([1, 2, 8]))
         group = int(rng.choice([1, 4, 5]))
         _check_plan(sc, P, N, hkv * group, hkv, int(rng.integers(16, 2000)))
+
+
+def test_planner_counts_the_merge_when_splitting(sc):
+    """The split count minimises the forward schedule plus the merge kernel
+    that follows it: one 8B-shape conversation (64 query tiles) is split 4
+    ways to fill 256 workgroup slots, while a 16-conversation batch whose
+    ~1100 unsplit items already balance over the slots is not split (its
+    merge would cost more than splitting saves); the 14B shape takes 3."""
+    from paper_2606_16135_amd import workloads as W
+    _, splits = sc.sc_attn_plan_query([8192], [512], 32, 8, 256)
+    assert splits == [4]
+    _, splits = sc.sc_attn_plan_query([32768], [1024], 40, 8, 256)
+    assert splits == [3]
+    wl = W.config(3)
+    items, splits = sc.sc_attn_plan_query([int(x) for x in wl.prefix_len], [int(x) for x in wl.new_len],
+                                          32, 8, 256)
+    assert splits == [1] * 16 and len(items) >= 1024
+    # the default slot count is one workgroup per CU of an MI355X
+    assert sc.sc_attn_plan_query([8192], [512], 32, 8, 0)[1] == [4]
