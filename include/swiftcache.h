@@ -19,6 +19,9 @@
  *  - Device pointers are HIP device addresses on the pool's device.  Host
  *    arrays (block tables, lengths) are read synchronously during the call
  *    and may be freed when it returns.
+ *  - Alignment: every pointer to K/V, q, k_new, v_new, output or pool-tier
+ *    data must be 16-byte aligned (the kernels move 16-byte chunks), lse
+ *    4-byte aligned; a misaligned pointer returns SC_ERR_INVALID.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
  *    device work is enqueued asynchronously on it; no call synchronises the
  *    caller's stream.  Caller-owned buffers must stay alive until that work

@@ -623,9 +623,14 @@ CopyArgs copy_args(const sc_pool *p, const sc_table *t, int mode) {
   return a;
 }
 
+// Element data is moved in 16-byte chunks; every row of it is a multiple
+// of 16 bytes long, so a 16-byte aligned base keeps every row aligned.
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
 sc_status check_active(const sc_table *t, const sc_active *dst) {
   if (dst == nullptr || dst->k == nullptr || dst->v == nullptr)
     return fail(SC_ERR_INVALID, "null active buffer");
+  if (!aligned16(dst->k) || !aligned16(dst->v)) return fail(SC_ERR_INVALID, "active buffer not 16-byte aligned");
   if (dst->capacity_tokens < t->total_kv)
     return fail(SC_ERR_RANGE, "active buffer holds %lld tokens, the table needs %lld",
                 (long long)dst->capacity_tokens, (long long)t->total_kv);
@@ -671,6 +676,9 @@ sc_status prefill_attn_single(const void *q, const void *k_active, const void *v
   if (st != SC_OK) return st;
   if (new_len == 0) return SC_OK;
   if (!q || !k_active || !v_active || !out) return fail(SC_ERR_INVALID, "null argument");
+  if (!aligned16(q) || !aligned16(k_active) || !aligned16(v_active) || !aligned16(out))
+    return fail(SC_ERR_INVALID, "q, k_active, v_active and out must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(lse) & 3) != 0) return fail(SC_ERR_INVALID, "lse must be 4-byte aligned");
   int device = 0;
   SC_HIP(hipGetDevice(&device));
   AttnPlan *plan = nullptr;
@@ -719,6 +727,8 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
   if (d.n_rc_blocks > 0 && (d.block_size < 16 || (d.block_size & (d.block_size - 1)) != 0))
     return fail(SC_ERR_UNSUPPORTED, "a regular cache needs a power-of-two block size >= 16 (got %d)",
                 d.block_size);
+  if (!aligned16(d.device_base) || !aligned16(d.host_base) || !aligned16(d.rc_base))
+    return fail(SC_ERR_INVALID, "caller-owned pool tiers must be 16-byte aligned");
   // Pools over caller-owned HBM without a host tier make no HIP call here.
   const bool needs_hip = (d.n_device_blocks > 0 && !d.device_base) || d.n_host_blocks > 0 ||
                          (d.n_rc_blocks > 0 && !d.rc_base);
@@ -1081,6 +1091,7 @@ sc_status sc_append_new_kv(sc_pool *pool, const sc_table *table, const void *k_n
   if (!pool || !table) return fail(SC_ERR_INVALID, "null argument");
   if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
   if (table->total_q > 0 && (!k_new || !v_new)) return fail(SC_ERR_INVALID, "null k_new/v_new");
+  if (!aligned16(k_new) || !aligned16(v_new)) return fail(SC_ERR_INVALID, "k_new/v_new not 16-byte aligned");
   sc_status st = check_active(table, dst);
   if (st != SC_OK) return st;
   DeviceGuard guard(pool->desc.device);
@@ -1095,6 +1106,7 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
   if (layer < 0 || layer >= pool->desc.n_layers)
     return fail(SC_ERR_RANGE, "layer %d outside [0, %d)", layer, pool->desc.n_layers);
   if (table->total_q > 0 && (!k_new || !v_new)) return fail(SC_ERR_INVALID, "null k_new/v_new");
+  if (!aligned16(k_new) || !aligned16(v_new)) return fail(SC_ERR_INVALID, "k_new/v_new not 16-byte aligned");
   DeviceGuard guard(pool->desc.device);
   return do_store(pool, table, layer, k_new, v_new, (hipStream_t)stream);
 }
@@ -1128,6 +1140,8 @@ sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, int32_t l
   if (st != SC_OK) return st;
   if (table->total_q == 0) return SC_OK;
   if (!q || !out) return fail(SC_ERR_INVALID, "null argument");
+  if (!aligned16(q) || !aligned16(out)) return fail(SC_ERR_INVALID, "q and out must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(lse) & 3) != 0) return fail(SC_ERR_INVALID, "lse must be 4-byte aligned");
   DeviceGuard guard(pool->desc.device);
   AttnPlan *plan = nullptr;
   st = table_plan(const_cast<sc_table *>(table), n_q_heads, &plan);
@@ -1177,6 +1191,9 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   for (int l = 0; l < n_layers; ++l) {
     if (!q_per_layer[l] || !out_per_layer[l] || (table->total_q > 0 && (!knew_per_layer[l] || !vnew_per_layer[l])))
       return fail(SC_ERR_INVALID, "null per-layer pointer at layer %d", l);
+    if (!aligned16(q_per_layer[l]) || !aligned16(out_per_layer[l]) || !aligned16(knew_per_layer[l]) ||
+        !aligned16(vnew_per_layer[l]))
+      return fail(SC_ERR_INVALID, "per-layer pointer at layer %d not 16-byte aligned", l);
   }
   DeviceGuard guard(pool->desc.device);
   const sc_pool_desc &d = pool->desc;

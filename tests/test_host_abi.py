@@ -157,6 +157,22 @@ def test_stack_status_validation(sc):
     assert e.value.status == sc.SC_ERR_INVALID
 
 
+def test_misaligned_pointers_are_rejected(sc):
+    """The kernels move 16-byte chunks: element pointers must be 16-byte
+    aligned, lse 4-byte aligned; checked before any device work."""
+    A = FAKE_BASE
+    for q, k, v, out in [(A + 2, A, A, A), (A, A + 8, A, A), (A, A, A + 4, A), (A, A, A, A + 2)]:
+        with pytest.raises(sc.SwiftCacheError) as e:
+            sc.sc_prefill_attn(q, k, v, 4, 4, 8, 8, 128, out)
+        assert e.value.status == sc.SC_ERR_INVALID and "16-byte aligned" in str(e.value)
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn(A, A, A, 4, 4, 8, 8, 128, A, lse=A + 2)
+    assert e.value.status == sc.SC_ERR_INVALID and "4-byte aligned" in str(e.value)
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_pool_create(2, 2, 64, 16, 8, 0, 0, FAKE_BASE + 8, 0)
+    assert e.value.status == sc.SC_ERR_INVALID and "16-byte aligned" in str(e.value)
+
+
 def test_attention_argument_validation(sc):
     with pytest.raises(sc.SwiftCacheError) as e:
         sc.sc_prefill_attn(1, 1, 1, 4, 4, 12, 8, 128, 1)
