@@ -271,7 +271,10 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
  * attention) whenever a copy workgroup can always run beside an attention
  * workgroup; otherwise it is a stream event wait.  The device wait is bounded
  * (about a second per workgroup); a workgroup that gives up writes NaN rows,
- * so a lost dependency is visible in the output, never silent.
+ * so a lost dependency is visible in the output, never silent.  Overlapped
+ * stacks on one table share its slot counter, so the library runs them one
+ * after another on the device even when they are enqueued from different
+ * threads or caller streams (each starts after the previous one ended).
  * Arrays of per-layer device pointers (host arrays of length n_layers):
  *   q_per_layer, knew_per_layer, vnew_per_layer, out_per_layer.
  * flags: SC_STACK_OVERLAP (two streams, two slots), SC_STACK_SERIAL

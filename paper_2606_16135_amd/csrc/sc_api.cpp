@@ -1009,10 +1009,11 @@ void sc_table_destroy(sc_table *table) {
     auto it = table->pool->live_max_dev.find(table->max_dev_id);
     if (it != table->pool->live_max_dev.end()) table->pool->live_max_dev.erase(it);
   }
-  if (table->d_items || table->d_sync || table->d_rc_ids || !table->plans.empty()) {
+  if (table->d_items || table->d_sync || table->d_rc_ids || table->last_overlap || !table->plans.empty()) {
     DeviceGuard guard(table->pool->desc.device);
     if (table->d_items) (void)hipFree(table->d_items);
     if (table->d_sync) (void)hipFree(table->d_sync);
+    if (table->last_overlap) (void)hipEventDestroy(table->last_overlap);
     if (table->d_rc_ids) (void)hipFree(table->d_rc_ids);
     for (auto &kv : table->plans) free_plan(&kv.second);
   }
@@ -1276,6 +1277,23 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   const bool device_wait = ss != nullptr || copy_fits_beside_attention(d.head_dim);
   if (never_ready && !device_wait)
     return fail(SC_ERR_UNSUPPORTED, "this stack waits on stream events; there is no device wait to time out");
+  // One overlapped stack with a device-side wait at a time per table (they
+  // share its slot counter, whose values must rise in the order the stacks
+  // run on the device): hold the table's stack lock from reserving the
+  // counter values until everything is enqueued, and start after the
+  // previous such stack ended.
+  sc_table *tw = const_cast<sc_table *>(table);
+  std::unique_lock<std::mutex> stack_lock(tw->stack_mu, std::defer_lock);
+  if (device_wait) {
+    stack_lock.lock();
+    if (!tw->last_overlap) {
+      hipError_t he = hipEventCreateWithFlags(&tw->last_overlap, hipEventDisableTiming);
+      if (he != hipSuccess) {
+        tw->last_overlap = nullptr;
+        return fail_hip(he, "hipEventCreate");
+      }
+    }
+  }
   uint64_t *sync = nullptr, base = 0;
   if (device_wait) {
     std::lock_guard<std::mutex> lk(const_cast<sc_table *>(table)->mu);
@@ -1310,6 +1328,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   const size_t reserve = ss ? 0 : copy_lds_reserve(d.device, d.head_dim);
   const int groups = ss ? 0 : copy_groups_beside_attention(d.device, table, n_q_heads, d.head_dim);
   auto body = [&]() -> sc_status {
+    if (device_wait && tw->last_overlap_recorded) SC_HIP(hipStreamWaitEvent(caller_cs, tw->last_overlap, 0));
     // Both streams start after everything already queued on the caller's
     // compute stream.
     SC_HIP(hipEventRecord(start, caller_cs));
@@ -1345,6 +1364,10 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
     if (cs != caller_cs) {
       SC_HIP(hipEventRecord(done, cs));
       SC_HIP(hipStreamWaitEvent(caller_cs, done, 0));
+    }
+    if (device_wait) {
+      SC_HIP(hipEventRecord(tw->last_overlap, caller_cs));
+      tw->last_overlap_recorded = true;
     }
     return SC_OK;
   };

@@ -225,4 +225,11 @@ struct sc_table {
   // (written by the copy stream, polled by attention), [1] = time-out flag.
   uint64_t *d_sync = nullptr;
   uint64_t sync_gen = 1;
+  // Overlapped stacks on one table share d_sync, so their device work must
+  // not interleave: stack_mu is held while one is enqueued, and each starts
+  // after the previous one's end event (last_overlap, recorded on its
+  // caller's compute stream).
+  std::mutex stack_mu;
+  hipEvent_t last_overlap = nullptr;
+  bool last_overlap_recorded = false;
 };

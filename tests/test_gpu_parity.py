@@ -248,6 +248,41 @@ def test_layer_stack_matches_oracle(name, mode):
         dp.close()
 
 
+def test_overlapped_stacks_on_one_table_from_two_streams():
+    """Two overlapped stacks on the same table, enqueued back to back on two
+    different caller streams with their own slots and outputs: they share
+    the table's slot counter, so the library runs them one after the other;
+    both must match the oracle."""
+    sc = require_gpu()
+    import torch
+    wl = W.small_workload(206, [700, 45], [90, 30], 4, 32, 8, 128)
+    pool_u16 = W.pool_numpy(wl)
+    dp = DevicePool(sc, wl, pool_u16)
+    try:
+        ins = [W.layer_inputs_numpy(wl, l) for l in range(wl.n_layers)]
+        dev = [[from_u16(x, "cuda", wl.dtype) for x in t] for t in ins]
+        runs = []
+        for _ in range(2):
+            outs = [torch.full((wl.total_q, wl.n_q_heads, wl.head_dim), float("nan"), dtype=W.torch_dtype(wl),
+                               device="cuda") for _ in range(wl.n_layers)]
+            runs.append((outs, [new_active(sc, wl) for _ in range(2)], torch.cuda.Stream(), torch.cuda.Stream()))
+        torch.cuda.synchronize()
+        for outs, slots, cs, xs in runs:
+            sc.sc_prefill_stack(dp.handle, dp.table, [d[0].data_ptr() for d in dev],
+                                [d[1].data_ptr() for d in dev], [d[2].data_ptr() for d in dev],
+                                [o.data_ptr() for o in outs], [s[2] for s in slots], wl.n_q_heads,
+                                sc.SC_STACK_OVERLAP | sc.SC_STACK_NO_STORE, 0.0, cs.cuda_stream, xs.cuda_stream)
+        torch.cuda.synchronize()
+        assert not sc.sc_table_stack_status(dp.table)
+        for r, (outs, *_) in enumerate(runs):
+            for l in range(wl.n_layers):
+                q, kn, vn = ins[l]
+                *_, o_ref, _ = _oracle_layer(wl, pool_u16, l, q, kn, vn)
+                compare_attention(to_u16(outs[l]), o_ref, f"stack {r} layer {l}", wl.dtype)
+    finally:
+        dp.close()
+
+
 def test_forced_slot_wait_timeout_is_reported_and_recoverable():
     """The failure path of the overlapped stack's device-side slot wait,
     forced from the host: with SC_STACK_TEST_NEVER_READY every attention
