@@ -258,8 +258,8 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
 /*
  * The whole layer stack with layer-wise pipelining (§3.3).  Per layer l, slot
  * s = l % 2 of `slots`:
- *   copy stream:    wait until attention(l-2) released slot s; fetch(l) and
- *                   append(l) into slot s; mark slot s ready; store(l).
+ *   copy stream:    wait until attention(l-2) released slot s; fetch(l),
+ *                   append(l) into slot s and store(l); mark slot s ready.
  *   compute stream: wait for slot s; attention(l) into out_per_layer[l];
  *                   release slot s.
  * so the fetch of layer l+1 runs while layer l's attention runs.  Two slots
@@ -268,10 +268,13 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
  * is enqueued and the compute stream is ordered after every store.
  * "Wait for slot s" is done by the attention kernel itself on a device
  * counter the copy stream advances (no stream-level wait in front of every
- * attention) whenever a copy workgroup can always run beside an attention
- * workgroup; otherwise it is a stream event wait.  The device wait is bounded
- * (about a second per workgroup); a workgroup that gives up writes NaN rows,
- * so a lost dependency is visible in the output, never silent.  Overlapped
+ * attention), and "wait until released" by a one-wave kernel on the copy
+ * stream polling a count of finished attention workgroups, whenever a copy
+ * workgroup can always run beside an attention workgroup; otherwise both are
+ * stream event waits.  The device waits are bounded (about a second); an
+ * attention workgroup that gives up writes NaN rows, and a copy whose wait
+ * gave up writes NaN into the slot instead of K/V, so a lost dependency is
+ * visible in the output, never silent.  Overlapped
  * stacks on one table share its slot counter, so the library runs them one
  * after another on the device even when they are enqueued from different
  * threads or caller streams (each starts after the previous one ended).
@@ -294,6 +297,11 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
  * come out NaN and sc_table_stack_status reports the time-out; every kernel
  * still exits.  SC_ERR_UNSUPPORTED if this stack would use the stream-level
  * wait (no device-side wait to time out).
+ * SC_STACK_TEST_NEVER_FREE (likewise): every wait for a slot's release
+ * (layers 2 and up) waits for a count the attention never reaches and gives
+ * up after a few hundred polls; those layers' slots are filled with NaN, so
+ * their rows come out NaN (layers whose slot was refilled while they read it
+ * may too), and sc_table_stack_status reports the time-out.
  */
 enum {
   SC_STACK_OVERLAP = 0,
@@ -302,7 +310,8 @@ enum {
   SC_STACK_MODE_MASK = 3,
   SC_STACK_NO_STORE = 4,
   SC_STACK_TEST_NEVER_READY = 8,
-  SC_STACK_DEBUG_POISON = 16
+  SC_STACK_DEBUG_POISON = 16,
+  SC_STACK_TEST_NEVER_FREE = 32
 };
 sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers,
                            const void *const *q_per_layer, const void *const *knew_per_layer,

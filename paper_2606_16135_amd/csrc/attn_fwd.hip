@@ -538,6 +538,15 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
     pv_tile<D, DT>(slot_v(n - 1), w.pf_prev, w.oacc, lane);
   }
 
+  // Done with K/V: every load of it has been consumed (loads past the range
+  // touch no memory), so the slot may be refilled once every workgroup of
+  // the launch has counted itself here.  Only the order after these reads
+  // matters, no data flows to the refill: a relaxed device-scope add.
+  if (a.done_counter != nullptr) {
+    __syncthreads();
+    if (tid == 0) __hip_atomic_fetch_add(a.done_counter, (uint64_t)1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+
   // Combine the two halves' denominators and normalise.
   const float l_tot = w.l_run + __shfl_xor(w.l_run, 32);
   const float inv = timed_out ? __builtin_nanf("") : l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -583,7 +592,13 @@ template <int D, int DT>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t smem[Geo<D>::kSmem];
   const WorkItem wi = a.items[blockIdx.x];
-  if (wi.seq < 0) return;
+  if (wi.seq < 0) {
+    // Padding slot (XCD placement): no K/V to read, but it counts as done
+    // like every other workgroup of the launch.
+    if (a.done_counter != nullptr && threadIdx.x == 0)
+      __hip_atomic_fetch_add(a.done_counter, (uint64_t)1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
   if (wi.paged)
     attn_item<D, DT, true>(a, wi, smem);
   else

@@ -10,6 +10,10 @@
 // then V half, Eq. 1), and consecutive rows of a sequence are contiguous in
 // the active buffer, so each item is one contiguous range on both sides.
 //
+// The overlapped layer stack launches all three of a layer in one grid
+// (kv_layer_copy_kernel) after a one-wave gate kernel that waits on the
+// device for the attention that last read the slot.
+//
 // HBM-bound: every lane moves 16-byte chunks with kUnroll loads in flight
 // before the matching stores, through buffer resources over the item's two
 // ranges.  Both sides are streamed once per call: the loads are
@@ -34,8 +38,10 @@ constexpr int kStorePolicy = 2;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// poison: write nan2 over the destination instead of copying (fetch and
+// append into a slot whose gate timed out).
 template <int MODE>
-__device__ __forceinline__ void copy_rows(const CopyArgs &a, int g) {
+__device__ __forceinline__ void copy_rows(const CopyArgs &a, int g, bool poison = false, uint32_t nan2 = 0) {
   const int item_idx = g >> 1;
   const int is_v = g & 1;
   const CopyItem it = a.items[item_idx];
@@ -64,7 +70,9 @@ __device__ __forceinline__ void copy_rows(const CopyArgs &a, int g) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t idx = base + u * kThreads + threadIdx.x;
-      if (idx < nchunks)
+      if (poison)
+        r[u] = u32x4{nan2, nan2, nan2, nan2};
+      else if (idx < nchunks)
         r[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(idx * 16), 0, kLoadPolicy));
     }
 #pragma unroll
@@ -85,6 +93,40 @@ __device__ __forceinline__ void copy_all(const CopyArgs &a) {
 __global__ __launch_bounds__(kThreads) void kv_fetch_kernel(CopyArgs a) { copy_all<COPY_FETCH>(a); }
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(CopyArgs a) { copy_all<COPY_APPEND>(a); }
 __global__ __launch_bounds__(kThreads) void kv_store_kernel(CopyArgs a) { copy_all<COPY_STORE>(a); }
+
+// The overlapped stack's per-layer copy: fetch, append and store item
+// halves in that order, strided over a capped grid.
+__global__ __launch_bounds__(kThreads) void kv_layer_copy_kernel(LayerCopyArgs a) {
+  const bool poison =
+      a.fail_word != nullptr && __hip_atomic_load(a.fail_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.fail_tag;
+  const int n0 = 2 * a.part[0].n_items;
+  const int n1 = n0 + 2 * a.part[1].n_items;
+  const int n2 = n1 + 2 * a.part[2].n_items;
+  for (int g = blockIdx.x; g < n2; g += gridDim.x) {
+    if (g < n0)
+      copy_rows<COPY_FETCH>(a.part[0], g, poison, a.nan2);
+    else if (g < n1)
+      copy_rows<COPY_APPEND>(a.part[1], g - n0, poison, a.nan2);
+    else
+      copy_rows<COPY_STORE>(a.part[2], g - n1);
+  }
+}
+
+// Holds its stream until *counter >= value.  The poll is a relaxed
+// device-scope load with a sleep between polls; the counter only rises.
+__global__ __launch_bounds__(64) void slot_gate_kernel(const uint64_t *counter, uint64_t value, uint32_t *timeout,
+                                                       uint64_t *fail_word, uint64_t fail_tag, int spin_limit) {
+  if (threadIdx.x != 0) return;
+  int spins = 0;
+  while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < value) {
+    if (++spins > spin_limit) {
+      __hip_atomic_store(timeout, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(fail_word, fail_tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    __builtin_amdgcn_s_sleep(8);
+  }
+}
 
 // Fills n16 16-byte chunks with a repeated 16-bit pattern (the debug
 // poisoning of an active slot before it is refilled).
@@ -109,7 +151,8 @@ hipError_t launch_kv_fill(void *p, size_t bytes, uint16_t pattern, hipStream_t s
 int kv_copy_vgprs() {
   int m = 0;
   for (const void *f : {reinterpret_cast<const void *>(&kv_fetch_kernel), reinterpret_cast<const void *>(&kv_append_kernel),
-                        reinterpret_cast<const void *>(&kv_store_kernel)}) {
+                        reinterpret_cast<const void *>(&kv_store_kernel),
+                        reinterpret_cast<const void *>(&kv_layer_copy_kernel)}) {
     hipFuncAttributes at{};
     if (hipFuncGetAttributes(&at, f) != hipSuccess) return -1;
     m = at.numRegs > m ? at.numRegs : m;
@@ -127,6 +170,21 @@ hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_rese
     hipLaunchKernelGGL(kv_append_kernel, grid, block, lds_reserve, stream, a);
   else
     hipLaunchKernelGGL(kv_store_kernel, grid, block, lds_reserve, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_layer_copy(const LayerCopyArgs &a, hipStream_t stream, size_t lds_reserve, int max_groups) {
+  const int halves = 2 * (a.part[0].n_items + a.part[1].n_items + a.part[2].n_items);
+  if (halves <= 0) return hipSuccess;
+  const int groups = max_groups > 0 && max_groups < halves ? max_groups : halves;
+  hipLaunchKernelGGL(kv_layer_copy_kernel, dim3(groups), dim3(kThreads), lds_reserve, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_slot_gate(const uint64_t *counter, uint64_t value, uint32_t *timeout, uint64_t *fail_word,
+                            uint64_t fail_tag, int spin_limit, hipStream_t stream) {
+  hipLaunchKernelGGL(slot_gate_kernel, dim3(1), dim3(64), 0, stream, counter, value, timeout, fail_word, fail_tag,
+                     spin_limit);
   return hipGetLastError();
 }
 

@@ -58,7 +58,7 @@ class DeviceGuard {
 // ---------------------------------------------------------------------------
 namespace {
 constexpr int kXcds = 8;                 // MI355X: workgroup w is dispatched to XCD w % 8
-constexpr int kMinSplitKeys = 512;
+constexpr int kMinSplitKeys = 2 * kAttnKeyTile;   // the schedule model below picks among the rest
 constexpr int kMaxSplits = kAttnMaxSplits;
 constexpr int kResidentPerCu = 1;        // one 8-wave workgroup per CU (LDS ring, 2 waves per SIMD)
 constexpr int kQueryDefaultSlots = 256 * kResidentPerCu;   // MI355X: 256 CUs
@@ -72,6 +72,15 @@ constexpr int64_t kMergeOverheadKeys = 64;  // partial write of a split item, in
 // ~33 us.
 constexpr int64_t kMergeLaunchKeys = 45;
 constexpr int64_t kMergeRowSplitsPerKey = 600;  // (rows x (splits + 1)) per key of merge time
+// Every item also reads its Q tile and writes its output or partial tile
+// (256 rows each way, 128 KiB at head_dim 128), and that traffic shares HBM
+// with every other item in flight: about 30 ns, one key, per item.  With
+// this term and two-tile splits allowed, the split count chosen for 21
+// single-sequence shapes (P 256..32768, N 16..1024, 32 or 40 query heads)
+// came within 2% of the fastest of 1..16 splits measured on MI355X for each;
+// short turns (P <= 4096, N <= 256) run 10-35% faster than with a 512-key
+// floor and no such term.
+constexpr int64_t kItemSharedKeys = 1;
 
 struct TileDesc {
   int32_t seq, kvh, q0, nq, keys;
@@ -199,7 +208,7 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
       if (S > 1) row_splits += (int64_t)N[b] * n_q_heads * (S + 1);
     }
     const int64_t merge = row_splits > 0 ? kMergeLaunchKeys + row_splits / kMergeRowSplitsPerKey : 0;
-    const int64_t span = lpt_makespan(costs, slots) + merge;
+    const int64_t span = lpt_makespan(costs, slots) + merge + kItemSharedKeys * (int64_t)n;
     if (best_span < 0 || span < best_span || (span == best_span && n < best_items)) {
       best_span = span;
       best_chunk = chunk;
@@ -371,7 +380,7 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
                         void *out, float *lse, int hq, int hkv, int head_dim, int dtype, float scale,
                         hipStream_t stream, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
                         hipEvent_t after_fwd = nullptr, const RcView &rc = RcView(),
-                        int spin_limit = kAttnReadySpinLimit) {
+                        int spin_limit = kAttnReadySpinLimit, uint64_t *done_counter = nullptr) {
   if (plan.n_items == 0) return SC_OK;
   // The kernel addresses one sequence's rows of one KV head with 32-bit
   // byte offsets.
@@ -423,6 +432,7 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
     a.ready_timeout = reinterpret_cast<uint32_t *>(const_cast<uint64_t *>(ready_flag + 1));
     a.ready_spin_limit = spin_limit;
   }
+  a.done_counter = done_counter;
   hipError_t e = launch_attn_fwd(a, head_dim, plan.n_items, stream);
   if (e != hipSuccess) return fail_hip(e, "attn_fwd launch");
   if (after_fwd) SC_HIP(hipEventRecord(after_fwd, stream));
@@ -666,6 +676,24 @@ sc_status do_store(sc_pool *p, const sc_table *t, int layer, const void *kn, con
   a.new_v = static_cast<const char *>(vn);
   hipError_t e = launch_kv_copy(a, s, lds_reserve, max_groups);
   return e == hipSuccess ? SC_OK : fail_hip(e, "store launch");
+}
+
+// Fetch, append and store of one layer as one launch (overlapped stack).
+LayerCopyArgs layer_copy_args(const sc_pool *p, const sc_table *t, int layer, const void *kn, const void *vn,
+                              const sc_active *dst, bool store) {
+  LayerCopyArgs la{};
+  const int64_t layer_off = (int64_t)layer * (int64_t)p->slice_bytes;
+  for (int m : {COPY_FETCH, COPY_APPEND, COPY_STORE}) {
+    CopyArgs &a = la.part[m == COPY_FETCH ? 0 : m == COPY_APPEND ? 1 : 2];
+    a = copy_args(p, t, m);
+    a.layer_off = m == COPY_APPEND ? 0 : layer_off;
+    a.new_k = static_cast<const char *>(kn);
+    a.new_v = static_cast<const char *>(vn);
+    a.act_k = m == COPY_STORE ? nullptr : static_cast<char *>(dst->k);
+    a.act_v = m == COPY_STORE ? nullptr : static_cast<char *>(dst->v);
+  }
+  if (!store) la.part[2].n_items = 0;
+  return la;
 }
 
 sc_status prefill_attn_single(const void *q, const void *k_active, const void *v_active, int32_t prefix_len,
@@ -1171,7 +1199,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   if (n_layers <= 0 || n_layers > pool->desc.n_layers)
     return fail(SC_ERR_RANGE, "n_layers %d outside [1, %d]", n_layers, pool->desc.n_layers);
   if (flags & ~(uint32_t)(SC_STACK_MODE_MASK | SC_STACK_NO_STORE | SC_STACK_TEST_NEVER_READY |
-                          SC_STACK_DEBUG_POISON))
+                          SC_STACK_DEBUG_POISON | SC_STACK_TEST_NEVER_FREE))
     return fail(SC_ERR_INVALID, "unknown flags");
   const uint32_t mode = flags & SC_STACK_MODE_MASK;
   if (mode > SC_STACK_ATTN_ONLY) return fail(SC_ERR_INVALID, "unknown stack mode");
@@ -1181,6 +1209,9 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
     return fail(SC_ERR_INVALID, "SC_STACK_DEBUG_POISON needs a stack that fetches");
   if (never_ready && mode != SC_STACK_OVERLAP)
     return fail(SC_ERR_INVALID, "SC_STACK_TEST_NEVER_READY needs SC_STACK_OVERLAP");
+  const bool never_free = (flags & SC_STACK_TEST_NEVER_FREE) != 0;
+  if (never_free && mode != SC_STACK_OVERLAP)
+    return fail(SC_ERR_INVALID, "SC_STACK_TEST_NEVER_FREE needs SC_STACK_OVERLAP");
   const bool do_st = !(flags & SC_STACK_NO_STORE);
   const int n_slots = mode == SC_STACK_SERIAL ? 1 : 2;
   for (int s = 0; s < n_slots; ++s) {
@@ -1229,13 +1260,13 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   const uint64_t never = never_ready ? (uint64_t)1 << 40 : 0;
   const int spin_limit = never_ready ? kAttnTestSpinLimit : kAttnReadySpinLimit;
   auto attn = [&](int l, const sc_active &slot, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
-                  hipEvent_t after_fwd = nullptr) {
+                  hipEvent_t after_fwd = nullptr, uint64_t *done_counter = nullptr) {
     RcView rc{pool, l, table->d_rc_ids};
     for (int c = 0; c < n_chunks; ++c) {
       sc_status r = run_attention(d.device, *plans[c], q_per_layer[l], slot.k, slot.v, out_per_layer[l], nullptr,
                                   n_q_heads, d.n_kv_heads, d.head_dim, d.dtype, scale, cs,
                                   c == 0 ? ready_flag : nullptr, ready_value + (ready_flag ? never : 0),
-                                  c == n_chunks - 1 ? after_fwd : nullptr, rc, spin_limit);
+                                  c == n_chunks - 1 ? after_fwd : nullptr, rc, spin_limit, done_counter);
       if (r != SC_OK) return r;
     }
     return SC_OK;
@@ -1269,13 +1300,20 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
 
   // Overlapped.  Attention of layer l waits on the device for the copy
   // stream's count of filled slots (table->d_sync[0], written by the copy
-  // stream after the append); a stream-level wait here would put a
+  // stream after the layer's copy); a stream-level wait here would put a
   // command-processor round trip (about 12 us measured) in front of every
-  // attention.  The copy stream, which has slack, waits on events free_[s]
-  // (attention of the layer that last used slot s has read it).
+  // attention.  In the other direction the copy stream runs a one-wave gate
+  // kernel that waits until every forward workgroup of the attention that
+  // last read slot s has counted itself done (table->d_sync[2]); fetch,
+  // append and store of the layer then run as one launch.  Per layer that
+  // leaves the host two launches on the copy stream, one counter write and
+  // the attention's launches, where separate copy launches and an event
+  // record plus a cross-stream wait cost about twice as much host time,
+  // which bounded short turns.  Without the device wait (a copy workgroup
+  // could be kept off a CU by attention) the streams wait on events.
   // Disjoint CU sets (host tier) never block each other.
   const bool device_wait = ss != nullptr || copy_fits_beside_attention(d.head_dim);
-  if (never_ready && !device_wait)
+  if ((never_ready || never_free) && !device_wait)
     return fail(SC_ERR_UNSUPPORTED, "this stack waits on stream events; there is no device wait to time out");
   // One overlapped stack with a device-side wait at a time per table (they
   // share its slot counter, whose values must rise in the order the stacks
@@ -1299,8 +1337,8 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
     std::lock_guard<std::mutex> lk(const_cast<sc_table *>(table)->mu);
     sc_table *t = const_cast<sc_table *>(table);
     if (!t->d_sync) {
-      SC_HIP(hipMalloc(reinterpret_cast<void **>(&t->d_sync), 2 * sizeof(uint64_t)));
-      const uint64_t zero[2] = {0, 0};
+      SC_HIP(hipMalloc(reinterpret_cast<void **>(&t->d_sync), 4 * sizeof(uint64_t)));
+      const uint64_t zero[4] = {0, 0, 0, 0};
       SC_HIP(hipMemcpy(t->d_sync, zero, sizeof(zero), hipMemcpyHostToDevice));
     }
     sync = t->d_sync;
@@ -1327,8 +1365,17 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   // Host-tier fetches already run on their own CUs (split streams).
   const size_t reserve = ss ? 0 : copy_lds_reserve(d.device, d.head_dim);
   const int groups = ss ? 0 : copy_groups_beside_attention(d.device, table, n_q_heads, d.head_dim);
+  // Forward workgroups per layer (every chunk's launch counts itself).
+  uint64_t fwd_groups = 0;
+  for (const AttnPlan *pl : plans) fwd_groups += (uint64_t)pl->n_items;
+  const uint32_t nan2 = (d.dtype == SC_DTYPE_F16 ? 0x7E00u : 0x7FC0u) * 0x10001u;
+  const uint64_t never_f = never_free ? (uint64_t)1 << 40 : 0;
+  const int gate_spin = never_free ? kAttnTestSpinLimit : kAttnReadySpinLimit;
   auto body = [&]() -> sc_status {
     if (device_wait && tw->last_overlap_recorded) SC_HIP(hipStreamWaitEvent(caller_cs, tw->last_overlap, 0));
+    // The done count starts from zero for this stack; the copy stream
+    // starts after this write (event below).
+    if (device_wait) SC_HIP(hipStreamWriteValue64(caller_cs, sync + 2, 0, 0));
     // Both streams start after everything already queued on the caller's
     // compute stream.
     SC_HIP(hipEventRecord(start, caller_cs));
@@ -1336,27 +1383,38 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
     if (cs != caller_cs) SC_HIP(hipStreamWaitEvent(cs, start, 0));
     for (int l = 0; l < n_layers; ++l) {
       const int s = l & 1;
-      if (l >= 2) SC_HIP(hipStreamWaitEvent(xs, free_[s], 0));
       sc_status r;
+      if (device_wait) {
+        // Slot s was last read by attention(l-2): wait for layers 0..l-2.
+        if (l >= 2) {
+          hipError_t e = launch_slot_gate(sync + 2, (uint64_t)(l - 1) * fwd_groups + never_f,
+                                          reinterpret_cast<uint32_t *>(sync + 1), sync + 3, base + l + 1,
+                                          gate_spin, xs);
+          if (e != hipSuccess) return fail_hip(e, "slot gate launch");
+        }
+        if (poison && (r = poison_slot(slots[s], xs)) != SC_OK) return r;
+        LayerCopyArgs la = layer_copy_args(pool, table, l, knew_per_layer[l], vnew_per_layer[l], &slots[s], do_st);
+        la.fail_word = sync + 3;
+        la.fail_tag = base + l + 1;
+        la.nan2 = nan2;
+        hipError_t e = launch_kv_layer_copy(la, xs, reserve, groups);
+        if (e != hipSuccess) return fail_hip(e, "layer copy launch");
+        SC_HIP(hipStreamWriteValue64(xs, sync, base + l + 1, 0));
+        if ((r = attn(l, slots[s], sync, base + l + 1, nullptr, sync + 2)) != SC_OK) return r;
+        continue;
+      }
+      if (l >= 2) SC_HIP(hipStreamWaitEvent(xs, free_[s], 0));
       if (poison && (r = poison_slot(slots[s], xs)) != SC_OK) return r;
       if ((r = do_fetch(pool, table, l, &slots[s], xs, reserve, groups)) != SC_OK) return r;
       if ((r = do_append(pool, table, knew_per_layer[l], vnew_per_layer[l], &slots[s], xs, reserve, groups)) !=
           SC_OK)
         return r;
-      if (device_wait) {
-        SC_HIP(hipStreamWriteValue64(xs, sync, base + l + 1, 0));
-      } else {
-        SC_HIP(hipEventRecord(ready[s], xs));
-      }
+      SC_HIP(hipEventRecord(ready[s], xs));
       if (do_st &&
           (r = do_store(pool, table, l, knew_per_layer[l], vnew_per_layer[l], xs, reserve, groups)) != SC_OK)
         return r;
-      if (device_wait) {
-        if ((r = attn(l, slots[s], sync, base + l + 1, free_[s])) != SC_OK) return r;
-      } else {
-        SC_HIP(hipStreamWaitEvent(cs, ready[s], 0));
-        if ((r = attn(l, slots[s], nullptr, 0, free_[s])) != SC_OK) return r;
-      }
+      SC_HIP(hipStreamWaitEvent(cs, ready[s], 0));
+      if ((r = attn(l, slots[s], nullptr, 0, free_[s])) != SC_OK) return r;
     }
     // The caller's compute stream ends after the last attention and store.
     SC_HIP(hipEventRecord(start, xs));

@@ -69,6 +69,25 @@ hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_rese
 // bytes (a multiple of 16, 16-byte aligned p) filled with a 16-bit pattern.
 hipError_t launch_kv_fill(void *p, size_t bytes, uint16_t pattern, hipStream_t stream);
 
+// One layer's fetch, append and store in one launch (overlapped layer
+// stack): workgroups take fetch item halves first, then append, then store.
+// If *fail_word == fail_tag when a workgroup starts (the slot gate below
+// timed out for this layer), fetch and append write the NaN pattern nan16
+// into the slot instead of data.
+struct LayerCopyArgs {
+  CopyArgs part[3];                // COPY_FETCH, COPY_APPEND, COPY_STORE
+  const uint64_t *fail_word;       // nullable
+  uint64_t fail_tag;
+  uint32_t nan2;                   // nan16 repeated in both halves
+};
+hipError_t launch_kv_layer_copy(const LayerCopyArgs &a, hipStream_t stream, size_t lds_reserve, int max_groups);
+// One-wave kernel that holds the stream until *counter >= value (the
+// attention workgroups that read a slot are all done with it), polling at
+// most spin_limit times; on time-out it sets *timeout and *fail_word =
+// fail_tag and ends.  One wave cannot keep an attention workgroup off a CU.
+hipError_t launch_slot_gate(const uint64_t *counter, uint64_t value, uint32_t *timeout, uint64_t *fail_word,
+                            uint64_t fail_tag, int spin_limit, hipStream_t stream);
+
 // ---------------------------------------------------------------------------
 // Attention work decomposition
 // ---------------------------------------------------------------------------
@@ -125,6 +144,10 @@ struct AttnArgs {
   uint64_t ready_value;
   uint32_t *ready_timeout;
   int32_t ready_spin_limit;
+  // Optional: every workgroup adds 1 to *done_counter once it has finished
+  // reading K/V (after its last key tile; timed-out and empty workgroups
+  // too), so that the next refill of the slot can wait on the device.
+  uint64_t *done_counter;
   // Regular cache (paged items): block i of sequence s is local block
   // rc_ids[seqs[s].rc_off + i] of the tier at rc_base, whose layer-l K rows
   // start at rc_base + id * rc_block_elems + rc_layer_elems (V rows
@@ -222,7 +245,10 @@ struct sc_table {
   // the whole new turn
   std::map<std::tuple<int, int, int, int>, sc::AttnPlan> plans;
   // Overlapped stack: [0] = count of layers whose active slot is filled
-  // (written by the copy stream, polled by attention), [1] = time-out flag.
+  // (written by the copy stream, polled by attention), [1] = time-out flag,
+  // [2] = forward workgroups of the running stack done with their slot
+  // (reset at its start, polled by the slot gates), [3] = tag of the last
+  // layer whose slot gate timed out.
   uint64_t *d_sync = nullptr;
   uint64_t sync_gen = 1;
   // Overlapped stacks on one table share d_sync, so their device work must

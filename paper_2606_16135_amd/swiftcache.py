@@ -36,6 +36,7 @@ SC_STACK_ATTN_ONLY = 2
 SC_STACK_NO_STORE = 4
 SC_STACK_TEST_NEVER_READY = 8
 SC_STACK_DEBUG_POISON = 16
+SC_STACK_TEST_NEVER_FREE = 32
 
 EXPORTED = [
     "sc_pool_create", "sc_pool_destroy", "sc_pool_layout_get", "sc_table_create",

@@ -283,16 +283,22 @@ def test_overlapped_stacks_on_one_table_from_two_streams():
         dp.close()
 
 
-def test_forced_slot_wait_timeout_is_reported_and_recoverable():
-    """The failure path of the overlapped stack's device-side slot wait,
-    forced from the host: with SC_STACK_TEST_NEVER_READY every attention
-    kernel waits for a slot count the copy stream never reaches, gives up
-    after a few hundred polls and writes NaN rows; every kernel exits, the
-    table reports the time-out, and after clearing the flag a normal stack
-    on the same table is correct again."""
+@pytest.mark.parametrize("which", ["ready", "free"])
+def test_forced_slot_wait_timeout_is_reported_and_recoverable(which):
+    """The failure paths of the overlapped stack's device-side slot waits,
+    forced from the host.  SC_STACK_TEST_NEVER_READY: every attention kernel
+    waits for a slot count the copy stream never reaches, gives up after a
+    few hundred polls and writes NaN rows.  SC_STACK_TEST_NEVER_FREE: every
+    copy into a slot (layers 2 and 3) waits for attention workgroups that
+    never all finish, gives up and fills the slot with NaN, so those layers'
+    rows are NaN.  Either way every kernel exits, the table reports the
+    time-out, and after clearing the flag a normal stack on the same table
+    is correct again."""
     sc = require_gpu()
     import torch
-    wl = W.small_workload(205, [300, 41], [70, 9], 3, 32, 8, 128)
+    flag = sc.SC_STACK_TEST_NEVER_READY if which == "ready" else sc.SC_STACK_TEST_NEVER_FREE
+    first_nan = 0 if which == "ready" else 2
+    wl = W.small_workload(205, [300, 41], [70, 9], 4, 32, 8, 128)
     pool_u16 = W.pool_numpy(wl)
     dp = DevicePool(sc, wl, pool_u16)
     try:
@@ -312,9 +318,9 @@ def test_forced_slot_wait_timeout_is_reported_and_recoverable():
             torch.cuda.synchronize()
 
         assert not sc.sc_table_stack_status(dp.table)
-        run(sc.SC_STACK_OVERLAP | sc.SC_STACK_NO_STORE | sc.SC_STACK_TEST_NEVER_READY)
-        for l, o in enumerate(outs):
-            assert bool(torch.isnan(o.float()).all()), f"layer {l}: rows written despite the time-out"
+        run(sc.SC_STACK_OVERLAP | sc.SC_STACK_NO_STORE | flag)
+        for l in range(first_nan, wl.n_layers):
+            assert bool(torch.isnan(outs[l].float()).all()), f"layer {l}: rows written despite the time-out"
         assert sc.sc_table_stack_status(dp.table, clear=True)
         assert not sc.sc_table_stack_status(dp.table)
         run(sc.SC_STACK_OVERLAP | sc.SC_STACK_NO_STORE)
@@ -324,7 +330,7 @@ def test_forced_slot_wait_timeout_is_reported_and_recoverable():
             *_, o_ref, _ = _oracle_layer(wl, pool_u16, l, q, kn, vn)
             compare_attention(to_u16(outs[l]), o_ref, f"after recovery, layer {l}", wl.dtype)
         with pytest.raises(sc.SwiftCacheError):
-            run(sc.SC_STACK_SERIAL | sc.SC_STACK_TEST_NEVER_READY)
+            run(sc.SC_STACK_SERIAL | flag)
     finally:
         dp.close()
 
