@@ -40,7 +40,7 @@ BF16_PEAK_TFLOPS = 2500.0
 # passes (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors that map the same
 # counters to a plain 256 MiB copy), per workload, for the kernels as they
 # are now; profiles/attention_<workload>.md holds the commands and readings.
-PMC_TRAFFIC = {"llama3-8b-P8192-N512": 80479656}
+PMC_TRAFFIC = {"llama3-8b-P8192-N512": 80546600}
 
 
 def attention_flops(wl):

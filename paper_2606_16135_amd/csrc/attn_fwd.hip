@@ -606,8 +606,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
 }
 
 // Split-key merge: D / 8 lanes per (token, head) row, 8 dims per lane.
-// Weights exp(lse_s - max) over the splits, weighted sum of the partials;
-// the loads of several splits are issued before they are used.
+// Weights exp(lse_s - max) over the splits, weighted sum of the partials.
 template <int D, int DT>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   constexpr int LPR = D / 8;
@@ -629,36 +628,37 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   const int S = a.seqs[lo].n_splits;
   if (S <= 1) return;
   const int64_t io_row = (int64_t)(a.seqs[lo].q_off + token - a.seqs[lo].cu_q) * a.n_q_heads + h;
+  // Every split's lse and partial row are loaded before any is used: one
+  // memory round trip per row, whatever the split count (a merge of a few
+  // thousand rows is latency-bound, not bandwidth-bound).
+  const uint16_t *po = a.part_o + row * D + sub * 8;
   float ls[kAttnMaxSplits];
-  float mx = -INFINITY;
+  u32x4 x[kAttnMaxSplits];
 #pragma unroll
   for (int s = 0; s < kAttnMaxSplits; ++s) {
-    ls[s] = s < S ? a.part_lse[s * rows + row] : -INFINITY;
-    mx = fmaxf(mx, ls[s]);
+    if (s < S) {
+      ls[s] = a.part_lse[s * rows + row];
+      x[s] = *reinterpret_cast<const u32x4 *>(po + (int64_t)s * rows * D);
+    }
   }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < kAttnMaxSplits; ++s)
+    if (s < S) mx = fmaxf(mx, ls[s]);
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float wsum = 0.f;
-  const uint16_t *po = a.part_o + row * D + sub * 8;
 #pragma unroll
-  for (int s0 = 0; s0 < kAttnMaxSplits; s0 += 4) {
-    if (s0 >= S) break;
-    u32x4 x[4];
+  for (int s = 0; s < kAttnMaxSplits; ++s)
+    if (s < S) {
+      const float wgt = ls[s] == -INFINITY ? 0.f : __expf(ls[s] - mx);
+      wsum += wgt;
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (s0 + u < S) x[u] = *reinterpret_cast<const u32x4 *>(po + (int64_t)(s0 + u) * rows * D);
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (s0 + u < S) {
-        const float wgt = ls[s0 + u] == -INFINITY ? 0.f : __expf(ls[s0 + u] - mx);
-        wsum += wgt;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const f32x2 v = Elem<DT>::unpack(x[u][e]);
-          acc[2 * e] += wgt * v[0];
-          acc[2 * e + 1] += wgt * v[1];
-        }
+      for (int e = 0; e < 4; ++e) {
+        const f32x2 v = Elem<DT>::unpack(x[s][e]);
+        acc[2 * e] += wgt * v[0];
+        acc[2 * e + 1] += wgt * v[1];
       }
-  }
+    }
   const float winv = wsum > 0.f ? 1.f / wsum : 0.f;
   u32x4 pk;
 #pragma unroll
