@@ -308,3 +308,54 @@ def test_planner_counts_the_merge_when_splitting(sc):
     assert splits == [1] * 16 and len(items) >= 1024
     # the default slot count is one workgroup per CU of an MI355X
     assert sc.sc_attn_plan_query([8192], [512], 32, 8, 0)[1] == [4]
+
+
+def test_planner_items_cover_every_query_tile_once(sc):
+    """Plan invariants at any shape: every (sequence, KV head) has all its
+    query tiles (rows of 256 / group heads' worth of queries); the key ranges
+    of one tile's items are contiguous, cover [0, P + q0 + nq) exactly once
+    and number the sequence's split count; regular-cache keys [0, rc) and
+    slot keys never share an item; all items of one (sequence, KV head) run
+    on one XCD (slot w on XCD w % 8)."""
+    rng = np.random.default_rng(2606_16135_31)
+    for _ in range(60):
+        b = int(rng.integers(1, 7))
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        g = int(rng.choice([1, 2, 4, 5, 8]))
+        P = [int(rng.integers(0, 20000)) for _ in range(b)]
+        N = [int(rng.integers(1, 1500)) for _ in range(b)]
+        rc = [16 * int(rng.integers(0, p // 16 + 1)) if rng.random() < 0.4 else 0 for p in P]
+        items, splits = sc.sc_attn_plan_query(P, N, hkv * g, hkv, 256, rc_keys=rc)
+        rows_q = 256 // g
+        groups, xcd = {}, {}
+        for w, it in enumerate(items):
+            seq, kvh, q0, nq, kb, ke, _, paged = (int(x) for x in it)
+            if seq < 0:
+                continue
+            groups.setdefault((seq, kvh, q0), []).append((kb, ke, nq, paged))
+            xcd.setdefault((seq, kvh), set()).add(w % 8)
+        for s in range(b):
+            for h in range(hkv):
+                assert sorted(q0 for (ss, hh, q0) in groups if ss == s and hh == h) == list(range(0, N[s], rows_q))
+                assert len(xcd[(s, h)]) == 1
+        for (s, h, q0), v in groups.items():
+            v.sort()
+            assert len(v) == splits[s]
+            pos = 0
+            for kb, ke, nq, paged in v:
+                assert nq == min(rows_q, N[s] - q0)
+                assert kb == pos and ke >= kb
+                assert (ke <= rc[s]) if paged else (kb >= rc[s])
+                pos = ke
+            assert pos == P[s] + v[0][2] + q0
+
+
+def test_planner_splits_short_turns(sc):
+    """Short new turns (a few hundred keys per query tile) are split down to
+    two-tile ranges so that enough workgroups run: measured on MI355X this
+    takes a P=1024, N=64 attention call (8 query tiles) from 24 to 17 us."""
+    for P, N in [(512, 32), (1024, 64), (2048, 64), (2048, 128)]:
+        items, splits = sc.sc_attn_plan_query([P], [N], 32, 8, 256)
+        assert splits[0] >= 4, (P, N, splits)
+        assert len(items) >= 32
+        assert min(int(it[5]) - int(it[4]) for it in items if it[0] >= 0 and it[5] > it[4]) >= 32
