@@ -447,17 +447,19 @@ sc_status sc_scale_down(int64_t worker_blocks, int32_t worker_block_size, int64_
                         int64_t meu_master, const int64_t *window_lens, int32_t n_window,
                         int64_t *worker_delta, int64_t *master_delta);
 
-/* Message of the last failed call on this thread ("" if none). */
 /*
- * Whether an attention workgroup of an overlapped stack on this table gave
- * up its device-side wait for a slot (and wrote NaN rows) since the table
- * was created or the flag was last cleared.  Reads device memory
- * synchronously: call it only after the streams passed to the stack have
- * been synchronised.  *timed_out = 0 or 1; clear != 0 resets the flag.
- * A table that never ran an overlapped stack reports 0.
+ * Whether a device-side wait of an overlapped stack on this table gave up
+ * since the table was created or the flag was last cleared: an attention
+ * workgroup waiting for its slot to be filled (it wrote NaN rows), or the
+ * copy stream's wait for a slot to be released (that layer's slot was
+ * filled with NaN).  Reads device memory synchronously: call it only after
+ * the streams passed to the stack have been synchronised.  *timed_out = 0
+ * or 1; clear != 0 resets the flag.  A table that never ran an overlapped
+ * stack reports 0.
  */
 sc_status sc_table_stack_status(const sc_table *table, int32_t *timed_out, int32_t clear);
 
+/* Message of the last failed call on this thread ("" if none). */
 const char *sc_last_error(void);
 
 /* Library version string. */
