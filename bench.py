@@ -1,6 +1,6 @@
 """Benchmark of the layer-wise prefix-KV reload + prefill attention path on one GPU.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--turn P,N]
 
 A step is one pass of the whole path over one batch: for every layer of the
 stack, fetch the layer's prefix KV from the donor pool through the block
@@ -102,6 +102,8 @@ def main():
     ap.add_argument("--chunk-tokens", type=int, default=0,
                     help="process the new turn in chunks of this many tokens over each fetched layer "
                          "(0: the whole turn in one attention launch per layer)")
+    ap.add_argument("--turn", type=str, default=None, metavar="P,N",
+                    help="config 2 with prefix P and new turn N tokens (e.g. 1024,64: a short turn)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["attention", "fetch", "copy"], default=None,
                     help="run only one kernel of the path, --steps times over every layer "
@@ -120,7 +122,8 @@ def main():
     sc.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
 
-    wl = W.config(args.config, rc_fraction=args.rc_fraction, dtype=args.dtype)
+    turn = tuple(int(x) for x in args.turn.split(",")) if args.turn else None
+    wl = W.config(args.config, rc_fraction=args.rc_fraction, dtype=args.dtype, turn=turn)
     td = W.torch_dtype(wl)
     dp = DevicePool(sc, wl, fill="torch")
     L = wl.n_layers

@@ -169,7 +169,7 @@ def make_workload(name, n_layers, n_q_heads, n_kv_heads, head_dim, prefix_len,
                     n_rc_blocks=n_rc, dtype=dtype)
 
 
-def config(index, seed=None, rc_fraction=0.0, dtype="bf16"):
+def config(index, seed=None, rc_fraction=0.0, dtype="bf16", turn=None):
     """The five benchmark shapes, numbered 1..5.
 
     1 tiny: 1 layer, 8/8 heads, D=64, prefix 256 (16 blocks) + new 64, pool of
@@ -184,6 +184,8 @@ def config(index, seed=None, rc_fraction=0.0, dtype="bf16"):
     5 long context, 8B shape: prefix 131072, new 2048; pool 2x what is needed,
       half of it on the host-pinned tier.
 
+    ``turn`` = (P, N) replaces shape 2's prefix and new-turn lengths (one
+    conversation of the 8B shape, e.g. a short turn on a short prefix).
     ``rc_fraction`` > 0 gives each sequence a regular-cache tier for that
     fraction of its full prefix blocks (see make_workload); ``dtype="f16"``
     draws fp16 values; the name and description say so.
@@ -196,8 +198,11 @@ def config(index, seed=None, rc_fraction=0.0, dtype="bf16"):
         kw = dict(pool_factor=64 / 20)
         desc = "1 layer, 8/8 heads, D=64, P=256, N=64"
     elif index == 2:
-        name, shape, p, n = "llama3-8b-P8192-N512", (32, 32, 8, 128), [8192], [512]
-        desc = "32 layers, 32q/8kv heads, D=128, P=8192, N=512, batch 1"
+        tp, tn = turn if turn is not None else (8192, 512)
+        if tp < 0 or tn < 1:
+            raise ValueError(f"turn {turn}: need P >= 0 and N >= 1")
+        name, shape, p, n = f"llama3-8b-P{tp}-N{tn}", (32, 32, 8, 128), [tp], [tn]
+        desc = f"32 layers, 32q/8kv heads, D=128, P={tp}, N={tn}, batch 1"
     elif index == 3:
         rng = np.random.default_rng(np.random.SeedSequence([seed, _tag_int("lengths")]))
         p = np.floor(np.clip(rng.lognormal(math.log(4096.0), 0.8, size=16), 512, 32768)).astype(np.int32)
@@ -214,6 +219,8 @@ def config(index, seed=None, rc_fraction=0.0, dtype="bf16"):
         desc = "32 layers, 32q/8kv, D=128, P=131072, N=2048, pool 2x, half host-pinned"
     else:
         raise ValueError(f"unknown config {index}")
+    if turn is not None and index != 2:
+        raise ValueError("turn applies to config 2 only")
     if rc_fraction:
         name += f"-rc{rc_fraction:g}"
         desc += f", regular cache for {rc_fraction:g} of the full prefix blocks"
