@@ -290,28 +290,46 @@ namespace {
 // ---------------------------------------------------------------------------
 // Split-key workspace: one grow-only buffer per (device, stream).  Work on
 // one stream is ordered, so reuse across calls on the same stream is safe.
+// Each buffer has its own lock, which a caller holds from the lookup until
+// the kernels that use the buffer are enqueued: a thread that must grow the
+// buffer (stream sync, free, allocate) can then never free it under another
+// thread that has looked it up but not yet launched with it.  The map only
+// grows, so a Workspace never moves.
 // ---------------------------------------------------------------------------
 struct Workspace {
+  std::mutex mu;
   void *ptr = nullptr;
   size_t bytes = 0;
 };
-std::mutex g_ws_mu;
-std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+std::mutex g_ws_mu;   // guards g_ws itself
+std::map<std::pair<int, hipStream_t>, std::unique_ptr<Workspace>> g_ws;
 
-// Partial log-sum-exps and outputs of split-key attention.
-sc_status get_workspace(int device, hipStream_t stream, size_t bytes, void **out) {
-  std::lock_guard<std::mutex> lk(g_ws_mu);
-  Workspace &ws = g_ws[{device, stream}];
-  if (ws.bytes < bytes) {
-    if (ws.ptr) {
-      SC_HIP(hipStreamSynchronize(stream));
-      SC_HIP(hipFree(ws.ptr));
-      ws = Workspace{};
-    }
-    SC_HIP(hipMalloc(&ws.ptr, bytes));
-    ws.bytes = bytes;
+// Partial log-sum-exps and outputs of split-key attention.  On success
+// *hold owns the buffer's lock; release it after the launches.
+sc_status get_workspace(int device, hipStream_t stream, size_t bytes, void **out,
+                        std::unique_lock<std::mutex> *hold) {
+  Workspace *ws = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    std::unique_ptr<Workspace> &slot = g_ws[{device, stream}];
+    if (!slot) slot.reset(new Workspace());
+    ws = slot.get();
   }
-  *out = ws.ptr;
+  std::unique_lock<std::mutex> lk(ws->mu);
+  if (ws->bytes < bytes) {
+    if (ws->ptr) {
+      // Earlier launches with this buffer were all enqueued on `stream`
+      // before their callers released the lock.
+      SC_HIP(hipStreamSynchronize(stream));
+      SC_HIP(hipFree(ws->ptr));
+      ws->ptr = nullptr;
+      ws->bytes = 0;
+    }
+    SC_HIP(hipMalloc(&ws->ptr, bytes));
+    ws->bytes = bytes;
+  }
+  *out = ws->ptr;
+  *hold = std::move(lk);
   return SC_OK;
 }
 
@@ -405,10 +423,13 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
   a.dtype = dtype;
   if (!(scale > 0.f)) scale = 1.f / std::sqrt((float)head_dim);
   a.scale_log2 = scale * 1.4426950408889634f;
+  // Held until the forward and merge kernels are enqueued (see get_workspace).
+  std::unique_lock<std::mutex> ws_hold;
   if (plan.max_splits > 1) {
     const size_t rows = (size_t)plan.max_splits * plan.total_q * hq;
     void *ws = nullptr;
-    sc_status st = get_workspace(device, stream, rows * ((size_t)head_dim * sizeof(uint16_t) + sizeof(float)), &ws);
+    sc_status st = get_workspace(device, stream, rows * ((size_t)head_dim * sizeof(uint16_t) + sizeof(float)), &ws,
+                                 &ws_hold);
     if (st != SC_OK) return st;
     a.part_o = static_cast<uint16_t *>(ws);
     a.part_lse = reinterpret_cast<float *>(a.part_o + rows * head_dim);
