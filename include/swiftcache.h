@@ -233,6 +233,34 @@ sc_status sc_prefill_attn_f16(const void *q, const void *k_active, const void *v
                               int32_t n_kv_heads, int32_t head_dim, float scale, void *out,
                               float *lse, void *stream);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, arithmetic, work decomposition and result (bit for bit) as
+ * sc_prefill_attn, but the call allocates nothing: no hipMalloc, hipFree or
+ * other allocating routine, and no device work list (each workgroup derives
+ * its (KV head, query tile, key split) from its index).  The split-key
+ * partials live in a file-scope device array of 64 MiB that the library's
+ * code object holds on every device it runs on until the process ends.
+ * That array is shared by every call on the device and keeps the last
+ * call's contents; calls that overlap on one device race on it (issue them
+ * on one stream, or serialise them).
+ * Errors: as sc_prefill_attn, plus SC_ERR_RANGE when the call's key splits
+ * need more than the 64 MiB of partials (splits x new_len x n_q_heads x
+ * (2 head_dim + 4) bytes) or more than 4096 (query tile, split) pairs.
+ */
+sc_status sc_prefill_attn_noalloc(const void *q, const void *k_active, const void *v_active,
+                                  int32_t prefix_len, int32_t new_len, int32_t n_q_heads,
+                                  int32_t n_kv_heads, int32_t head_dim, float scale, void *out,
+                                  float *lse, void *stream);
+
+/* Host only: the key-split count sc_prefill_attn_noalloc uses for one
+ * sequence on `slots` resident workgroups (<= 0: 256), which equals the
+ * split count sc_attn_plan_query reports for the same sequence.
+ * Errors: SC_ERR_INVALID (null splits, negative length, heads),
+ * SC_ERR_RANGE (shape beyond the allocation-free planner's buffers). */
+sc_status sc_attn_noalloc_splits(int32_t prefix_len, int32_t new_len, int32_t n_q_heads,
+                                 int32_t n_kv_heads, int32_t slots, int32_t *splits);
+
 /* The same attention for every sequence of a table (packed varlen layout)
  * at layer `layer`: q, out [sum N][n_q_heads][head_dim]; kv = the active
  * buffer filled by sc_fetch_layer_kv + sc_append_new_kv; lse (nullable)

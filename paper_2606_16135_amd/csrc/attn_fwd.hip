@@ -61,6 +61,7 @@
 #include "sc_internal.h"
 
 #include <cmath>
+#include <mutex>
 #include <type_traits>
 
 namespace sc {
@@ -290,7 +291,7 @@ template <int D, int DT, bool kPaged>
 __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi, uint16_t *smem) {
   using G_ = Geo<D>;
   constexpr int NCH = G_::kChunksPerThread;
-  const SeqDesc sd = a.seqs[wi.seq];
+  const SeqDesc sd = a.seqs != nullptr ? a.seqs[wi.seq] : a.seq0;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -588,10 +589,38 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
   if (half == 0) a.part_lse[prow] = lse_val;
 }
 
+// Item of workgroup w in an implicit work list (see AttnArgs::seq0).
+__device__ __forceinline__ WorkItem implicit_item(const AttnArgs &a, int w) {
+  WorkItem wi{-1, 0, 0, 0, 0, 0, 0, 0};
+  const int S = a.imp_splits;
+  const int per_kvh = a.imp_tiles * S;
+  const int j = w >> 3;
+  const int g = (w & 7) * a.imp_per_xcd + j;
+  if (j >= a.imp_per_xcd || g >= a.n_kv_heads * per_kvh) return wi;
+  const int kvh = g / per_kvh;
+  const int r = g - kvh * per_kvh;
+  const int tile = r / S;
+  const int sp = r - tile * S;
+  const int q0 = tile * a.rows_q;
+  const int nq = min(a.rows_q, a.seq0.n_new - q0);
+  const int keys = a.seq0.prefix + q0 + nq;
+  const int t = (keys + KT - 1) / KT;
+  const int b0 = min(keys, (sp * t / S) * KT);
+  const int b1 = min(keys, ((sp + 1) * t / S) * KT);
+  wi.seq = 0;
+  wi.kvh = kvh;
+  wi.q0 = q0;
+  wi.nq = nq;
+  wi.k_begin = b0;
+  wi.k_end = max(b0, b1);
+  wi.split = sp;
+  return wi;
+}
+
 template <int D, int DT>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t smem[Geo<D>::kSmem];
-  const WorkItem wi = a.items[blockIdx.x];
+  const WorkItem wi = a.items != nullptr ? a.items[blockIdx.x] : implicit_item(a, blockIdx.x);
   if (wi.seq < 0) {
     // Padding slot (XCD placement): no K/V to read, but it counts as done
     // like every other workgroup of the launch.
@@ -625,9 +654,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
       if (a.seqs[mid].cu_q <= token) lo = mid; else hi = mid - 1;
     }
   }
-  const int S = a.seqs[lo].n_splits;
+  const SeqDesc sd = a.seqs != nullptr ? a.seqs[lo] : a.seq0;
+  const int S = sd.n_splits;
   if (S <= 1) return;
-  const int64_t io_row = (int64_t)(a.seqs[lo].q_off + token - a.seqs[lo].cu_q) * a.n_q_heads + h;
+  const int64_t io_row = (int64_t)(sd.q_off + token - sd.cu_q) * a.n_q_heads + h;
   // Every split's lse and partial row are loaded before any is used: one
   // memory round trip per row, whatever the split count (a merge of a few
   // thousand rows is latency-bound, not bandwidth-bound).
@@ -668,7 +698,38 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
     a.lse[(int64_t)h * a.total_q + token] = wsum > 0.f ? mx + __logf(wsum) : -INFINITY;
 }
 
+// Split-key partials of the allocation-free entry point: one array per
+// device, held by the loaded code object until the process ends.  Host code
+// must use the address hipGetSymbolAddress returns, never the symbol.
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
 }  // namespace
+
+hipError_t noalloc_scratch(int device, void **ptr, size_t *bytes) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (addr[device] == nullptr) {
+    // Each device holds its own copy of the array at its own address, so
+    // the lookup runs with that device current.
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != device && (e = hipSetDevice(device)) != hipSuccess) return e;
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != device) (void)hipSetDevice(cur);
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    addr[device] = p;
+  }
+  *ptr = addr[device];
+  *bytes = kNoAllocScratchBytes;
+  return hipSuccess;
+}
 
 hipError_t launch_attn_fwd(const AttnArgs &a, int head_dim, int n_items, hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;

@@ -101,6 +101,67 @@ int64_t lpt_makespan(std::vector<int64_t> &costs, int slots) {
 }
 }  // namespace
 
+// The split count plan_attention chooses for one sequence without a
+// regular cache, computed in fixed-size buffers (no heap memory): the same
+// candidates, item costs, LPT schedule and merge term.  Each (query tile,
+// split) cost stands for n_kv_heads identical items.  Returns false when the
+// candidates' item lists exceed the buffers.
+constexpr int kNoAllocMaxCosts = 4096;
+constexpr int kNoAllocMaxSlots = 2048;
+
+bool single_splits_noalloc(int P, int N, int hq, int hkv, int slots, int *splits_out) {
+  const int group = hq / hkv;
+  const int rows_q = kAttnRows / group;
+  const int n_qt = (N + rows_q - 1) / rows_q;
+  const int64_t max_kv = (int64_t)P + N;
+  if (slots < 1 || slots > kNoAllocMaxSlots) return false;
+  int64_t costs[kNoAllocMaxCosts];
+  int64_t heap[kNoAllocMaxSlots];
+  auto splits_of = [&](int64_t chunk) {
+    return (int)std::min<int64_t>(kMaxSplits, std::max<int64_t>(1, (max_kv + chunk - 1) / chunk));
+  };
+  int64_t best_chunk = std::max<int64_t>(max_kv, 1), best_span = -1, best_items = 0;
+  for (int s = 1; s <= kMaxSplits && n_qt > 0; ++s) {
+    int64_t chunk = (max_kv + s - 1) / s;
+    chunk = ((chunk + kAttnKeyTile - 1) / kAttnKeyTile) * kAttnKeyTile;
+    if (s > 1 && chunk < kMinSplitKeys) break;
+    const int S = splits_of(chunk);
+    if ((int64_t)n_qt * S > kNoAllocMaxCosts) return false;
+    int nc = 0;
+    for (int tile = 0; tile < n_qt; ++tile) {
+      const int q0 = tile * rows_q;
+      const int keys = P + q0 + std::min(rows_q, N - q0);
+      const int t = (keys + kAttnKeyTile - 1) / kAttnKeyTile;
+      for (int sp = 0; sp < S; ++sp) {
+        const int b0 = std::min(keys, (int)((int64_t)sp * t / S) * kAttnKeyTile);
+        const int b1 = std::min(keys, (int)((int64_t)(sp + 1) * t / S) * kAttnKeyTile);
+        costs[nc++] = (std::max(b0, b1) - b0) + kItemOverheadKeys + (S > 1 ? kMergeOverheadKeys : 0);
+      }
+    }
+    std::sort(costs, costs + nc, std::greater<int64_t>());
+    std::fill(heap, heap + slots, (int64_t)0);   // all zero: already a heap
+    auto cmp = std::greater<int64_t>();
+    for (int i = 0; i < nc; ++i)
+      for (int g = 0; g < hkv; ++g) {
+        std::pop_heap(heap, heap + slots, cmp);
+        heap[slots - 1] += costs[i];
+        std::push_heap(heap, heap + slots, cmp);
+      }
+    const int64_t makespan = *std::max_element(heap, heap + slots);
+    const int64_t n = (int64_t)nc * hkv;
+    const int64_t row_splits = S > 1 ? (int64_t)N * hq * (S + 1) : 0;
+    const int64_t merge = row_splits > 0 ? kMergeLaunchKeys + row_splits / kMergeRowSplitsPerKey : 0;
+    const int64_t span = makespan + merge + kItemSharedKeys * n;
+    if (best_span < 0 || span < best_span || (span == best_span && n < best_items)) {
+      best_span = span;
+      best_chunk = chunk;
+      best_items = n;
+    }
+  }
+  *splits_out = splits_of(best_chunk);
+  return true;
+}
+
 int attn_slots(int device) {
   static std::mutex mu;
   static std::map<int, int> cache;
@@ -1176,6 +1237,89 @@ sc_status sc_prefill_attn_f16(const void *q, const void *k_active, const void *v
   clear_error();
   return prefill_attn_single(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_heads, head_dim,
                              SC_DTYPE_F16, scale, out, lse, stream);
+}
+
+sc_status sc_prefill_attn_noalloc(const void *q, const void *k_active, const void *v_active, int32_t prefix_len,
+                                  int32_t new_len, int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                  float scale, void *out, float *lse, void *stream) {
+  clear_error();
+  if (prefix_len < 0 || new_len < 0) return fail(SC_ERR_INVALID, "negative length");
+  sc_status st = check_heads(n_q_heads, n_kv_heads, head_dim);
+  if (st != SC_OK) return st;
+  if (new_len == 0) return SC_OK;
+  if (!q || !k_active || !v_active || !out) return fail(SC_ERR_INVALID, "null argument");
+  if (!aligned16(q) || !aligned16(k_active) || !aligned16(v_active) || !aligned16(out))
+    return fail(SC_ERR_INVALID, "q, k_active, v_active and out must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(lse) & 3) != 0) return fail(SC_ERR_INVALID, "lse must be 4-byte aligned");
+  if (((int64_t)prefix_len + new_len) * n_kv_heads * head_dim * 2 >= ((int64_t)1 << 31))
+    return fail(SC_ERR_UNSUPPORTED, "sequence of %lld tokens x %d KV heads x head_dim %d exceeds 2 GiB of keys",
+                (long long)prefix_len + new_len, n_kv_heads, head_dim);
+  int device = 0;
+  SC_HIP(hipGetDevice(&device));
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || cus <= 0)
+    cus = 256;
+  int S = 1;
+  if (!single_splits_noalloc(prefix_len, new_len, n_q_heads, n_kv_heads, cus * kResidentPerCu, &S))
+    return fail(SC_ERR_RANGE, "new turn of %d tokens needs more work items than the allocation-free planner "
+                "holds (%d query tiles x splits)", new_len, kNoAllocMaxCosts);
+  void *scr = nullptr;
+  size_t scr_bytes = 0;
+  SC_HIP(noalloc_scratch(device, &scr, &scr_bytes));
+  const size_t rows = (size_t)S * new_len * n_q_heads;
+  const size_t need = S > 1 ? rows * ((size_t)head_dim * sizeof(uint16_t) + sizeof(float)) : 0;
+  if (need > scr_bytes)
+    return fail(SC_ERR_RANGE, "%d key splits x %d tokens x %d heads need %zu bytes of split-key scratch; the "
+                "allocation-free entry point has %zu", S, new_len, n_q_heads, need, scr_bytes);
+  const int group = n_q_heads / n_kv_heads;
+  const int rows_q = kAttnRows / group;
+  const int n_qt = (new_len + rows_q - 1) / rows_q;
+  const int64_t total_items = (int64_t)n_kv_heads * n_qt * S;
+  AttnArgs a{};
+  a.q = static_cast<const uint16_t *>(q);
+  a.k = static_cast<const uint16_t *>(k_active);
+  a.v = static_cast<const uint16_t *>(v_active);
+  a.out = static_cast<uint16_t *>(out);
+  a.lse = lse;
+  a.n_seqs = 1;
+  a.total_q = new_len;
+  a.n_q_heads = n_q_heads;
+  a.n_kv_heads = n_kv_heads;
+  a.group = group;
+  a.rows_q = rows_q;
+  a.dtype = SC_DTYPE_BF16;
+  if (!(scale > 0.f)) scale = 1.f / std::sqrt((float)head_dim);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.seq0 = SeqDesc{0, 0, prefix_len, new_len, S, 0, 0, 0};
+  a.imp_tiles = n_qt;
+  a.imp_splits = S;
+  a.imp_per_xcd = (int32_t)((total_items + kXcds - 1) / kXcds);
+  if (S > 1) {
+    a.part_o = static_cast<uint16_t *>(scr);
+    a.part_lse = reinterpret_cast<float *>(a.part_o + rows * head_dim);
+  }
+  hipError_t e = launch_attn_fwd(a, head_dim, kXcds * a.imp_per_xcd, (hipStream_t)stream);
+  if (e != hipSuccess) return fail_hip(e, "attn_fwd launch");
+  if (S > 1) {
+    e = launch_attn_merge(a, head_dim, (hipStream_t)stream);
+    if (e != hipSuccess) return fail_hip(e, "attn_merge launch");
+  }
+  return SC_OK;
+}
+
+sc_status sc_attn_noalloc_splits(int32_t prefix_len, int32_t new_len, int32_t n_q_heads, int32_t n_kv_heads,
+                                 int32_t slots, int32_t *splits) {
+  clear_error();
+  if (!splits) return fail(SC_ERR_INVALID, "null argument");
+  if (prefix_len < 0 || new_len < 0) return fail(SC_ERR_INVALID, "negative length");
+  sc_status st = check_heads(n_q_heads, n_kv_heads, 128);
+  if (st != SC_OK) return st;
+  int S = 1;
+  if (!single_splits_noalloc(prefix_len, new_len, n_q_heads, n_kv_heads, slots > 0 ? slots : kQueryDefaultSlots,
+                             &S))
+    return fail(SC_ERR_RANGE, "shape exceeds the allocation-free planner's buffers");
+  *splits = S;
+  return SC_OK;
 }
 
 sc_status sc_prefill_attn_varlen(sc_pool *pool, const sc_table *table, int32_t layer, const void *q,

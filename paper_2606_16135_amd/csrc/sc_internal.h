@@ -158,6 +158,17 @@ struct AttnArgs {
   int64_t rc_layer_elems;
   int64_t rc_half_elems;
   int32_t block_shift;
+  // Implicit work list (one sequence, no regular cache; the allocation-free
+  // entry point): items == nullptr and seqs == nullptr.  The sequence is
+  // seq0; workgroup w takes item g = (w % 8) * imp_per_xcd + w / 8 of the
+  // list ordered (KV head, query tile, key split), so consecutive items --
+  // one KV head's -- share an XCD.  Split sp of a tile with `keys` keys
+  // covers tiles [sp * t / S, (sp + 1) * t / S) of its t = ceil(keys / 32)
+  // key tiles, exactly as plan_attention divides them.
+  SeqDesc seq0;
+  int32_t imp_tiles;      // query tiles per KV head
+  int32_t imp_splits;     // key splits per query tile (S)
+  int32_t imp_per_xcd;    // items per XCD (grid = 8 * imp_per_xcd)
 };
 
 // Tile geometry the planner and the kernel agree on.
@@ -170,6 +181,10 @@ constexpr int kAttnReadySpinLimit = 1 << 22;
 constexpr int kAttnTestSpinLimit = 256;
 
 hipError_t launch_attn_fwd(const AttnArgs &a, int head_dim, int n_items, hipStream_t stream);
+// Allocation-free calls: the device address of this device's file-scope
+// split-key scratch array (looked up once per device, with that device
+// current) and its size in bytes.
+hipError_t noalloc_scratch(int device, void **ptr, size_t *bytes);
 size_t attn_fwd_lds_bytes(int head_dim);
 int attn_fwd_vgprs(int head_dim);   // per work item, -1 if unknown
 int kv_copy_vgprs();                // largest of the three copy kernels

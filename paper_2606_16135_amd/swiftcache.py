@@ -41,7 +41,8 @@ SC_STACK_TEST_NEVER_FREE = 32
 EXPORTED = [
     "sc_pool_create", "sc_pool_destroy", "sc_pool_layout_get", "sc_table_create",
     "sc_table_destroy", "sc_table_totals", "sc_table_stack_status", "sc_fetch_layer_kv", "sc_append_new_kv",
-    "sc_prefill_attn", "sc_prefill_attn_f16", "sc_prefill_attn_varlen", "sc_store_layer_kv",
+    "sc_prefill_attn", "sc_prefill_attn_f16", "sc_prefill_attn_noalloc", "sc_attn_noalloc_splits",
+    "sc_prefill_attn_varlen", "sc_store_layer_kv",
     "sc_prefill_stack", "sc_prefill_stack_chunked", "sc_attn_plan_query", "sc_pool_resize", "sc_plan_capacity", "sc_elastic_unit", "sc_scale_up",
     "sc_scale_down", "sc_last_error", "sc_version",
 ]
@@ -113,6 +114,8 @@ def load():
         "sc_append_new_kv": (I32, [P, P, VP, VP, ctypes.POINTER(sc_active), VP]),
         "sc_prefill_attn": (I32, [VP, VP, VP, I32, I32, I32, I32, I32, F32, VP, VP, VP]),
         "sc_prefill_attn_f16": (I32, [VP, VP, VP, I32, I32, I32, I32, I32, F32, VP, VP, VP]),
+        "sc_prefill_attn_noalloc": (I32, [VP, VP, VP, I32, I32, I32, I32, I32, F32, VP, VP, VP]),
+        "sc_attn_noalloc_splits": (I32, [I32, I32, I32, I32, I32, i32p]),
         "sc_prefill_attn_varlen": (I32, [P, P, I32, VP, ctypes.POINTER(sc_active), I32, F32, VP, VP, VP]),
         "sc_store_layer_kv": (I32, [P, P, I32, VP, VP, VP]),
         "sc_prefill_stack": (I32, [P, P, I32, ctypes.POINTER(VP), ctypes.POINTER(VP),
@@ -227,6 +230,18 @@ def sc_prefill_attn_f16(q, k_active, v_active, prefix_len, new_len, n_q_heads, n
                         out, lse=0, scale=0.0, stream=0):
     _check(load().sc_prefill_attn_f16(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_heads,
                                       head_dim, scale, out, lse or None, stream or None))
+
+
+def sc_prefill_attn_noalloc(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_heads, head_dim,
+                            out, lse=0, scale=0.0, stream=0):
+    _check(load().sc_prefill_attn_noalloc(q, k_active, v_active, prefix_len, new_len, n_q_heads, n_kv_heads,
+                                          head_dim, scale, out, lse or None, stream or None))
+
+
+def sc_attn_noalloc_splits(prefix_len, new_len, n_q_heads, n_kv_heads, slots=0):
+    s = ctypes.c_int32()
+    _check(load().sc_attn_noalloc_splits(prefix_len, new_len, n_q_heads, n_kv_heads, slots, ctypes.byref(s)))
+    return s.value
 
 
 def sc_prefill_attn_varlen(pool, table, layer, q, kv, n_q_heads, out, lse=0, scale=0.0, stream=0):

@@ -359,3 +359,85 @@ def test_planner_splits_short_turns(sc):
         assert splits[0] >= 4, (P, N, splits)
         assert len(items) >= 32
         assert min(int(it[5]) - int(it[4]) for it in items if it[0] >= 0 and it[5] > it[4]) >= 32
+
+
+def test_noalloc_split_choice_equals_the_planner(sc):
+    """The allocation-free entry point chooses its key splits in fixed-size
+    buffers; for one sequence it must choose what the planner chooses, so
+    that its output equals sc_prefill_attn's bit for bit."""
+    rng = np.random.default_rng(2606_16135_71)
+    shapes = [(8192, 512, 32, 8), (32768, 1024, 40, 8), (131072, 2048, 32, 8), (1024, 64, 32, 8),
+              (0, 1, 8, 8), (5, 300, 8, 2), (3000, 4096, 32, 8)]
+    for _ in range(150):
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        g = int(rng.choice([1, 2, 4, 5, 8, 16]))
+        shapes.append((int(rng.integers(0, 60000)), int(rng.integers(1, 3000)), hkv * g, hkv))
+    for P, N, hq, hkv in shapes:
+        for slots in (256, 240, 64):
+            _, splits = sc.sc_attn_plan_query([P], [N], hq, hkv, slots)
+            assert sc.sc_attn_noalloc_splits(P, N, hq, hkv, slots) == splits[0], (P, N, hq, hkv, slots)
+
+
+def _implicit_items(P, N, hq, hkv, S):
+    """The items the attention kernel derives from its workgroup index when
+    it is launched without a work list (the allocation-free entry point):
+    workgroup w takes entry (w % 8) * per + w // 8 of the list ordered
+    (KV head, query tile, split)."""
+    rows_q = ROWS // (hq // hkv)
+    n_qt = -(-N // rows_q)
+    total = hkv * n_qt * S
+    per = -(-total // 8)
+    out = []
+    for w in range(8 * per):
+        j, g = w // 8, (w % 8) * per + w // 8
+        if j >= per or g >= total:
+            continue
+        kvh, r = divmod(g, n_qt * S)
+        tile, sp = divmod(r, S)
+        q0 = tile * rows_q
+        nq = min(rows_q, N - q0)
+        keys = P + q0 + nq
+        t = -(-keys // KEY_TILE)
+        b0 = min(keys, (sp * t // S) * KEY_TILE)
+        b1 = min(keys, ((sp + 1) * t // S) * KEY_TILE)
+        out.append((0, kvh, q0, nq, b0, max(b0, b1), sp, 0))
+    return out
+
+
+def test_noalloc_implicit_items_equal_the_planned_items(sc):
+    """Without a work list each workgroup derives its item from its index;
+    the set of items must be the planner's for the same sequence (same
+    query tiles, key ranges and split indices, every one exactly once), and
+    one KV head's items must sit on as few XCDs as the list allows."""
+    rng = np.random.default_rng(2606_16135_72)
+    shapes = [(8192, 512, 32, 8), (32768, 1024, 40, 8), (3000, 700, 32, 8), (0, 130, 8, 8), (5000, 40, 8, 2)]
+    for _ in range(60):
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        g = int(rng.choice([1, 2, 4, 5, 8]))
+        shapes.append((int(rng.integers(0, 20000)), int(rng.integers(1, 1500)), hkv * g, hkv))
+    for P, N, hq, hkv in shapes:
+        items, splits = sc.sc_attn_plan_query([P], [N], hq, hkv, 256)
+        planned = sorted(tuple(int(x) for x in it) for it in items if it[0] >= 0)
+        implicit = _implicit_items(P, N, hq, hkv, splits[0])
+        assert sorted(implicit) == planned, (P, N, hq, hkv)
+        assert len(set(implicit)) == len(implicit)
+
+
+def test_noalloc_argument_validation(sc):
+    """Checked before any device work, as for sc_prefill_attn."""
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn_noalloc(1, 1, 1, 4, 4, 12, 8, 128, 1)
+    assert e.value.status == sc.SC_ERR_INVALID
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn_noalloc(1, 1, 1, 4, 4, 8, 8, 80, 1)
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn_noalloc(FAKE_BASE + 2, FAKE_BASE, FAKE_BASE, 4, 4, 8, 8, 128, FAKE_BASE)
+    assert e.value.status == sc.SC_ERR_INVALID and "16-byte aligned" in str(e.value)
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn_noalloc(1, 1, 1, -1, 4, 8, 8, 128, 1)
+    assert e.value.status == sc.SC_ERR_INVALID
+    sc.sc_prefill_attn_noalloc(0, 0, 0, 5, 0, 8, 8, 128, 0)          # new_len == 0 is a no-op
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_attn_noalloc_splits(4, 70000, 32, 8)                   # beyond the fixed buffers
+    assert e.value.status == sc.SC_ERR_RANGE
