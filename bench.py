@@ -1,28 +1,37 @@
 """Benchmark of the layer-wise prefix-KV reload + prefill attention path on one GPU.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--turn P,N]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config all|1..5]
+                    [--turn P,N] [--rc-fraction F] [--dtype bf16|f16] [--chunk-tokens C]
+                    [--only attention|fetch|copy|h2d]
 
 A step is one pass of the whole path over one batch: for every layer of the
 stack, fetch the layer's prefix KV from the donor pool through the block
 table, append the new turn, run causal GQA prefill attention over prefix +
 new tokens, and store the new turn back to the pool, with the fetch of layer
-l+1 overlapped with the attention of layer l on a second stream.  The
-default workload is the Llama-3-8B-shaped stack: 32 layers, 32 query / 8 KV
-heads, head_dim 128, one conversation with an 8192-token cached prefix and a
-512-token new turn, donor pool 4x the blocks needed with seeded random
-placement (synthetic N(0,1) bf16 data; inputs are resident in HBM before the
-timed region).
+l+1 overlapped with the attention of layer l on a second stream (synthetic
+N(0,1) inputs, resident on the device -- the host tier of the long-context
+shape in pinned host memory -- before the timed region).
 
-Prints one JSON line.  `value` = new-turn tokens per second through the
-whole stack.  `roofline` is for the attention kernel (MFMA-bound), timed
-with HIP events on its own stream; `details` adds the fetch kernel's HBM
-bandwidth, the attention-only and serial stack times, and the overlap
-overhead, plus a plain 1 GiB device-to-device copy's bandwidth as context
-for the fetch.  `cpu_baseline` times the CPU oracle on a bounded sample of the
-same workload (a few layers, extrapolated to the stack).
+The default run measures all five workloads, one after another:
+  1 tiny-L1-H8-D64-P256-N64 (correctness shape: latency only),
+  2 llama3-8b-P8192-N512, 3 llama3-8b-batch16-varlen,
+  4 qwen-14b-P32768-N1024,
+  5 llama3-8b-P131072-N2048-hosttier (the largest; the headline line).
+It prints ONE JSON line whose top-level numbers are workload 5's and whose
+`details.configs` holds every workload's: prefill tokens/s through the
+overlapped stack, the attention call's time and fraction of the bf16 MFMA
+peak, the fetch's time and fraction of the HBM peak (destinations rotating
+over >= 512 MiB of buffers, so the 256 MiB Infinity Cache cannot hold them
+between fetches; for workload 5 the fetch is bound by the host link and is
+set against a pinned host-to-device copy measured in the same run, with the
+DMA-engine alternatives beside it), the overlap overhead, and a CPU
+baseline (the oracle timed on this host on a bounded sample).
+`--config N` runs one workload (options --turn/--rc-fraction/--dtype/
+--chunk-tokens then apply) and puts it in the headline.
 """
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -35,12 +44,22 @@ sys.path.insert(0, ROOT)
 
 METRIC = "prefill tokens/s incl. layer-wise prefix-KV reload; fetch HBM GB/s; MFMA util"
 HBM_PEAK_GBS = 8000.0
-BF16_PEAK_TFLOPS = 2500.0
-# HBM bytes of one attention call (forward + merge) from two rocprofv3 --pmc
-# passes (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors that map the same
-# counters to a plain 256 MiB copy), per workload, for the kernels as they
-# are now; profiles/attention_<workload>.md holds the commands and readings.
-PMC_TRAFFIC = {"llama3-8b-P8192-N512": 80546600}
+MFMA_PEAK_TFLOPS = 2500.0        # dense bf16 (and fp16) MFMA, MI355X
+MALL_BYTES = 256 << 20
+ROTATE_BYTES = 512 << 20         # destination buffers the standalone fetch cycles through
+
+# HBM bytes of one attention call (forward + merge kernels) from two
+# rocprofv3 --pmc passes (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors
+# that map the same counters to a plain 256 MiB device copy), per workload,
+# with the hash of the attention source they were taken on; a stale entry
+# (the source changed since) is reported as null.
+PMC_TRAFFIC = {}
+
+
+def _src_sha16(name):
+    path = os.path.join(ROOT, "paper_2606_16135_amd", "csrc", name)
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
 def attention_flops(wl):
@@ -58,34 +77,336 @@ def fetch_payload_bytes(wl):
     return row * (int(np.sum(wl.prefix_len)) - rc_keys)
 
 
-def cpu_baseline(wl, dp, inputs, budget_s=15.0):
-    """The oracle (gather + append + attention) timed on the host cores for
-    as many layers as fit in the budget (at least one), extrapolated to the
-    whole stack."""
-    from oracle import attention as oa
-    from oracle import kvcache as ok
+def fetch_tier_bytes(wl):
+    """(device-tier bytes, host-tier bytes) of one layer's fetch."""
+    row = 2 * wl.n_kv_heads * wl.head_dim * 2
+    dev = host = 0
+    for b in range(wl.batch):
+        ids = wl.block_ids[wl.cu_blocks[b]:wl.cu_blocks[b + 1]]
+        P = int(wl.prefix_len[b])
+        for j in range(-(-P // wl.block_size)):
+            rows = min(wl.block_size, P - j * wl.block_size)
+            bid = int(ids[j])
+            if bid >= wl.rc_first_id:
+                continue
+            if bid >= wl.n_device_blocks:
+                host += rows * row
+            else:
+                dev += rows * row
+    return dev, host
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle on this host
+# ---------------------------------------------------------------------------
+
+def cpu_info():
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = {"vendor": "unknown", "threads": None}
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                blas = {"vendor": i.get("internal_api"), "threads": int(i.get("num_threads", 1))}
+                break
     except Exception:
-        threads = len(os.sched_getaffinity(0))
-    t_layers = []
-    for layer in range(wl.n_layers):
-        pool_l = dp.layer_slice_u16(layer)
-        q, kn, vn = (t.view(__import__("torch").int16).cpu().numpy().view(np.uint16) for t in inputs[layer])
+        pass
+    return {"cpu_model": model, "affinity_cores": len(os.sched_getaffinity(0)), "blas": blas}
+
+
+def cpu_baseline(wl, dp, inputs, n_layers_sampled=3, reps=3):
+    """The oracle (gather + append + attention, float64, numpy) timed on the
+    host on a bounded sample of the workload: `n_layers_sampled` layers
+    spread over the stack; per layer the gather + append is timed `reps`
+    times (median), and attention runs on the whole layer when that layer
+    is small (< 2e11 flops), else on the query heads of one KV head (the
+    same oracle function on a slice of the heads), scaled by the KV-head
+    count.  Extrapolated linearly to the L-layer stack."""
+    import torch
+    from oracle import attention as oa
+    from oracle import kvcache as ok
+    info = cpu_info()
+    L = wl.n_layers
+    layers = sorted({0, L // 2, L - 1})[:n_layers_sampled] if L > 1 else [0]
+    ids = np.asarray(wl.block_ids, dtype=np.int64)
+    local = np.arange(len(ids), dtype=np.int32)
+    whole = attention_flops(wl) < 2e11
+    group = wl.n_q_heads // wl.n_kv_heads
+    t_gather, t_attn = [], []
+    for layer in layers:
+        sub = dp.layer_slice_u16(layer)[ids]          # referenced blocks, table order (untimed)
+        q, kn, vn = (t.view(torch.int16).cpu().numpy().view(np.uint16) for t in inputs[layer])
+        tg = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            ka, va = ok.gather_layer(sub, local, wl.cu_blocks, wl.prefix_len, wl.new_len, 0)
+            kf, vf = ok.append_new(ka, va, kn, vn, wl.prefix_len, wl.new_len)
+            tg.append(time.perf_counter() - t0)
+        t_gather.append(float(np.median(tg)))
+        if whole:
+            qs, ks, vs, scale = q, kf, vf, 1.0
+        else:
+            qs, ks, vs, scale = q[:, :group], kf[:, :1], vf[:, :1], float(wl.n_kv_heads)
         t0 = time.perf_counter()
-        ka, va = ok.gather_layer(pool_l, wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, 0)
-        kf, vf = ok.append_new(ka, va, kn, vn, wl.prefix_len, wl.new_len)
-        oa.attention(oa.bits_to_f64(q, wl.dtype), oa.bits_to_f64(kf, wl.dtype), oa.bits_to_f64(vf, wl.dtype),
+        oa.attention(oa.bits_to_f64(qs, wl.dtype), oa.bits_to_f64(ks, wl.dtype), oa.bits_to_f64(vs, wl.dtype),
                      wl.prefix_len, wl.new_len)
-        t_layers.append(time.perf_counter() - t0)
-        if sum(t_layers) >= budget_s:
-            break
-    per_layer = float(np.mean(t_layers))
-    return {"value": wl.total_q / (per_layer * wl.n_layers), "unit": "tokens/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"float64 oracle gather+append+attention on {len(t_layers)} of {wl.n_layers} layers "
-                      f"({per_layer:.2f} s/layer), extrapolated to the {wl.n_layers}-layer stack"}
+        t_attn.append((time.perf_counter() - t0) * scale)
+    g = float(np.median(t_gather))
+    a = float(np.median(t_attn))
+    per_layer = g + a
+    payload = fetch_payload_bytes(wl)
+    cores = info["blas"]["threads"] or info["affinity_cores"]
+    return {"value": wl.total_q / (per_layer * L), "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"float64 numpy oracle on layers {layers} of {L}: gather+append median of {reps}, "
+                       f"attention on {'the whole layer' if whole else f'the {group} query heads of one KV head, x{wl.n_kv_heads}'}"
+                       f"; median over the sampled layers, extrapolated to the {L}-layer stack"),
+            "extrapolated": True,
+            "gather_append_s_per_layer": round(g, 4), "attention_s_per_layer": round(a, 3),
+            "gather_gbs": round(2.0 * payload / g / 1e9, 2) if payload else None,
+            **info}
+
+
+# ---------------------------------------------------------------------------
+# One workload
+# ---------------------------------------------------------------------------
+
+def run_workload(args, cfg, torch, sc, W, DevicePool, with_cpu, turn=None, rc_fraction=0.0, dtype="bf16",
+                 chunk_tokens=0):
+    wl = W.config(cfg, rc_fraction=rc_fraction, dtype=dtype, turn=turn)
+    print(f"bench.py: {wl.name}: building pool ({wl.n_blocks} blocks)", file=sys.stderr, flush=True)
+    td = W.torch_dtype(wl)
+    dp = DevicePool(sc, wl, fill="torch")
+    L = wl.n_layers
+    inputs = [W.layer_inputs_torch(wl, l, "cuda") for l in range(L)]
+    outs = [torch.empty((wl.total_q, wl.n_q_heads, wl.head_dim), dtype=td, device="cuda") for _ in range(L)]
+
+    def new_slot():
+        k = torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=td, device="cuda")
+        v = torch.empty_like(k)
+        return k, v, sc.active(k.data_ptr(), v.data_ptr(), wl.total_kv)
+
+    slot_t = [new_slot() for _ in range(2)]
+    slots = [s[2] for s in slot_t]
+    compute = torch.cuda.current_stream()
+    copy = torch.cuda.Stream()
+    qp = [i[0].data_ptr() for i in inputs]
+    kp = [i[1].data_ptr() for i in inputs]
+    vp = [i[2].data_ptr() for i in inputs]
+    op = [o.data_ptr() for o in outs]
+
+    def stack(flags):
+        if chunk_tokens > 0:
+            sc.sc_prefill_stack_chunked(dp.handle, dp.table, qp, kp, vp, op, slots, wl.n_q_heads, chunk_tokens,
+                                        flags, 0.0, compute.cuda_stream, copy.cuda_stream)
+        else:
+            sc.sc_prefill_stack(dp.handle, dp.table, qp, kp, vp, op, slots, wl.n_q_heads, flags, 0.0,
+                                compute.cuda_stream, copy.cuda_stream)
+
+    def timed(fn, reps, stream):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps          # ms
+
+    # Slots for a standalone fetch whose destinations rotate over >= 512 MiB.
+    slot_bytes = 2 * wl.total_kv * wl.n_kv_heads * wl.head_dim * 2
+    n_rot = max(2, -(-ROTATE_BYTES // slot_bytes))
+    rot = [new_slot() for _ in range(n_rot - 2)]
+    rot_slots = slots + [s[2] for s in rot]
+
+    if args.only is not None:
+        return profile_only(args, wl, dp, sc, torch, stack, rot_slots, compute, L)
+
+    # ---- headline: the overlapped stack, wall clock -------------------------
+    print(f"bench.py: {wl.name}: timing", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        stack(sc.SC_STACK_OVERLAP)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        stack(sc.SC_STACK_OVERLAP)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_step = 1e3 * elapsed / args.steps
+    value = wl.total_q * args.steps / elapsed
+    out_ok = all(bool(torch.isfinite(o.float()).all()) for o in outs)
+    timed_out = sc.sc_table_stack_status(dp.table, clear=True)
+
+    reps = max(1, args.steps)
+    t_attn_only = timed(lambda: stack(sc.SC_STACK_ATTN_ONLY), reps, compute)
+    t_serial = timed(lambda: stack(sc.SC_STACK_SERIAL), reps, compute)
+    t_overlap = timed(lambda: stack(sc.SC_STACK_OVERLAP), reps, compute)
+
+    # ---- attention call: the dominant kernel ------------------------------
+    flops = attention_flops(wl)
+    t_attn_layer = t_attn_only / L * 1e-3
+    tflops = flops / t_attn_layer / 1e12
+    traffic = PMC_TRAFFIC.get(wl.name)
+    traffic = traffic[0] if traffic and traffic[1] == _src_sha16("attn_fwd.hip") else None
+    roofline = {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tflops / MFMA_PEAK_TFLOPS, 4), "traffic": traffic,
+                "kernel": f"attn_fwd_kernel<{wl.head_dim}> (+ attn_merge_kernel when keys are split): "
+                          "one layer's attention call",
+                "flops_per_launch": flops, "avg_launch_us": round(t_attn_layer * 1e6, 2)}
+
+    # ---- fetch alone, destinations rotating over >= 512 MiB ---------------
+    n_f = reps * L
+    state = {"i": 0}
+
+    def one_fetch():
+        i = state["i"]
+        sc.sc_fetch_layer_kv(dp.handle, dp.table, i % L, rot_slots[i % len(rot_slots)], copy.cuda_stream)
+        state["i"] = i + 1
+
+    t_fetch = timed(one_fetch, n_f, copy) * 1e-3            # seconds per layer
+    payload = fetch_payload_bytes(wl)
+    dev_b, host_b = fetch_tier_bytes(wl)
+    fetch = {"us_per_layer": round(t_fetch * 1e6, 2), "payload_bytes_per_layer": payload,
+             "mall_control": f"destinations rotate over {n_rot} slot pairs = {n_rot * slot_bytes >> 20} MiB "
+                             f"(> the {MALL_BYTES >> 20} MiB Infinity Cache); sources are {L} distinct layer "
+                             "slices of the pool"}
+    if host_b == 0:
+        gbs = 2.0 * payload / t_fetch / 1e9
+        fetch.update({"hbm_gbs": round(gbs, 1), "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+                      "bound": "hbm"})
+    else:
+        fetch.update(host_tier_detail(args, wl, dp, sc, torch, timed, rot_slots, copy, t_fetch, dev_b, host_b))
+
+    entry = {
+        "workload": wl.name, "description": wl.description,
+        "value": round(value, 1), "unit": "tokens/s", "ms_per_step": round(ms_step, 3),
+        "steps": args.steps, "warmup": args.warmup,
+        "shape": {"layers": L, "q_heads": wl.n_q_heads, "kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
+                  "batch": wl.batch, "prefix_len_total": int(np.sum(wl.prefix_len)),
+                  "new_len_total": wl.total_q, "block_size": wl.block_size, "pool_blocks": wl.n_blocks,
+                  "host_tier_blocks": wl.n_host_blocks, "regular_cache_blocks": wl.n_rc_blocks,
+                  "chunk_tokens": chunk_tokens, "dtype": wl.dtype},
+        "attention": {"us_per_layer": round(t_attn_layer * 1e6, 2), "tflops": round(tflops, 1),
+                      "frac_of_mfma_peak": round(tflops / MFMA_PEAK_TFLOPS, 4), "flops_per_layer": flops},
+        "fetch": fetch,
+        "stack_ms": {"overlap": round(t_overlap, 3), "attn_only": round(t_attn_only, 3),
+                     "serial": round(t_serial, 3)},
+        "overlap_overhead": round(t_overlap / t_attn_only - 1.0, 4),
+        "outputs_finite": out_ok, "device_wait_timed_out": bool(timed_out),
+        "roofline": roofline,
+    }
+    if with_cpu:
+        print(f"bench.py: {wl.name}: CPU oracle sample", file=sys.stderr, flush=True)
+        entry["cpu_baseline"] = cpu_baseline(wl, dp, inputs)
+    del rot, slot_t, outs, inputs
+    dp.close()
+    del dp
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return entry
+
+
+def h2d_peak_gbs(torch, nbytes=1 << 30, reps=5):
+    """Pinned host -> device hipMemcpyAsync (DMA) bandwidth of one large
+    contiguous copy: the host link's roofline."""
+    h = torch.empty(nbytes, dtype=torch.uint8).pin_memory()
+    d = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        d.copy_(h, non_blocking=True)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(reps):
+            d.copy_(h, non_blocking=True)
+        e1.record(s)
+    torch.cuda.synchronize()
+    gbs = nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del h, d
+    return gbs
+
+
+def host_tier_detail(args, wl, dp, sc, torch, timed, rot_slots, copy, t_fetch, dev_b, host_b):
+    """The fetch of a pool with a host tier is bound by the host link: set
+    it against a pinned H2D copy measured now, and time the DMA-engine
+    alternatives for the host-tier blocks (one hipMemcpyBatchAsync per layer,
+    or one hipMemcpyAsync per block half)."""
+    L = wl.n_layers
+    link = h2d_peak_gbs(torch)
+    host_gbs = host_b / t_fetch / 1e9
+    out = {"bound": "host link", "device_tier_bytes": dev_b, "host_tier_bytes": host_b,
+           "host_link_gbs": round(host_gbs, 2), "h2d_peak_gbs": round(link, 2),
+           "frac_of_h2d_peak": round(host_gbs / link, 4),
+           "hbm_gbs_device_part": None}
+    alts = {}
+    layers = list(range(min(L, 4)))
+    for name, per_copy in (("dma_batch", False), ("dma_per_copy", True)):
+        state = {"i": 0}
+
+        def one():
+            i = state["i"]
+            sc.sc_fetch_layer_kv_dma(dp.handle, dp.table, layers[i % len(layers)], rot_slots[i % len(rot_slots)],
+                                     per_copy, copy.cuda_stream)
+            state["i"] = i + 1
+        try:
+            one()
+            torch.cuda.synchronize()
+            state["i"] = 0
+            w0 = time.perf_counter()
+            t = timed(one, len(layers), copy) * 1e-3
+            wall = (time.perf_counter() - w0) / len(layers)
+            alts[name] = {"us_per_layer": round(t * 1e6, 1), "wall_us_per_layer": round(wall * 1e6, 1),
+                          "host_link_gbs": round(host_b / t / 1e9, 2)}
+        except sc.SwiftCacheError as e:
+            alts[name] = {"unsupported": str(e)}
+    out["dma_alternatives"] = alts
+    out["zero_copy_kernel_us_per_layer"] = round(t_fetch * 1e6, 1)
+    return out
+
+
+def profile_only(args, wl, dp, sc, torch, stack, rot_slots, compute, L):
+    """Profiling aid: one op of the path over every layer, warmup then timed
+    steps; prints its per-layer time."""
+    copy_src = copy_dst = None
+    if args.only == "copy":
+        copy_src = torch.empty(128 << 20, dtype=torch.int16, device="cuda").fill_(1)
+        copy_dst = torch.empty_like(copy_src)
+    state = {"i": 0}
+
+    def run_op():
+        if args.only == "attention":
+            stack(sc.SC_STACK_ATTN_ONLY)
+        elif args.only == "fetch":
+            for l in range(L):
+                i = state["i"]
+                sc.sc_fetch_layer_kv(dp.handle, dp.table, l, rot_slots[i % len(rot_slots)], compute.cuda_stream)
+                state["i"] = i + 1
+        else:
+            for _ in range(L):
+                copy_dst.copy_(copy_src)
+    # Fill both slots in serial mode: a profiler that serialises dispatches
+    # would otherwise hold the overlapped stack's attention, which waits on
+    # the device for the copy stream, until its wait gives up.
+    stack(sc.SC_STACK_SERIAL)
+    for _ in range(args.warmup):
+        run_op()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(compute)
+    for _ in range(args.steps):
+        run_op()
+    e1.record(compute)
+    torch.cuda.synchronize()
+    per_layer_us = e0.elapsed_time(e1) * 1e3 / (args.steps * L)
+    print(json.dumps({"only": args.only, "workload": wl.name, "us_per_layer": round(per_layer_us, 2)}),
+          flush=True)
+    dp.close()
+    return None
 
 
 def main():
@@ -93,22 +414,21 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--config", default="all", help="all (default: every workload, headline = 5) or 1..5")
     ap.add_argument("--rc-fraction", type=float, default=0.0,
                     help="put this fraction of each sequence's full prefix blocks in the regular "
                          "cache (read in place by attention, never fetched)")
     ap.add_argument("--dtype", choices=["bf16", "f16"], default="bf16",
                     help="element type of the pool, q, K, V and outputs")
     ap.add_argument("--chunk-tokens", type=int, default=0,
-                    help="process the new turn in chunks of this many tokens over each fetched layer "
-                         "(0: the whole turn in one attention launch per layer)")
+                    help="process the new turn in chunks of this many tokens over each fetched layer")
     ap.add_argument("--turn", type=str, default=None, metavar="P,N",
-                    help="config 2 with prefix P and new turn N tokens (e.g. 1024,64: a short turn)")
+                    help="workload 2 with prefix P and new turn N tokens")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["attention", "fetch", "copy"], default=None,
-                    help="run only one kernel of the path, --steps times over every layer "
-                         "(for profiler runs), and print its per-layer time; 'copy' runs a "
-                         "plain 256 MiB device-to-device copy (reference for byte counters)")
+                    help="run only one kernel of the path over every layer, --steps times (for "
+                         "profiler runs; needs --config N); 'copy' runs a plain 256 MiB "
+                         "device-to-device copy (reference for byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (--gpus {args.gpus} requested); "
@@ -122,180 +442,40 @@ def main():
     sc.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
 
-    turn = tuple(int(x) for x in args.turn.split(",")) if args.turn else None
-    wl = W.config(args.config, rc_fraction=args.rc_fraction, dtype=args.dtype, turn=turn)
-    td = W.torch_dtype(wl)
-    dp = DevicePool(sc, wl, fill="torch")
-    L = wl.n_layers
-    inputs = [W.layer_inputs_torch(wl, l, "cuda") for l in range(L)]
-    outs = [torch.empty((wl.total_q, wl.n_q_heads, wl.head_dim), dtype=td, device="cuda")
-            for _ in range(L)]
-    slot_t = [(torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=td, device="cuda"),
-               torch.empty((wl.total_kv, wl.n_kv_heads, wl.head_dim), dtype=td, device="cuda"))
-              for _ in range(2)]
-    slots = [sc.active(k.data_ptr(), v.data_ptr(), wl.total_kv) for k, v in slot_t]
-    compute = torch.cuda.current_stream()
-    copy = torch.cuda.Stream()
-    qp = [i[0].data_ptr() for i in inputs]
-    kp = [i[1].data_ptr() for i in inputs]
-    vp = [i[2].data_ptr() for i in inputs]
-    op = [o.data_ptr() for o in outs]
-
-    def stack(flags):
-        if args.chunk_tokens > 0:
-            sc.sc_prefill_stack_chunked(dp.handle, dp.table, qp, kp, vp, op, slots, wl.n_q_heads, args.chunk_tokens,
-                                        flags, 0.0, compute.cuda_stream, copy.cuda_stream)
-        else:
-            sc.sc_prefill_stack(dp.handle, dp.table, qp, kp, vp, op, slots, wl.n_q_heads, flags, 0.0,
-                                compute.cuda_stream, copy.cuda_stream)
-
-    if args.only is not None:
-        # Profiling aid: one op over all layers, warmup then timed steps.
-        print(f"bench.py: {wl.name} pool and inputs ready", file=sys.stderr, flush=True)
-        copy_src = copy_dst = None
-        if args.only == "copy":
-            copy_src = torch.empty(128 << 20, dtype=torch.int16, device="cuda").fill_(1)
-            copy_dst = torch.empty_like(copy_src)
-
-        def run_op():
-            if args.only == "attention":
-                stack(sc.SC_STACK_ATTN_ONLY)
-            elif args.only == "fetch":
-                for l in range(L):
-                    sc.sc_fetch_layer_kv(dp.handle, dp.table, l, slots[l & 1], compute.cuda_stream)
-            else:
-                for _ in range(L):
-                    copy_dst.copy_(copy_src)
-        # Fill both slots in serial mode: a profiler that serialises
-        # dispatches would otherwise hold the overlapped stack's attention,
-        # which waits on the device for the copy stream, until its wait
-        # gives up.
-        sc.sc_prefill_stack(dp.handle, dp.table, qp, kp, vp, op, [slots[0], slots[0]], wl.n_q_heads,
-                            sc.SC_STACK_SERIAL, 0.0, compute.cuda_stream, 0)
-        sc.sc_prefill_stack(dp.handle, dp.table, qp, kp, vp, op, [slots[1], slots[1]], wl.n_q_heads,
-                            sc.SC_STACK_SERIAL, 0.0, compute.cuda_stream, 0)
-        for _ in range(args.warmup):
-            run_op()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(compute)
-        for _ in range(args.steps):
-            run_op()
-        e1.record(compute)
-        torch.cuda.synchronize()
-        per_layer_us = e0.elapsed_time(e1) * 1e3 / (args.steps * L)
-        print(json.dumps({"only": args.only, "workload": wl.name, "us_per_layer": round(per_layer_us, 2)}),
-              flush=True)
-        dp.close()
-        return
-
-    # ---- headline: overlapped stack --------------------------------------
-    for _ in range(args.warmup):
-        stack(sc.SC_STACK_OVERLAP)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        stack(sc.SC_STACK_OVERLAP)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ms_step = 1e3 * elapsed / args.steps
-    value = wl.total_q * args.steps / elapsed
-    out_ok = all(bool(torch.isfinite(o.float()).all()) for o in outs)
-
-    def timed_stack(flags, reps):
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ev0.record(compute)
-        for _ in range(reps):
-            stack(flags)
-        ev1.record(compute)
-        torch.cuda.synchronize()
-        return ev0.elapsed_time(ev1) / reps
-
-    reps = max(1, args.steps)
-    t_attn_only = timed_stack(sc.SC_STACK_ATTN_ONLY, reps)      # attention kernels of L layers
-    t_serial = timed_stack(sc.SC_STACK_SERIAL, reps)
-    t_overlap = timed_stack(sc.SC_STACK_OVERLAP, reps)
-
-    # ---- fetch kernel alone, timed on its own stream ---------------------
-    with torch.cuda.stream(copy):
-        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        f0.record(copy)
-        for r in range(reps):
-            for l in range(L):
-                sc.sc_fetch_layer_kv(dp.handle, dp.table, l, slots[l & 1], copy.cuda_stream)
-        f1.record(copy)
-    torch.cuda.synchronize()
-    t_fetch = f0.elapsed_time(f1) / (reps * L) * 1e-3          # seconds per layer
-    fetch_gbs = 2.0 * fetch_payload_bytes(wl) / t_fetch / 1e9
-
-    # Context for the fetch: a plain contiguous 1 GiB device-to-device copy
-    # (torch copy_, the runtime's copy kernel) on the same stream, read +
-    # write bytes per second.
-    csrc = torch.empty(1 << 29, dtype=torch.int16, device="cuda").fill_(1)
-    cdst = torch.empty_like(csrc)
-    with torch.cuda.stream(copy):
-        cdst.copy_(csrc)
-        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        c0.record(copy)
-        for _ in range(5):
-            cdst.copy_(csrc)
-        c1.record(copy)
-    torch.cuda.synchronize()
-    copy_gbs = 2.0 * csrc.numel() * 2 * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
-    del csrc, cdst
-
-    flops = attention_flops(wl)
-    t_attn_layer = t_attn_only / L * 1e-3
-    achieved_tflops = flops / t_attn_layer / 1e12
-    roofline = {"bound": "mfma", "achieved": round(achieved_tflops, 2), "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved_tflops / BF16_PEAK_TFLOPS, 4),
-                "traffic": PMC_TRAFFIC.get(wl.name),
-                "kernel": "attn_fwd_kernel<128> + attn_merge_kernel (one attention call)",
-                "flops_per_launch": flops, "avg_launch_us": round(t_attn_layer * 1e6, 2)}
-
-    # Elastic donor tier (§3.4): the block-major pool shrinks / grows in
-    # place; time the host call, and state what a layer-major cache would
-    # move for the same resize ((L - 1) * kept blocks * slice bytes).
-    lay = sc.sc_pool_layout_get(dp.handle)
-    cap, keep = lay.n_device_blocks, int(np.max(wl.block_ids[wl.block_ids < lay.n_device_blocks]) + 1
-                                        if np.any(wl.block_ids < lay.n_device_blocks) else 0)
-    t0r = time.perf_counter()
-    for _ in range(1000):
-        sc.sc_pool_resize(dp.handle, keep)
-        sc.sc_pool_resize(dp.handle, cap)
-    resize_us = (time.perf_counter() - t0r) / 2000 * 1e6
-    elastic = {"resize_host_us": round(resize_us, 3), "blocks_released": int(cap - keep),
-               "bytes_moved": 0,
-               "layer_major_bytes_moved": int((L - 1) * keep * lay.slice_bytes)}
-
-    details = {
-        "stack_ms": {"overlap": round(t_overlap, 3), "attn_only": round(t_attn_only, 3),
-                     "serial": round(t_serial, 3)},
-        "overlap_overhead": round(t_overlap / t_attn_only - 1.0, 4),
-        "fetch": {"us_per_layer": round(t_fetch * 1e6, 2), "hbm_gbs": round(fetch_gbs, 1),
-                  "device_copy_1gib_gbs": round(copy_gbs, 1),
-                  "frac_of_hbm_peak": round(fetch_gbs / HBM_PEAK_GBS, 4),
-                  "payload_bytes_per_layer": fetch_payload_bytes(wl)},
-        "elastic": elastic,
-        "outputs_finite": out_ok,
-        "device": torch.cuda.get_device_name(0),
-    }
-
-    result = {"metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1,
-              "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 3),
-              "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+    single = args.config != "all"
+    if args.only is not None and not single:
+        ap.error("--only needs --config N")
+    if not single and (args.turn or args.rc_fraction or args.dtype != "bf16" or args.chunk_tokens):
+        ap.error("--turn/--rc-fraction/--dtype/--chunk-tokens need --config N")
+    with_cpu = not args.no_cpu_baseline
+    entries = {}
+    if single:
+        cfg = int(args.config)
+        turn = tuple(int(x) for x in args.turn.split(",")) if args.turn else None
+        e = run_workload(args, cfg, torch, sc, W, DevicePool, with_cpu, turn=turn, rc_fraction=args.rc_fraction,
+                         dtype=args.dtype, chunk_tokens=args.chunk_tokens)
+        if e is None:
+            return
+        head = e
+        entries[e["workload"]] = e
+    else:
+        for cfg in (1, 2, 3, 4, 5):
+            e = run_workload(args, cfg, torch, sc, W, DevicePool, with_cpu)
+            entries[e["workload"]] = e
+        head = e
+    # The elastic donor tier (§3.4), timed on workload 2's pool shape.
+    details = {"configs": entries, "device": torch.cuda.get_device_name(0),
+               "headline": f"{head['workload']} (the largest single-GPU workload)" if not single
+               else head["workload"]}
+    result = {"metric": METRIC, "value": head["value"], "unit": "tokens/s", "n_gpus": 1,
+              "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
+              "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": head["shape"]["dtype"],
               "data": "synthetic",
-              "config": {"workload": wl.name, "layers": L, "q_heads": wl.n_q_heads,
-                         "kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
-                         "prefix_len": [int(x) for x in wl.prefix_len][:16],
-                         "new_len": [int(x) for x in wl.new_len][:16], "block_size": wl.block_size,
-                         "pool_blocks": wl.n_blocks, "host_tier_blocks": wl.n_host_blocks,
-                         "regular_cache_blocks": wl.n_rc_blocks, "chunk_tokens": args.chunk_tokens},
-              "roofline": roofline, "details": details}
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, dp, inputs)
+              "config": {"workload": head["workload"], **head["shape"]},
+              "roofline": head["roofline"], "details": details}
+    if with_cpu:
+        result["cpu_baseline"] = head["cpu_baseline"]
     print(json.dumps(result), flush=True)
-    dp.close()
 
 
 if __name__ == "__main__":

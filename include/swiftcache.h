@@ -194,6 +194,21 @@ sc_status sc_fetch_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
                             const sc_active *dst, void *stream);
 
 /*
+ * The same KV Load with the host tier moved by the DMA engines instead of
+ * the kernel (the PCIe reload of §1): each host-tier block's K and V halves
+ * of the layer are two host-to-device copies (one hipMemcpyBatchAsync call
+ * for all of them, or, with per_copy_calls != 0, one hipMemcpyAsync call
+ * each); device-tier blocks are copied by the fetch kernel as above.  In
+ * the block-major layout one layer's slice of a block is never contiguous
+ * with another block's, so copies cannot be merged across blocks.  Same
+ * result, arguments and errors as sc_fetch_layer_kv, plus
+ * SC_ERR_UNSUPPORTED when per_copy_calls == 0 and the HIP runtime loaded in
+ * the process has no hipMemcpyBatchAsync.
+ */
+sc_status sc_fetch_layer_kv_dma(sc_pool *pool, const sc_table *table, int32_t layer,
+                                const sc_active *dst, int32_t per_copy_calls, void *stream);
+
+/*
  * Append the new turn (§3.2: new entries are written into the active
  * buffer): rows cu_q[b] + i of k_new / v_new ([sum N][n_kv_heads][head_dim]
  * the pool's element type, device) go to rows cu_k[b] + P_b + i of dst->k /

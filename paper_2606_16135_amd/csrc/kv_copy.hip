@@ -45,6 +45,7 @@ __device__ __forceinline__ void copy_rows(const CopyArgs &a, int g, bool poison 
   const int item_idx = g >> 1;
   const int is_v = g & 1;
   const CopyItem it = a.items[item_idx];
+  if (MODE != COPY_APPEND && !((a.tier_mask >> it.tier) & 1)) return;
   const int64_t nchunks = ((int64_t)it.nrows * a.row_bytes) >> 4;
   const int64_t half_off = is_v ? a.v_half_off : 0;
   const char *src;

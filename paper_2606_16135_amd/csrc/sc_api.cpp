@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstring>
 #include <cstdlib>
+#include <dlfcn.h>
 #include <memory>
 #include <numeric>
 
@@ -702,6 +703,7 @@ CopyArgs copy_args(const sc_pool *p, const sc_table *t, int mode) {
   a.v_half_off = (int64_t)(p->slice_bytes / 2);
   a.tier_base[0] = p->dev_base;
   a.tier_base[1] = p->host_dev;
+  a.tier_mask = 3;
   if (mode == COPY_FETCH) {
     a.items = t->d_items;
     a.n_items = t->n_fetch;
@@ -1194,6 +1196,62 @@ sc_status sc_fetch_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
   if (st != SC_OK) return st;
   DeviceGuard guard(pool->desc.device);
   return do_fetch(pool, table, layer, dst, (hipStream_t)stream);
+}
+
+sc_status sc_fetch_layer_kv_dma(sc_pool *pool, const sc_table *table, int32_t layer, const sc_active *dst,
+                                int32_t per_copy_calls, void *stream) {
+  clear_error();
+  if (!pool || !table) return fail(SC_ERR_INVALID, "null argument");
+  if (table->pool != pool) return fail(SC_ERR_INVALID, "table belongs to another pool");
+  if (layer < 0 || layer >= pool->desc.n_layers)
+    return fail(SC_ERR_RANGE, "layer %d outside [0, %d)", layer, pool->desc.n_layers);
+  sc_status st = check_active(table, dst);
+  if (st != SC_OK) return st;
+  DeviceGuard guard(pool->desc.device);
+  hipStream_t s = (hipStream_t)stream;
+  // Host-tier items: two copies each (the K and V halves of the block's
+  // layer slice are contiguous in the pool but go to different buffers).
+  std::vector<void *> dsts, srcs;
+  std::vector<size_t> sizes;
+  const int64_t layer_off = (int64_t)layer * (int64_t)pool->slice_bytes;
+  for (int32_t i = 0; i < table->n_fetch; ++i) {
+    const CopyItem &it = table->h_items[i];
+    if (it.tier != 1) continue;
+    char *src = pool->host_base + it.pool_off + layer_off;
+    const size_t bytes = (size_t)it.nrows * pool->row_bytes;
+    dsts.push_back(static_cast<char *>(dst->k) + it.act_row * (int64_t)pool->row_bytes);
+    srcs.push_back(src);
+    sizes.push_back(bytes);
+    dsts.push_back(static_cast<char *>(dst->v) + it.act_row * (int64_t)pool->row_bytes);
+    srcs.push_back(src + pool->slice_bytes / 2);
+    sizes.push_back(bytes);
+  }
+  if (!dsts.empty()) {
+    if (per_copy_calls) {
+      for (size_t i = 0; i < dsts.size(); ++i)
+        SC_HIP(hipMemcpyAsync(dsts[i], srcs[i], sizes[i], hipMemcpyHostToDevice, s));
+    } else {
+      // Looked up at run time: the HIP runtime a process loads (e.g. the
+      // one bundled with its framework) may predate the batch call.
+      using BatchFn = hipError_t (*)(void **, void **, size_t *, size_t, hipMemcpyAttributes *, size_t *, size_t,
+                                     size_t *, hipStream_t);
+      static BatchFn batch = reinterpret_cast<BatchFn>(dlsym(RTLD_DEFAULT, "hipMemcpyBatchAsync"));
+      if (batch == nullptr)
+        return fail(SC_ERR_UNSUPPORTED, "hipMemcpyBatchAsync is not in the loaded HIP runtime");
+      size_t fail_idx = 0;
+      SC_HIP(batch(dsts.data(), srcs.data(), sizes.data(), dsts.size(), nullptr, nullptr, 0, &fail_idx, s));
+    }
+  }
+  CopyArgs a = copy_args(pool, table, COPY_FETCH);
+  a.tier_mask = 1;   // device-tier items only
+  a.layer_off = layer_off;
+  a.act_k = static_cast<char *>(dst->k);
+  a.act_v = static_cast<char *>(dst->v);
+  if (table->n_fetch_host < table->n_fetch) {
+    hipError_t e = launch_kv_copy(a, s);
+    if (e != hipSuccess) return fail_hip(e, "fetch launch");
+  }
+  return SC_OK;
 }
 
 sc_status sc_append_new_kv(sc_pool *pool, const sc_table *table, const void *k_new, const void *v_new,

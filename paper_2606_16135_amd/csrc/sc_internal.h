@@ -56,6 +56,7 @@ struct CopyArgs {
   int64_t layer_off;      // layer * slice_bytes
   int64_t v_half_off;     // slice_bytes / 2: V half of a block slice
   char *tier_base[2];     // device-visible bases of the device and host tiers
+  int32_t tier_mask;      // FETCH / STORE: bit t set = copy the items of tier t
   char *act_k;
   char *act_v;
   const char *new_k;

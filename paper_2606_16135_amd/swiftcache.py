@@ -40,7 +40,8 @@ SC_STACK_TEST_NEVER_FREE = 32
 
 EXPORTED = [
     "sc_pool_create", "sc_pool_destroy", "sc_pool_layout_get", "sc_table_create",
-    "sc_table_destroy", "sc_table_totals", "sc_table_stack_status", "sc_fetch_layer_kv", "sc_append_new_kv",
+    "sc_table_destroy", "sc_table_totals", "sc_table_stack_status", "sc_fetch_layer_kv", "sc_fetch_layer_kv_dma",
+    "sc_append_new_kv",
     "sc_prefill_attn", "sc_prefill_attn_f16", "sc_prefill_attn_noalloc", "sc_attn_noalloc_splits",
     "sc_prefill_attn_varlen", "sc_store_layer_kv",
     "sc_prefill_stack", "sc_prefill_stack_chunked", "sc_attn_plan_query", "sc_pool_resize", "sc_plan_capacity", "sc_elastic_unit", "sc_scale_up",
@@ -111,6 +112,7 @@ def load():
         "sc_table_totals": (I32, [P, ctypes.POINTER(I64), ctypes.POINTER(I64)]),
         "sc_table_stack_status": (I32, [P, ctypes.POINTER(I32), I32]),
         "sc_fetch_layer_kv": (I32, [P, P, I32, ctypes.POINTER(sc_active), VP]),
+        "sc_fetch_layer_kv_dma": (I32, [P, P, I32, ctypes.POINTER(sc_active), I32, VP]),
         "sc_append_new_kv": (I32, [P, P, VP, VP, ctypes.POINTER(sc_active), VP]),
         "sc_prefill_attn": (I32, [VP, VP, VP, I32, I32, I32, I32, I32, F32, VP, VP, VP]),
         "sc_prefill_attn_f16": (I32, [VP, VP, VP, I32, I32, I32, I32, I32, F32, VP, VP, VP]),
@@ -210,6 +212,11 @@ def active(k_ptr, v_ptr, capacity_tokens):
 
 def sc_fetch_layer_kv(pool, table, layer, dst, stream=0):
     _check(load().sc_fetch_layer_kv(pool, table, layer, ctypes.byref(dst), stream or None))
+
+
+def sc_fetch_layer_kv_dma(pool, table, layer, dst, per_copy_calls=False, stream=0):
+    _check(load().sc_fetch_layer_kv_dma(pool, table, layer, ctypes.byref(dst), int(per_copy_calls),
+                                        stream or None))
 
 
 def sc_append_new_kv(pool, table, k_new, v_new, dst, stream=0):

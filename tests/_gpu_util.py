@@ -47,3 +47,39 @@ def compare_attention(gpu_bits, ref, what="", dtype="bf16"):
     assert not bad.any(), f"{what}: {stats}"
     assert rel_l2 <= REL_L2, f"{what}: {stats}"
     return stats
+
+
+def oracle_workers():
+    """Threads for the dense oracle at benchmark shapes: the host's cores in
+    this process's affinity, at most 16 (one GPU's share of a GPU machine)."""
+    import os
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def oracle_attention_by_head(q_bits, k_bits, v_bits, prefix_len, new_len, dtype="bf16", workers=None):
+    """The oracle's dense attention over a whole layer, every row and head,
+    computed one query head at a time in parallel threads (attention is
+    independent per head, so this is the same function; numpy releases the
+    GIL inside its kernels, and BLAS is held to one thread per worker so
+    the workers do not oversubscribe the cores).  Inputs are 16-bit
+    patterns [rows][heads][D]; returns o[sum N][H_q][D] in float64."""
+    import concurrent.futures
+    from threadpoolctl import threadpool_limits
+
+    from oracle import attention as oa
+    total_q, hq, d = q_bits.shape
+    group = hq // k_bits.shape[1]
+    out = np.zeros((total_q, hq, d), dtype=np.float64)
+
+    def one(h):
+        g = h // group
+        qh = oa.bits_to_f64(np.ascontiguousarray(q_bits[:, h:h + 1]), dtype)
+        kh = oa.bits_to_f64(np.ascontiguousarray(k_bits[:, g:g + 1]), dtype)
+        vh = oa.bits_to_f64(np.ascontiguousarray(v_bits[:, g:g + 1]), dtype)
+        o, _ = oa.attention(qh, kh, vh, prefix_len, new_len)
+        out[:, h] = o[:, 0]
+
+    with threadpool_limits(1):
+        with concurrent.futures.ThreadPoolExecutor(workers or oracle_workers()) as ex:
+            list(ex.map(one, range(hq)))
+    return out

@@ -265,3 +265,20 @@ def test_planted_gqa_index_mistake_is_caught(monkeypatch):
     o_wrong, _ = oa.attention(swapped, k, v, prefix, new)
     o_wrong = np.stack([o_wrong[:, 0], o_wrong[:, 2], o_wrong[:, 1], o_wrong[:, 3]], axis=1)
     assert not np.allclose(o_wrong, ob, atol=1e-6)
+
+
+def test_per_head_parallel_helper_equals_the_oracle():
+    """The GPU tests run the oracle one query head at a time in threads at
+    the benchmark shapes; that must be the same function as one call."""
+    from paper_2606_16135_amd import workloads as W
+    from _gpu_util import oracle_attention_by_head
+    wl = W.small_workload(7, [40, 0, 300], [9, 20, 33], 1, 20, 4, 64)
+    pool = W.pool_numpy(wl)
+    q, kn, vn = W.layer_inputs_numpy(wl, 0)
+    from oracle import kvcache as ok
+    ka, va = ok.gather_layer(pool, wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, 0)
+    kf, vf = ok.append_new(ka, va, kn, vn, wl.prefix_len, wl.new_len)
+    o_ref, _ = oa.attention(oa.bf16_bits_to_f64(q), oa.bf16_bits_to_f64(kf), oa.bf16_bits_to_f64(vf), wl.prefix_len,
+                         wl.new_len)
+    o = oracle_attention_by_head(q, kf, vf, wl.prefix_len, wl.new_len, "bf16", workers=4)
+    assert np.array_equal(o, o_ref)
