@@ -312,6 +312,46 @@ def run_workload(args, cfg, torch, sc, W, DevicePool, with_cpu, turn=None, rc_fr
     return entry
 
 
+def elastic_resize(torch, sc, W, reps=5):
+    """The elastic donor tier (§3.4): a library-owned HBM tier of workload
+    2's pool shape (L = 32, 2 MiB blocks) shrinks by a quarter and grows back;
+    both calls are timed on the host and the device's free memory is read
+    around them.  A layer-major cache would have to move every kept block of
+    every layer but the first for the same resize; that count is the
+    formula (L - 1) * kept * slice_bytes."""
+    wl = W.config(2)
+    cap = wl.n_device_blocks
+    keep = cap - cap // 4
+    pool = sc.sc_pool_create(wl.n_layers, wl.n_kv_heads, wl.head_dim, wl.block_size, cap)
+    try:
+        lay = sc.sc_pool_layout_get(pool)
+        t_shrink, t_grow, freed, taken = [], [], [], []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            f0 = torch.cuda.mem_get_info()[0]
+            t0 = time.perf_counter()
+            sc.sc_pool_resize(pool, keep)
+            t1 = time.perf_counter()
+            f1 = torch.cuda.mem_get_info()[0]
+            sc.sc_pool_resize(pool, cap)
+            t2 = time.perf_counter()
+            f2 = torch.cuda.mem_get_info()[0]
+            t_shrink.append(t1 - t0)
+            t_grow.append(t2 - t1)
+            freed.append(f1 - f0)
+            taken.append(f1 - f2)
+        return {"pool_blocks": cap, "released_blocks": cap - keep, "block_bytes": lay.block_bytes,
+                "chunk_blocks": lay.device_chunk_blocks,
+                "shrink_ms": round(1e3 * float(np.median(t_shrink)), 3),
+                "grow_ms": round(1e3 * float(np.median(t_grow)), 3),
+                "device_free_bytes_after_shrink": int(np.median(freed)),
+                "device_free_bytes_taken_by_grow": int(np.median(taken)),
+                "kept_blocks_moved": 0,
+                "layer_major_bytes_to_move": int((wl.n_layers - 1) * keep * lay.slice_bytes)}
+    finally:
+        sc.sc_pool_destroy(pool)
+
+
 def h2d_peak_gbs(torch, nbytes=1 << 30, reps=5):
     """Pinned host -> device hipMemcpyAsync (DMA) bandwidth of one large
     contiguous copy: the host link's roofline."""
@@ -463,8 +503,8 @@ def main():
             e = run_workload(args, cfg, torch, sc, W, DevicePool, with_cpu)
             entries[e["workload"]] = e
         head = e
-    # The elastic donor tier (§3.4), timed on workload 2's pool shape.
     details = {"configs": entries, "device": torch.cuda.get_device_name(0),
+               "elastic_resize": elastic_resize(torch, sc, W) if not single else None,
                "headline": f"{head['workload']} (the largest single-GPU workload)" if not single
                else head["workload"]}
     result = {"metric": METRIC, "value": head["value"], "unit": "tokens/s", "n_gpus": 1,

@@ -94,9 +94,13 @@ typedef struct sc_table sc_table;   /* opaque, library-owned */
  * memory of at least n_device_blocks * block_bytes (device memory on
  * `device`) and n_host_blocks * block_bytes (pinned host memory from
  * hipHostMalloc, mapped for device access) bytes, and never frees it.  When
- * NULL the library allocates the tier (hipMalloc / hipHostMalloc) and frees
- * it in sc_pool_destroy.  rc_base likewise for n_rc_blocks * block_bytes of
- * device memory.
+ * NULL the library allocates the tier and frees it in sc_pool_destroy: the
+ * host tier with hipHostMalloc; the HBM tier as one reserved virtual address
+ * range of the full capacity whose physical memory is mapped in chunks of
+ * whole blocks (hipMemCreate / hipMemMap, plain cached device memory), so
+ * that sc_pool_resize really appends and releases memory, or, where the
+ * runtime lacks virtual memory management, with one hipMalloc.  rc_base
+ * likewise for n_rc_blocks * block_bytes of device memory (hipMalloc).
  */
 typedef struct {
   int32_t n_layers;
@@ -125,6 +129,8 @@ typedef struct {
   void *rc_base;             /* regular-cache tier base (device address), or NULL */
   int64_t n_rc_blocks;
   int32_t dtype;             /* sc_dtype */
+  int64_t device_bytes_mapped;  /* physical bytes behind the HBM tier now (0: caller-owned) */
+  int64_t device_chunk_blocks;  /* blocks per physical chunk of an elastic tier (0: one allocation) */
 } sc_pool_layout;
 
 /* Active-layer buffer (the layer stream cache slot, §3.2): caller-owned
@@ -413,14 +419,22 @@ sc_status sc_attn_plan_query(int32_t batch, const int32_t *prefix_len, const int
  * Resize the pool's HBM tier in place (§3.4 "Block-Major Layout": the
  * elastic cache grows by appending blocks at the end and shrinks by
  * releasing the last ones; with all layers of a block contiguous, nothing
- * else moves, so the cost is O(1) whatever the layer count).  Afterwards ids
- * [0, n_device_blocks) are usable; ids of the host tier do not change (they
- * start at the HBM capacity given at creation).  Tables created later may
- * only use ids below the new count.
+ * else moves, so the cost does not depend on the layer count).  Afterwards
+ * ids [0, n_device_blocks) are usable; ids of the host tier do not change
+ * (they start at the HBM capacity given at creation).  Tables created later
+ * may only use ids below the new count.
+ * A library-owned HBM tier (device_base NULL at creation) changes its
+ * physical memory: shrinking unmaps and frees the chunks wholly past the new
+ * count (after waiting for the device to finish the work already queued,
+ * which may still read them), growing maps fresh chunks after the last one
+ * (their contents are undefined until stored).  Kept blocks keep their
+ * addresses and bytes.  Over caller-owned memory the call only moves the
+ * bound on usable ids.
  * Errors: SC_ERR_INVALID (null pool); SC_ERR_RANGE (n_device_blocks < 0 or
  * above the capacity the pool was created with); SC_ERR_INVALID when a live
  * table still references an HBM block at or above the new count (the
- * message names it).
+ * message names it); SC_ERR_OOM when growing cannot map memory (the tier
+ * is left as it was); SC_ERR_HIP when unmapping fails.
  */
 sc_status sc_pool_resize(sc_pool *pool, int64_t n_device_blocks);
 

@@ -801,6 +801,105 @@ sc_status prefill_attn_single(const void *q, const void *k_active, const void *v
                        scale, (hipStream_t)stream);
 }
 
+// ---------------------------------------------------------------------------
+// Elastic HBM tier (§3.4 "Block-Major Layout"): one reserved virtual range
+// for the tier's capacity, physical memory mapped chunk by chunk at its
+// start.  Growing maps chunks after the last one, shrinking unmaps the last
+// ones; the blocks that stay keep their addresses and contents.
+// ---------------------------------------------------------------------------
+hipMemAllocationProp vmm_prop(int device) {
+  hipMemAllocationProp prop{};
+  prop.type = hipMemAllocationTypePinned;   // plain (cached) device memory
+  prop.location.type = hipMemLocationTypeDevice;
+  prop.location.id = device;
+  return prop;
+}
+
+// Maps one more chunk after the mapped ones.
+hipError_t vmm_append_chunk(sc_pool *p) {
+  const hipMemAllocationProp prop = vmm_prop(p->desc.device);
+  char *at = p->dev_base + p->vmm_handles.size() * p->vmm_chunk_bytes;
+  if (at + p->vmm_chunk_bytes > p->dev_base + p->vmm_reserved) return hipErrorInvalidValue;
+  hipMemGenericAllocationHandle_t h{};
+  hipError_t e = hipMemCreate(&h, p->vmm_chunk_bytes, &prop, 0);
+  if (e != hipSuccess) return e;
+  e = hipMemMap(at, p->vmm_chunk_bytes, 0, h, 0);
+  if (e != hipSuccess) {
+    (void)hipMemRelease(h);
+    return e;
+  }
+  hipMemAccessDesc ad{};
+  ad.location = prop.location;
+  ad.flags = hipMemAccessFlagsProtReadWrite;
+  e = hipMemSetAccess(at, p->vmm_chunk_bytes, &ad, 1);
+  if (e != hipSuccess) {
+    (void)hipMemUnmap(at, p->vmm_chunk_bytes);
+    (void)hipMemRelease(h);
+    return e;
+  }
+  p->vmm_handles.push_back(h);
+  return hipSuccess;
+}
+
+// Unmaps and frees the last mapped chunk (no device work may still use it).
+hipError_t vmm_release_last_chunk(sc_pool *p) {
+  char *at = p->dev_base + (p->vmm_handles.size() - 1) * p->vmm_chunk_bytes;
+  hipError_t e = hipMemUnmap(at, p->vmm_chunk_bytes);
+  hipError_t e2 = hipMemRelease(p->vmm_handles.back());
+  p->vmm_handles.pop_back();
+  return e != hipSuccess ? e : e2;
+}
+
+// Reserves the tier's range and maps chunks for its first n blocks.  Returns
+// hipErrorNotSupported (nothing reserved) when the runtime has no virtual
+// memory management for the device.
+hipError_t vmm_create(sc_pool *p, int64_t n_blocks) {
+  const hipMemAllocationProp prop = vmm_prop(p->desc.device);
+  size_t gran = 0;
+  hipError_t e = hipMemGetAllocationGranularity(&gran, &prop, hipMemAllocationGranularityMinimum);
+  if (e != hipSuccess || gran == 0) return hipErrorNotSupported;
+  // Chunks hold whole blocks and are a multiple of the granularity: a
+  // multiple of lcm(block_bytes, gran), about kVmmChunkTarget bytes.  Each
+  // map or unmap call costs tens to hundreds of microseconds whatever its
+  // size (measured on MI355X with 2 MiB chunks: ~70 us to map, ~0.4 ms to
+  // unmap), so chunks much smaller than the usual resize step only add
+  // calls; 32 MiB is 16 blocks of the 8B shape, the paper's minimum elastic
+  // unit for a Qwen3-8B worker beside a Qwen3-32B master (Eq. 9).
+  constexpr size_t kVmmChunkTarget = (size_t)32 << 20;
+  const size_t g = std::gcd(p->block_bytes, gran);
+  const size_t unit = p->block_bytes / g * gran;
+  const size_t chunk = unit * std::max<size_t>(1, kVmmChunkTarget / unit);
+  const int64_t chunk_blocks = (int64_t)(chunk / p->block_bytes);
+  const int64_t cap_chunks = (p->desc.n_device_blocks + chunk_blocks - 1) / chunk_blocks;
+  void *base = nullptr;
+  e = hipMemAddressReserve(&base, (size_t)cap_chunks * chunk, gran, nullptr, 0);
+  if (e != hipSuccess) return e == hipErrorOutOfMemory ? e : hipErrorNotSupported;
+  p->dev_base = static_cast<char *>(base);
+  p->vmm = true;
+  p->vmm_reserved = (size_t)cap_chunks * chunk;
+  p->vmm_chunk_bytes = chunk;
+  p->vmm_chunk_blocks = chunk_blocks;
+  const int64_t need = (n_blocks + chunk_blocks - 1) / chunk_blocks;
+  while ((int64_t)p->vmm_handles.size() < need) {
+    e = vmm_append_chunk(p);
+    if (e != hipSuccess) break;
+  }
+  if (e != hipSuccess) {
+    while (!p->vmm_handles.empty()) (void)vmm_release_last_chunk(p);
+    (void)hipMemAddressFree(p->dev_base, p->vmm_reserved);
+    p->dev_base = nullptr;
+    p->vmm = false;
+  }
+  return e;
+}
+
+void vmm_destroy(sc_pool *p) {
+  while (!p->vmm_handles.empty()) (void)vmm_release_last_chunk(p);
+  if (p->dev_base) (void)hipMemAddressFree(p->dev_base, p->vmm_reserved);
+  p->dev_base = nullptr;
+  p->vmm = false;
+}
+
 }  // namespace
 }  // namespace sc
 
@@ -861,9 +960,16 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
     if (d.device_base) {
       p->dev_base = static_cast<char *>(d.device_base);
     } else {
-      hipError_t e = hipMalloc(reinterpret_cast<void **>(&p->dev_base), dev_bytes);
-      if (e != hipSuccess) return fail(SC_ERR_OOM, "hipMalloc(%zu) for the device tier: %s", dev_bytes,
-                                       hipGetErrorString(e));
+      // Elastic (chunk-mapped) when the runtime supports virtual memory
+      // management for the device, one allocation otherwise.
+      hipError_t e = vmm_create(p.get(), d.n_device_blocks);
+      if (e == hipErrorNotSupported) {
+        e = hipMalloc(reinterpret_cast<void **>(&p->dev_base), dev_bytes);
+        if (e != hipSuccess) return fail(SC_ERR_OOM, "hipMalloc(%zu) for the device tier: %s", dev_bytes,
+                                         hipGetErrorString(e));
+      } else if (e != hipSuccess) {
+        return fail(SC_ERR_OOM, "mapping %zu bytes for the device tier: %s", dev_bytes, hipGetErrorString(e));
+      }
       p->own_dev = true;
     }
   }
@@ -874,7 +980,8 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
       hipError_t e = hipHostMalloc(reinterpret_cast<void **>(&p->host_base), host_bytes,
                                    hipHostMallocMapped | hipHostMallocPortable);
       if (e != hipSuccess) {
-        if (p->own_dev) (void)hipFree(p->dev_base);
+        if (p->vmm) vmm_destroy(p.get());
+        else if (p->own_dev) (void)hipFree(p->dev_base);
         return fail(SC_ERR_OOM, "hipHostMalloc(%zu) for the host tier: %s", host_bytes, hipGetErrorString(e));
       }
       p->own_host = true;
@@ -882,7 +989,8 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
     void *devp = nullptr;
     hipError_t e = hipHostGetDevicePointer(&devp, p->host_base, 0);
     if (e != hipSuccess || devp == nullptr) {
-      if (p->own_dev) (void)hipFree(p->dev_base);
+      if (p->vmm) vmm_destroy(p.get());
+      else if (p->own_dev) (void)hipFree(p->dev_base);
       if (p->own_host) (void)hipHostFree(p->host_base);
       return fail(SC_ERR_INVALID, "host tier is not pinned, mapped memory: %s", hipGetErrorString(e));
     }
@@ -895,7 +1003,8 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
       const size_t rc_bytes = (size_t)d.n_rc_blocks * p->block_bytes;
       hipError_t e = hipMalloc(reinterpret_cast<void **>(&p->rc_base), rc_bytes);
       if (e != hipSuccess) {
-        if (p->own_dev) (void)hipFree(p->dev_base);
+        if (p->vmm) vmm_destroy(p.get());
+        else if (p->own_dev) (void)hipFree(p->dev_base);
         if (p->own_host) (void)hipHostFree(p->host_base);
         return fail(SC_ERR_OOM, "hipMalloc(%zu) for the regular cache: %s", rc_bytes, hipGetErrorString(e));
       }
@@ -910,7 +1019,8 @@ void sc_pool_destroy(sc_pool *pool) {
   if (!pool) return;
   if (pool->own_dev || pool->own_host || pool->own_rc) {
     DeviceGuard guard(pool->desc.device);
-    if (pool->own_dev && pool->dev_base) (void)hipFree(pool->dev_base);
+    if (pool->vmm) vmm_destroy(pool);
+    else if (pool->own_dev && pool->dev_base) (void)hipFree(pool->dev_base);
     if (pool->own_host && pool->host_base) (void)hipHostFree(pool->host_base);
     if (pool->own_rc && pool->rc_base) (void)hipFree(pool->rc_base);
   }
@@ -927,7 +1037,28 @@ sc_status sc_pool_resize(sc_pool *pool, int64_t n_device_blocks) {
   if (!pool->live_max_dev.empty() && *pool->live_max_dev.rbegin() >= n_device_blocks)
     return fail(SC_ERR_INVALID, "a live table still references HBM block %lld", (long long)*pool->live_max_dev.rbegin());
   // Block-major layout: the blocks that stay keep their addresses; the ones
-  // released (or appended) are the last ones.  No data moves.
+  // released (or appended) are the last ones.  No data moves.  A
+  // chunk-mapped tier also frees (or maps) the physical memory of the
+  // chunks past (up to) the new count.
+  if (pool->vmm) {
+    DeviceGuard guard(pool->desc.device);
+    const int64_t need = (n_device_blocks + pool->vmm_chunk_blocks - 1) / pool->vmm_chunk_blocks;
+    const int64_t had = (int64_t)pool->vmm_handles.size();
+    if (need < had) {
+      // Work already queued (e.g. by tables since destroyed) may still read
+      // the chunks about to go.
+      SC_HIP(hipDeviceSynchronize());
+      while ((int64_t)pool->vmm_handles.size() > need) SC_HIP(vmm_release_last_chunk(pool));
+    }
+    while ((int64_t)pool->vmm_handles.size() < need) {
+      hipError_t e = vmm_append_chunk(pool);
+      if (e != hipSuccess) {
+        while ((int64_t)pool->vmm_handles.size() > had) (void)vmm_release_last_chunk(pool);
+        return fail(SC_ERR_OOM, "mapping HBM blocks [%lld, %lld): %s",
+                    (long long)(had * pool->vmm_chunk_blocks), (long long)n_device_blocks, hipGetErrorString(e));
+      }
+    }
+  }
   pool->dev_lent = n_device_blocks;
   return SC_OK;
 }
@@ -947,6 +1078,9 @@ sc_status sc_pool_layout_get(const sc_pool *pool, sc_pool_layout *out) {
   out->dtype = pool->desc.dtype;
   std::lock_guard<std::mutex> lk(const_cast<sc_pool *>(pool)->mu);
   out->device_blocks_lent = pool->dev_lent;
+  out->device_bytes_mapped = pool->vmm ? (int64_t)(pool->vmm_handles.size() * pool->vmm_chunk_bytes)
+                                       : (pool->own_dev ? (int64_t)(pool->desc.n_device_blocks * pool->block_bytes) : 0);
+  out->device_chunk_blocks = pool->vmm ? pool->vmm_chunk_blocks : 0;
   return SC_OK;
 }
 

@@ -233,6 +233,17 @@ struct sc_pool {
   std::mutex mu;
   std::multiset<int64_t> live_max_dev;
   char *dev_base = nullptr;
+  // Library-owned HBM tier backed chunk by chunk: dev_base starts a reserved
+  // virtual range of vmm_reserved bytes; physical chunks of vmm_chunk_bytes
+  // (whole blocks, a multiple of the allocation granularity) are mapped at
+  // its start, vmm_handles[i] at dev_base + i * vmm_chunk_bytes.
+  // sc_pool_resize appends or releases chunks at the tail; the mapped ones
+  // never move.
+  bool vmm = false;
+  size_t vmm_reserved = 0;
+  size_t vmm_chunk_bytes = 0;
+  int64_t vmm_chunk_blocks = 0;
+  std::vector<hipMemGenericAllocationHandle_t> vmm_handles;
   char *host_base = nullptr;      // host address of the host tier
   char *host_dev = nullptr;       // device-visible address of the host tier
   bool own_dev = false;

@@ -70,7 +70,8 @@ class sc_pool_layout(ctypes.Structure):
                 ("row_bytes", ctypes.c_size_t), ("n_device_blocks", ctypes.c_int64),
                 ("n_host_blocks", ctypes.c_int64), ("device_blocks_lent", ctypes.c_int64),
                 ("rc_base", ctypes.c_void_p), ("n_rc_blocks", ctypes.c_int64),
-                ("dtype", ctypes.c_int32)]
+                ("dtype", ctypes.c_int32), ("device_bytes_mapped", ctypes.c_int64),
+                ("device_chunk_blocks", ctypes.c_int64)]
 
 
 class sc_model_shape(ctypes.Structure):

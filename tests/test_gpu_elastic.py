@@ -8,7 +8,7 @@ import pytest
 from oracle import kvcache as ok
 from paper_2606_16135_amd import workloads as W
 
-from _gpu_util import DevicePool, new_active, require_gpu, to_u16
+from _gpu_util import DevicePool, from_u16, new_active, require_gpu, to_u16
 
 pytestmark = pytest.mark.gpu
 
@@ -57,3 +57,98 @@ def test_resize_keeps_blocks_in_place_and_protects_live_tables():
         if dp.table is not None:
             sc.sc_table_destroy(dp.table)
         sc.sc_pool_destroy(dp.handle)
+
+
+def test_library_owned_tier_releases_and_maps_physical_memory():
+    """A library-owned HBM tier is one reserved range with physical chunks
+    mapped at its start: shrinking releases the memory of the chunks past
+    the new count (the device's free memory grows by that much), the kept
+    blocks keep their addresses and bytes, and growing maps fresh chunks that
+    store and fetch like any other block."""
+    sc = require_gpu()
+    import torch
+
+    L, hkv, d, bs, cap = 32, 8, 128, 16, 256          # 2 MiB blocks, 512 MiB tier
+    pool = sc.sc_pool_create(L, hkv, d, bs, cap)       # device_base NULL: library-owned
+    stream = torch.cuda.current_stream().cuda_stream
+    rng = np.random.default_rng(2606_16135_81)
+    tables = []
+
+    def table(ids, P, N):
+        t = sc.sc_table_create(pool, ids, [0, len(ids)], [P], [N], stream)
+        tables.append(t)
+        return t
+
+    def drop(t):
+        sc.sc_table_destroy(t)
+        tables.remove(t)
+
+    def store(ids, layers):
+        n = len(ids) * bs
+        t = table(ids, 0, n)
+        data = {}
+        for l in layers:
+            k = W.normal_bits(rng, (n, hkv, d))
+            v = W.normal_bits(rng, (n, hkv, d))
+            kd, vd = from_u16(k, "cuda"), from_u16(v, "cuda")
+            sc.sc_store_layer_kv(pool, t, l, kd.data_ptr(), vd.data_ptr(), stream)
+            torch.cuda.synchronize()
+            data[l] = (k, v)
+        drop(t)
+        return data
+
+    def fetch_equals(ids, data):
+        n = len(ids) * bs
+        t = table(ids, n, 0)
+        ok_all = True
+        for l, (k, v) in data.items():
+            kb = torch.full((n, hkv, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+            vb = torch.full_like(kb, float("nan"))
+            sc.sc_fetch_layer_kv(pool, t, l, sc.active(kb.data_ptr(), vb.data_ptr(), n), stream)
+            torch.cuda.synchronize()
+            ok_all &= np.array_equal(to_u16(kb), k) and np.array_equal(to_u16(vb), v)
+        drop(t)
+        return ok_all
+
+    try:
+        lay = sc.sc_pool_layout_get(pool)
+        chunk = lay.device_chunk_blocks
+        print(f"\n[elastic] chunk {chunk} blocks, mapped {lay.device_bytes_mapped >> 20} MiB", flush=True)
+        assert chunk >= 1, "library-owned HBM tier is not chunk-mapped"
+        assert lay.device_bytes_mapped >= cap * lay.block_bytes
+        base = lay.device_base
+        low = [int(x) for x in rng.permutation(cap // 2)[:40]]
+        high = [int(x) for x in cap // 2 + rng.permutation(cap // 2)[:8]]
+        data_low = store(low, [0, L - 1])
+        keep_high = table(high, len(high) * bs, 0)       # a live table on the upper half
+        with pytest.raises(sc.SwiftCacheError) as e:
+            sc.sc_pool_resize(pool, cap // 2)
+        assert e.value.status == sc.SC_ERR_INVALID
+        drop(keep_high)
+
+        torch.cuda.synchronize()
+        free0 = torch.cuda.mem_get_info()[0]
+        sc.sc_pool_resize(pool, cap // 2)
+        free1 = torch.cuda.mem_get_info()[0]
+        lay = sc.sc_pool_layout_get(pool)
+        released = (cap - cap // 2) * lay.block_bytes
+        print(f"[elastic] shrink to {cap // 2}: mapped {lay.device_bytes_mapped >> 20} MiB, "
+              f"device free memory +{(free1 - free0) >> 20} MiB", flush=True)
+        assert lay.device_base == base and lay.device_blocks_lent == cap // 2
+        assert lay.device_bytes_mapped <= (cap // 2 + chunk) * lay.block_bytes
+        assert free1 - free0 >= released - chunk * lay.block_bytes - (64 << 20)
+        assert fetch_equals(low, data_low), "kept blocks changed when the tier shrank"
+
+        sc.sc_pool_resize(pool, cap)
+        free2 = torch.cuda.mem_get_info()[0]
+        lay = sc.sc_pool_layout_get(pool)
+        print(f"[elastic] grow to {cap}: mapped {lay.device_bytes_mapped >> 20} MiB, "
+              f"device free memory -{(free1 - free2) >> 20} MiB", flush=True)
+        assert lay.device_base == base and lay.device_bytes_mapped >= cap * lay.block_bytes
+        data_high = store(high, [0, L // 2])
+        assert fetch_equals(high, data_high), "regrown blocks do not hold what was stored"
+        assert fetch_equals(low, data_low), "kept blocks changed when the tier grew"
+    finally:
+        for t in list(tables):
+            sc.sc_table_destroy(t)
+        sc.sc_pool_destroy(pool)
