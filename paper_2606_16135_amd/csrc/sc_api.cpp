@@ -177,6 +177,46 @@ int attn_slots(int device) {
   return slots;
 }
 
+struct GroupItems {
+  int64_t cost = 0;
+  std::vector<WorkItem> items;
+};
+
+// Places the items of each (sequence, KV head) group on one XCD (workgroup
+// w runs on XCD w mod 8), groups by decreasing cost onto the least loaded
+// XCD, longest items first within an XCD.
+void place_items(std::vector<GroupItems> &groups, AttnPlan *plan) {
+  std::stable_sort(groups.begin(), groups.end(),
+                   [](const GroupItems &x, const GroupItems &y) { return x.cost > y.cost; });
+  std::vector<int64_t> load(kXcds, 0);
+  std::vector<std::vector<WorkItem>> per_xcd(kXcds);
+  for (auto &gi : groups) {
+    const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+    load[x] += gi.cost;
+    per_xcd[x].insert(per_xcd[x].end(), gi.items.begin(), gi.items.end());
+  }
+  size_t max_len = 0;
+  int n_real = 0;
+  for (auto &v : per_xcd) {
+    // Longest items first; equal costs keep split-major order so that the
+    // workgroups resident together read the same key range.
+    std::stable_sort(v.begin(), v.end(), [](const WorkItem &x, const WorkItem &y) {
+      const int cx = x.k_end - x.k_begin, cy = y.k_end - y.k_begin;
+      if (cx != cy) return cx > cy;
+      if (x.seq != y.seq) return x.seq < y.seq;
+      if (x.split != y.split) return x.split < y.split;
+      return x.q0 < y.q0;
+    });
+    max_len = std::max(max_len, v.size());
+    n_real += (int)v.size();
+  }
+  plan->items.assign(max_len * kXcds, WorkItem{-1, 0, 0, 0, 0, 0, 0, 0});
+  for (int x = 0; x < kXcds; ++x)
+    for (size_t j = 0; j < per_xcd[x].size(); ++j) plan->items[j * kXcds + x] = per_xcd[x][j];
+  plan->n_items = (int)plan->items.size();
+  plan->n_real_items = n_real;
+}
+
 void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N, int n_q_heads,
                     int n_kv_heads, int slots, AttnPlan *plan, const std::vector<int32_t> &rc_keys,
                     const std::vector<int32_t> &rc_off, const std::vector<int32_t> &cu_k,
@@ -286,10 +326,6 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
 
   // Items, grouped by (sequence, KV head) so that one group's K/V stays in
   // one XCD's L2.
-  struct GroupItems {
-    int64_t cost = 0;
-    std::vector<WorkItem> items;
-  };
   std::vector<GroupItems> groups;
   size_t ti = 0;
   for (int b = 0; b < batch; ++b) {
@@ -316,35 +352,7 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
       if (!gi.items.empty()) groups.push_back(std::move(gi));
     }
   }
-  std::stable_sort(groups.begin(), groups.end(),
-                   [](const GroupItems &x, const GroupItems &y) { return x.cost > y.cost; });
-  std::vector<int64_t> load(kXcds, 0);
-  std::vector<std::vector<WorkItem>> per_xcd(kXcds);
-  for (auto &gi : groups) {
-    const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-    load[x] += gi.cost;
-    per_xcd[x].insert(per_xcd[x].end(), gi.items.begin(), gi.items.end());
-  }
-  size_t max_len = 0;
-  int n_real = 0;
-  for (auto &v : per_xcd) {
-    // Longest items first; equal costs keep split-major order so that the
-    // workgroups resident together read the same key range.
-    std::stable_sort(v.begin(), v.end(), [](const WorkItem &x, const WorkItem &y) {
-      const int cx = x.k_end - x.k_begin, cy = y.k_end - y.k_begin;
-      if (cx != cy) return cx > cy;
-      if (x.seq != y.seq) return x.seq < y.seq;
-      if (x.split != y.split) return x.split < y.split;
-      return x.q0 < y.q0;
-    });
-    max_len = std::max(max_len, v.size());
-    n_real += (int)v.size();
-  }
-  plan->items.assign(max_len * kXcds, WorkItem{-1, 0, 0, 0, 0, 0, 0, 0});
-  for (int x = 0; x < kXcds; ++x)
-    for (size_t j = 0; j < per_xcd[x].size(); ++j) plan->items[j * kXcds + x] = per_xcd[x][j];
-  plan->n_items = (int)plan->items.size();
-  plan->n_real_items = n_real;
+  place_items(groups, plan);
 }
 
 namespace {
@@ -418,10 +426,10 @@ void free_plan(AttnPlan *plan) {
 // an eviction (which drains the device first) never frees a plan that
 // another thread is about to launch with.
 std::mutex g_plan_mu;
-std::map<std::tuple<int, int, int, int, int>, std::unique_ptr<AttnPlan>> g_single_plans;
+std::map<std::tuple<int, int, int, int, int, int>, std::unique_ptr<AttnPlan>> g_single_plans;
 
-sc_status single_plan(int device, int P, int N, int hq, int hkv, AttnPlan **out) {
-  auto key = std::make_tuple(device, P, N, hq, hkv);
+sc_status single_plan(int device, int P, int N, int hq, int hkv, int head_dim, AttnPlan **out) {
+  auto key = std::make_tuple(device, P, N, hq, hkv, head_dim);
   auto it = g_single_plans.find(key);
   if (it != g_single_plans.end()) {
     *out = it->second.get();
@@ -795,7 +803,7 @@ sc_status prefill_attn_single(const void *q, const void *k_active, const void *v
   SC_HIP(hipGetDevice(&device));
   AttnPlan *plan = nullptr;
   std::lock_guard<std::mutex> lk(g_plan_mu);
-  st = single_plan(device, prefix_len, new_len, n_q_heads, n_kv_heads, &plan);
+  st = single_plan(device, prefix_len, new_len, n_q_heads, n_kv_heads, head_dim, &plan);
   if (st != SC_OK) return st;
   return run_attention(device, *plan, q, k_active, v_active, out, lse, n_q_heads, n_kv_heads, head_dim, dtype,
                        scale, (hipStream_t)stream);

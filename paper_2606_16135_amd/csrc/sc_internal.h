@@ -218,6 +218,7 @@ void plan_attention(const std::vector<int32_t> &P, const std::vector<int32_t> &N
                     const std::vector<int32_t> &q_off = {});
 int attn_slots(int device);
 
+
 }  // namespace sc
 
 // ---------------------------------------------------------------------------
