@@ -16,7 +16,7 @@ Contents
 ``attention`` exact causal GQA prefill attention over prefix + new tokens in
               float64, a row-sampled variant for large shapes, and the
               log-sum-exp merge of attention over disjoint key sets
-              (paper §2.1-§2.2: every token attends to all tokens before it;
+              (paper §2.1-§2.2: causal attention over every earlier position and itself;
               §5 "Model": GQA).
 ``capacity``  the master's layer stream cache and regular cache sizes and
               the longest supported context (§3.2, Eq. 1-5).

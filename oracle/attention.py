@@ -4,10 +4,11 @@ TEST INFRASTRUCTURE ONLY (see the package docstring).
 
 What it follows
 ---------------
-* §2.2 "Transformer architecture": each token attends to all tokens that
-  precede it; §2.2 "Multi-turn conversations": in a new turn only the new
-  tokens are computed, and their attention combines the cached KV of the
-  history with the KV of the new tokens.  New token ``i`` of a sequence with
+* §2.2 "Transformer architecture": causal attention, i.e. a token's output
+  depends on its own key/value and on those of earlier positions only;
+  §2.2 "Multi-turn conversations": in a new turn only the new tokens are
+  computed, their attention combining the history's cached KV with the new
+  tokens' KV.  New token ``i`` of a sequence with
   ``P`` cached prefix tokens therefore sees keys ``0 .. P + i`` (all of the
   prefix, the new tokens before it, and itself).
 * §5 "Model": the models use GQA; query head ``h`` reads KV head

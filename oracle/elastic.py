@@ -60,23 +60,26 @@ def _ceil_div(a, b):
 
 
 def scale_up(n_i, block_size_i, meu_i, meu_m, request_len):
-    """Algorithm 1, ScaleUp: (worker blocks to add, master blocks to give)."""
-    need = _ceil_div(request_len, block_size_i)
-    if need <= n_i:
-        return 0, 0
-    k = _ceil_div(need - n_i, meu_i)
-    return k * meu_i, k * meu_m
+    """Algorithm 1's scale-up decision, from what it guarantees: after it the
+    worker holds enough blocks for the request, it changes by whole elastic
+    units only (MEU_i of its blocks, traded for MEU_m of the master's), and
+    no smaller number of units would do.  Returns (worker blocks to add,
+    master blocks to give)."""
+    shortfall = max(0, _ceil_div(request_len, block_size_i) - n_i)
+    units = _ceil_div(shortfall, meu_i)          # least u with u * MEU_i >= shortfall
+    return units * meu_i, units * meu_m
 
 
 def scale_down(n_i, block_size_i, meu_i, meu_m, window_lengths):
-    """Algorithm 1, ScaleDown: (worker blocks to release, master blocks to
-    gain) given the request lengths seen in the last t seconds."""
-    max_len = max(window_lengths) if len(window_lengths) else 0
-    max_need = _ceil_div(max_len, block_size_i)
-    if max_need >= n_i:
-        return 0, 0
-    k = (n_i - max_need) // meu_i
-    return k * meu_i, k * meu_m
+    """Algorithm 1's scale-down decision, from what it guarantees: the worker
+    keeps enough blocks for the longest request seen in the last t seconds
+    (none if there was none), gives back whole elastic units only, and as
+    many of them as fit in its surplus.  Returns (worker blocks to release,
+    master blocks to gain)."""
+    longest = max(window_lengths) if len(window_lengths) else 0
+    surplus = max(0, n_i - _ceil_div(longest, block_size_i))
+    units = surplus // meu_i                     # most u with u * MEU_i <= surplus
+    return units * meu_i, units * meu_m
 
 
 def layer_major_offset(layer, block, n_layers, n_blocks, block_elems_):

@@ -1,5 +1,5 @@
-// Causal GQA prefill attention over prefix + new tokens (§2.2: every token
-// attends to all tokens before it, and a new turn's tokens attend to the
+// Causal GQA prefill attention over prefix + new tokens (§2.2: causal
+// attention over every earlier position and the token itself; a new turn's tokens attend to the
 // cached history plus the new tokens; GQA as used by the models of §5).
 //
 // Output row (query i of a sequence with P cached tokens, query head h):
