@@ -49,15 +49,20 @@
 // the exponent range, which the limit bounds.  No per-tile row max is
 // computed on the common path.
 //
-// K and V tiles each live in a 4-entry LDS ring (slot = tile mod 4).
-// Iteration j reads K(j+1) and V(j-1), writes K(j+3) and V(j+1) from
-// registers loaded in iteration j-1 and loads K(j+4) and V(j+2).  Because a
-// tile is written two iterations before it is read, only every second
-// iteration ends with a workgroup barrier (one that orders LDS only; global
-// loads stay in flight across it), which halves the barrier waits and lets
-// the waves drift apart by up to an iteration.  The loop is unrolled by two
-// so that the barrier placement and the score registers are fixed at
-// compile time.
+// K and V tiles each live in a 4-entry LDS ring (slot = tile mod 4), and
+// iteration j reads K(j+1) and V(j-1).  With head_dim 128 the tiles go from
+// memory straight into LDS (buffer loads with the LDS flag, swizzled rows
+// instead of padded ones, 64 KiB of LDS): the even iteration of each pair
+// issues the loads of K(j+3), K(j+4), V(j+1) and V(j+2), and the pair ends
+// with one barrier after they have landed.  With head_dim 64 the tiles are
+// staged through registers: iteration j writes K(j+3) and V(j+1) loaded in
+// iteration j-1 and loads K(j+4) and V(j+2).  Either way a tile is in place
+// at least a barrier before it is read and only every second iteration ends
+// with a workgroup barrier (one that lets global loads meant for later
+// iterations stay in flight), which halves the barrier waits and lets the
+// waves drift apart by up to an iteration.  The loop is unrolled so that
+// the ring slots, the barrier placement and the score registers are fixed
+// at compile time.
 #include "sc_internal.h"
 
 #include <cmath>
@@ -181,6 +186,55 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// head_dim 128: K/V ring slots loaded straight into LDS (see attn_item).
+// One array per slot and operand, so the compiler can tell that a load in
+// flight into one slot does not alias reads of another and needs no wait.
+struct DmaGeo {
+  static constexpr int kRowBytes = 128 * 2;               // one key row of one KV head
+  static constexpr int kSlotBytes = KT * kRowBytes;        // one tile, 8 KiB
+};
+__shared__ __attribute__((aligned(1024))) unsigned char dma_k0[DmaGeo::kSlotBytes];
+__shared__ __attribute__((aligned(1024))) unsigned char dma_k1[DmaGeo::kSlotBytes];
+__shared__ __attribute__((aligned(1024))) unsigned char dma_k2[DmaGeo::kSlotBytes];
+__shared__ __attribute__((aligned(1024))) unsigned char dma_k3[DmaGeo::kSlotBytes];
+__shared__ __attribute__((aligned(1024))) unsigned char dma_v0[DmaGeo::kSlotBytes];
+__shared__ __attribute__((aligned(1024))) unsigned char dma_v1[DmaGeo::kSlotBytes];
+__shared__ __attribute__((aligned(1024))) unsigned char dma_v2[DmaGeo::kSlotBytes];
+__shared__ __attribute__((aligned(1024))) unsigned char dma_v3[DmaGeo::kSlotBytes];
+template <int S>
+__device__ __forceinline__ unsigned char *dma_k_slot() {
+  static_assert(S >= 0 && S < 4, "ring slot");
+  return S == 0 ? dma_k0 : S == 1 ? dma_k1 : S == 2 ? dma_k2 : dma_k3;
+}
+template <int S>
+__device__ __forceinline__ unsigned char *dma_v_slot() {
+  static_assert(S >= 0 && S < 4, "ring slot");
+  return S == 0 ? dma_v0 : S == 1 ? dma_v1 : S == 2 ? dma_v2 : dma_v3;
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Wait until at most VM vector-memory operations of this wave (loads into
+// LDS included) are in flight and its LDS and scalar loads are done, then a
+// workgroup barrier.  No memory-model fence: the fence of __syncthreads
+// would wait for every load into LDS, including those meant to stay in
+// flight.
+template <int VM>
+__device__ __forceinline__ void dma_barrier() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4) | (0 << 8));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Wait for every vector-memory operation of this wave.
+__device__ __forceinline__ void dma_wait_all() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8));
+  asm volatile("" ::: "memory");
 }
 
 // S^T(tile) = K_tile . Q^T: D / 16 dependent MFMAs.
@@ -351,84 +405,6 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
         __builtin_amdgcn_readfirstlane((int)(range_bytes > off ? range_bytes - off : 0u)), 0x00020000);
   };
 
-  // Staging: chunk c = tid + 512 i of a (K tile, V tile) pair; whether it is
-  // a K or a V chunk is uniform over a wave.
-  int voff[NCH], lds_off[NCH], crow[NCH], ccol[NCH];
-  bool is_v[NCH];
-#pragma unroll
-  for (int i = 0; i < NCH; ++i) {
-    is_v[i] = wave * 64 + kThreads * i >= G_::kTileChunks;
-    const int c = tid + kThreads * i - (is_v[i] ? G_::kTileChunks : 0);
-    const int r = c / G_::kChunksPerRow, cc = c % G_::kChunksPerRow;
-    voff[i] = (int)((r * kv_stride + cc * 8) * 2);
-    lds_off[i] = is_v[i] ? G_::kSlots * G_::kTileK + r * G_::kLdsV + cc * 8 : r * G_::kLdsK + cc * 8;
-    crow[i] = r;
-    ccol[i] = wi.kvh * D + cc * 8;
-  }
-  // Regular-cache item: key k of the sequence is row k mod B of local block
-  // rc_ids[rc_off + k / B], read in place.  A wave's chunk i covers 4 (D=128)
-  // or 8 (D=64) consecutive rows of a tile that start on a multiple of that
-  // count, and B >= 16 is a power of two, so those rows share one block: its
-  // index is wave-uniform and the load goes through a buffer resource over
-  // that block's layer slice.  The index of tile t + 1 is read while tile t
-  // is loaded (tiles of one chunk are loaded in order, one per call), so the
-  // data loads never wait on it.  Rows past the range read the clamped last
-  // block; they are masked.
-  const int32_t *rc_ids = kPaged ? a.rc_ids + sd.rc_off : nullptr;
-  const uint16_t *rc_layer = kPaged ? a.rc_base + a.rc_layer_elems : nullptr;
-  const int rc_mask = (1 << a.block_shift) - 1;
-  const uint32_t rc_slice_bytes = (uint32_t)(a.rc_half_elems * 4);
-  int rc_next[NCH];
-#pragma unroll
-  for (int i = 0; i < NCH; ++i) rc_next[i] = 0;
-  // The index table is read through the constant address space: the host
-  // writes it before the launch and nothing writes it during the kernel, so
-  // the uniform index loads are scalar loads.
-  const __attribute__((address_space(4))) int32_t *rc_ids_c =
-      (const __attribute__((address_space(4))) int32_t *)rc_ids;
-  auto rc_block = [&](int t, int i) {
-    const int row0 = __builtin_amdgcn_readfirstlane(crow[i]);
-    return rc_ids_c[min(k_begin + t * KT + row0, k_end - 1) >> a.block_shift];
-  };
-  // A negative tile index (prologue only) skips that half of the pair.
-  u32x4 lr[NCH];
-  auto stage_load = [&](u32x4 (&lr)[NCH], int kj, int vj) {
-#pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int t = is_v[i] ? vj : kj;
-      if (t < 0) continue;
-      if (kPaged) {
-        const int blk = __builtin_amdgcn_readfirstlane(t == 0 ? rc_block(0, i) : rc_next[i]);
-        rc_next[i] = rc_block(t + 1, i);
-        const uint16_t *base = rc_layer + (int64_t)blk * a.rc_block_elems;
-        const int row = (k_begin + t * KT + crow[i]) & rc_mask;
-        const int off = (int)((row * kv_stride + ccol[i] + (is_v[i] ? a.rc_half_elems : 0)) * 2);
-        lr[i] = __builtin_bit_cast(
-            u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(base), (short)0,
-                                                         (int)rc_slice_bytes, 0x00020000),
-                       off, 0, 0));
-      } else {
-        lr[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc(is_v[i] ? vb : kb, t),
-                                                                                 voff[i], 0, 0));
-      }
-    }
-  };
-  // kt / vt: the tiles the K and V chunks hold (ring slot = tile mod 4); a
-  // negative tile skips that half.
-  auto stage_store = [&](const u32x4 (&lr)[NCH], int kt, int vt) {
-#pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int t = is_v[i] ? vt : kt;
-      if (t >= 0) {
-        const int slot_off = is_v[i] ? (t & 3) * G_::kTileV : (t & 3) * G_::kTileK;
-        *reinterpret_cast<u32x4 *>(smem + lds_off[i] + slot_off) = lr[i];
-      }
-    }
-  };
-  auto slot_k = [&](int t) { return smem + (t & 3) * G_::kTileK; };
-  auto slot_v = [&](int t) { return smem + G_::kSlots * G_::kTileK + (t & 3) * G_::kTileV; };
-
   // First tile that needs the mask, the same for the whole workgroup: it
   // reaches past the key range or past the diagonal of the first query.
   const int diag0 = sd.prefix + wi.q0;
@@ -463,80 +439,363 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
     timed_out = s_timeout != 0;
   }
 
-  if (n > 0 && !timed_out) {
-    // Prologue: K(0), K(1), K(2) and V(0) into the rings (their loads in
-    // flight together), K(3) and V(1) loaded for iteration 0, then QK(0).
+  if constexpr (D == 128) {
+    // K and V tiles go from memory straight into LDS (buffer loads with the
+    // LDS flag; no staging registers).  Wave w loads rows 4 w .. 4 w + 3 of
+    // every K and V tile: one 16-byte load per lane and operand, lane i
+    // filling bytes 16 i .. 16 i + 15 of the wave's four rows.  Rows are
+    // unpadded (256 bytes); chunk c of K row r sits at position c ^ (r mod 16)
+    // and of V row r at c ^ 4 (r mod 4), which keeps the K fragment reads and
+    // the V transpose reads free of bank conflicts.  Each lane loads the
+    // chunk that belongs at its position.
+    const int row_bytes = (int)(kv_stride * 2);
+    const int l4 = lane >> 4;
+    const int p16 = lane & 15;
+    const int my_row = 4 * wave;
+    const int voff_k = l4 * row_bytes + ((p16 ^ (4 * (wave & 3) + l4)) << 4);
+    const int voff_v = l4 * row_bytes + ((p16 ^ (l4 << 2)) << 4);
+    // This lane's LDS read offsets within a slot: K fragment k (row col,
+    // chunk 2 k + half) and the transpose read of dim block c (key row
+    // tr_row; the other key rows of the product are immediates).
+    int k_rd[D / 16], v_rd[D / 32];
+#pragma unroll
+    for (int k = 0; k < D / 16; ++k) k_rd[k] = col * DmaGeo::kRowBytes + (((2 * k + half) ^ (col & 15)) << 4);
     {
-      u32x4 lb[NCH], lc[NCH];
-      stage_load(lr, 0, 0);
-      stage_load(lb, 1, -1);
-      stage_load(lc, 2, -1);
-      stage_store(lr, 0, 0);
-      stage_store(lb, 1, -1);
-      stage_store(lc, 2, -1);
-      stage_load(lr, 3, 1);
+      const int tr_row = 4 * half + ((lane & 15) >> 2);
+      const int lo = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+      const int x = (lane >> 2) & 3;
+#pragma unroll
+      for (int c = 0; c < D / 32; ++c) v_rd[c] = tr_row * DmaGeo::kRowBytes + ((4 * (c ^ x) + lo) << 4) + 8 * (lane & 1);
     }
-    lds_barrier();
-    qk_tile<D, DT>(slot_k(0), w.qf, w.s[0], lane);
+    // Regular-cache item: key k of the sequence is row k mod B of local
+    // block rc_ids[rc_off + k / B], read in place.  A wave's four rows start
+    // on a multiple of 4 and B >= 16 is a power of two, so they share one
+    // block; its index is a scalar load (the table is read through the
+    // constant address space: the host writes it before the launch), made a
+    // pair of iterations before the tile's data load.
+    const __attribute__((address_space(4))) int32_t *rc_ids_c =
+        kPaged ? (const __attribute__((address_space(4))) int32_t *)(a.rc_ids + sd.rc_off) : nullptr;
+    const uint16_t *rc_layer = kPaged ? a.rc_base + a.rc_layer_elems : nullptr;
+    const int rc_mask = (1 << a.block_shift) - 1;
+    auto blk_of = [&](int t) -> int {
+      if constexpr (!kPaged) {
+        return 0;
+      } else {
+        return rc_ids_c[min(k_begin + t * KT + my_row, k_end - 1) >> a.block_shift];
+      }
+    };
+    // This wave's four rows of tile t, K (kV false) or V, into `slot`.  The
+    // buffer resource ends after the last row of the item's range (of the
+    // block, for a regular-cache item), so rows past it, and whole tiles
+    // past the last one, load zeros without touching memory.
+    auto dma = [&](unsigned char *slot, int t, auto v_tag, int blk) {
+      constexpr bool kV = decltype(v_tag)::value;
+      const int key = k_begin + t * KT + my_row;
+      const char *base;
+      int range;
+      if constexpr (kPaged) {
+        const int rib = min(key, k_end - 1) & rc_mask;   // first row within the block
+        const int rows = min(rc_mask + 1 - rib, k_end - key);
+        base = reinterpret_cast<const char *>(rc_layer + (int64_t)blk * a.rc_block_elems +
+                                              (kV ? a.rc_half_elems : 0) + (int64_t)rib * kv_stride +
+                                              (int64_t)wi.kvh * D);
+        range = rows > 0 ? ((rows - 1) * row_bytes + 2 * D) : 0;
+      } else {
+        const uint32_t off = (uint32_t)t * tile_bytes + (uint32_t)(my_row * row_bytes);
+        base = reinterpret_cast<const char *>(kV ? vb : kb) + off;
+        range = (int)(range_bytes > off ? range_bytes - off : 0u);
+      }
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<char *>(base), (short)0, __builtin_amdgcn_readfirstlane(range), 0x00020000);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)(slot + my_row * DmaGeo::kRowBytes), 16,
+                                               kV ? voff_v : voff_k, 0, 0, 0);
+    };
+    auto qk = [&](const unsigned char *slot, f32x16 &s) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = 0.f;
+#pragma unroll
+      for (int k = 0; k < D / 16; ++k)
+        s = Elem<DT>::mfma(*reinterpret_cast<const u32x4 *>(slot + k_rd[k]), w.qf[k], s);
+    };
+    // O^T += V^T . P^T, operands as in pv_tile.
+    auto pv = [&](const unsigned char *slot) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int c = 0; c < D / 32; ++c) {
+          const unsigned char *p = slot + v_rd[c] + 16 * t * DmaGeo::kRowBytes;
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)p);
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p + 8 * DmaGeo::kRowBytes));
+          u32x4 vw;
+          vw[0] = __builtin_bit_cast(u32x2, lo)[0];
+          vw[1] = __builtin_bit_cast(u32x2, lo)[1];
+          vw[2] = __builtin_bit_cast(u32x2, hi)[0];
+          vw[3] = __builtin_bit_cast(u32x2, hi)[1];
+          w.oacc[c] = Elem<DT>::mfma(vw, w.pf_prev[t], w.oacc[c]);
+        }
+    };
 
-    // Iteration j (tile parity PAR): QK(j+1) and PV(j-1) on the MFMA pipe,
-    // softmax(j) on the VALU, then K(j+3), V(j+1) into the rings and K(j+4),
-    // V(j+2) from memory.  Tile j's scores live in s[PAR].  The rings hold
-    // four tiles, so a workgroup barrier is needed only after even
-    // iterations: the two iterations between barriers read K(j+1), V(j-1)
-    // written at least one barrier earlier and write the two slots read
-    // last before that barrier.
-    auto iterate = [&](auto par_tag, auto mask_tag, auto qk_tag, auto pv_tag, auto first_tag, int j) {
-      constexpr int PAR = decltype(par_tag)::value;
-      constexpr bool kMask = decltype(mask_tag)::value;
-      constexpr bool kQk = decltype(qk_tag)::value;
-      constexpr bool kPv = decltype(pv_tag)::value;
-      constexpr bool kFirst = decltype(first_tag)::value;
-      __builtin_assume(j >= 0);
-      f32x16 &sc = w.s[PAR];
-      u32x4 pf[2];
-      if (kQk) qk_tile<D, DT>(slot_k(j + 1), w.qf, w.s[PAR ^ 1], lane);
-      if (kPv) pv_tile<D, DT>(slot_v(j - 1), w.pf_prev, w.oacc, lane);
-      if (kMask) apply_mask(sc, lim_of(j));
-      if (kFirst) {
-        const float tm = tile_max(sc, sl2);
-        w.m_run = tm > -INFINITY ? tm : 0.f;
+    if (n > 0 && !timed_out) {
+      using T = std::true_type;
+      using F = std::false_type;
+      // Regular-cache block indices of the tiles the current pair loads into
+      // K (bk0, bk1) and V (bv0, bv1), and of the next pair's K tiles.
+      int bv0 = 0, bv1 = 0, bk0 = 0, bk1 = 0, bn0 = 0, bn1 = 0;
+      // Prologue: K(0), K(1), K(2) and V(0), then QK(0).  Iteration 0 loads
+      // K(4) into the slot QK(0) reads: a second barrier.
+      {
+        const int b0 = blk_of(0), b1 = blk_of(1), b2 = blk_of(2);
+        dma(dma_k_slot<0>(), 0, F(), b0);
+        dma(dma_v_slot<0>(), 0, T(), b0);
+        dma(dma_k_slot<1>(), 1, F(), b1);
+        dma(dma_k_slot<2>(), 2, F(), b2);
+        bv0 = b1;
+        bv1 = b2;
+        bk0 = blk_of(3);
+        bk1 = blk_of(4);
       }
-      float rs = softmax_tile<DT>(sc, pf, sl2, w.m_run);
-      if (!kFirst && __builtin_amdgcn_ballot_w64(!(rs <= Elem<DT>::kSumLimit))) rs = settle_max<D, DT>(w, sc, pf, sl2);
-      w.l_run += rs;
-      stage_store(lr, j + 3, j + 1);
-      stage_load(lr, j + 4, j + 2);
-      if (PAR == 0) lds_barrier();
-      w.pf_prev[0] = pf[0];
-      w.pf_prev[1] = pf[1];
-    };
-    using T = std::true_type;
-    using F = std::false_type;
-    using P0 = std::integral_constant<int, 0>;
-    using P1 = std::integral_constant<int, 1>;
-    // j = 0: masked variant (exact for any tile), exact max.
-    if (n > 1) iterate(P0(), T(), T(), F(), T(), 0); else iterate(P0(), T(), F(), F(), T(), 0);
-    // Steady state j = 1 .. n - 2, unrolled by two so that tile parity is
-    // known at compile time: unmasked tiles, then masked ones.
-    int j = 1;
-    auto steady = [&](auto mask_tag, int j_end) {
-      if (j < j_end && (j & 1) == 0) iterate(P0(), mask_tag, T(), T(), F(), j++);
-      for (; j + 1 < j_end; j += 2) {
-        iterate(P1(), mask_tag, T(), T(), F(), j);
-        iterate(P0(), mask_tag, T(), T(), F(), j + 1);
+      dma_barrier<0>();
+      qk(dma_k_slot<0>(), w.s[0]);
+      dma_barrier<0>();
+
+      // Iteration j (J = j mod 4 is the ring slot of tile j; tile j's scores
+      // live in s[j mod 2]).  An even iteration starts a pair of iterations:
+      // it loads K(j+3), K(j+4), V(j+1) and V(j+2) into the slots last read
+      // in the previous pair; the odd one ends the pair with a barrier after
+      // all of them have landed, so every load has two iterations to land
+      // and only every second iteration waits at a barrier.  Loads of tiles
+      // past the last one load zeros.  QK(j+1) runs in every iteration, also
+      // the last, whose product of a stale slot is never used: one body
+      // throughout keeps the MFMA accumulators in place and the MFMAs in the
+      // same basic block as the softmax they interleave with.
+      auto iterate = [&](auto j_tag, auto mask_tag, auto first_tag, int j) {
+        constexpr int J = decltype(j_tag)::value;
+        constexpr bool kMask = decltype(mask_tag)::value;
+        constexpr bool kFirst = decltype(first_tag)::value;
+        constexpr int PAR = J & 1;
+        if constexpr (PAR == 0) {
+          dma(dma_k_slot<(J + 3) % 4>(), j + 3, F(), bk0);
+          dma(dma_k_slot<J>(), j + 4, F(), bk1);
+          dma(dma_v_slot<(J + 1) % 4>(), j + 1, T(), bv0);
+          dma(dma_v_slot<(J + 2) % 4>(), j + 2, T(), bv1);
+          bn0 = blk_of(j + 5);
+          bn1 = blk_of(j + 6);
+        }
+        qk(dma_k_slot<(J + 1) % 4>(), w.s[PAR ^ 1]);
+        if constexpr (!kFirst) pv(dma_v_slot<(J + 3) % 4>());
+        f32x16 &sc = w.s[PAR];
+        u32x4 pf[2];
+        if constexpr (kMask) apply_mask(sc, lim_of(j));
+        if constexpr (kFirst) {
+          const float tm = tile_max(sc, sl2);
+          w.m_run = tm > -INFINITY ? tm : 0.f;
+        }
+        float rs = softmax_tile<DT>(sc, pf, sl2, w.m_run);
+        if (!kFirst && __builtin_amdgcn_ballot_w64(!(rs <= Elem<DT>::kSumLimit))) rs = settle_max<D, DT>(w, sc, pf, sl2);
+        w.l_run += rs;
+        w.pf_prev[0] = pf[0];
+        w.pf_prev[1] = pf[1];
+        if constexpr (PAR == 1) {
+          dma_barrier<0>();
+          bv0 = bk0;
+          bv1 = bk1;
+          bk0 = bn0;
+          bk1 = bn1;
+        }
+      };
+      using I0 = std::integral_constant<int, 0>;
+      using I1 = std::integral_constant<int, 1>;
+      using I2 = std::integral_constant<int, 2>;
+      using I3 = std::integral_constant<int, 3>;
+      // j = 0..3 masked (exact for any tile; j = 0 sets the reference max),
+      // then whole groups of four unmasked tiles, then the rest masked.
+      iterate(I0(), T(), T(), 0);
+      int j = 1;
+      if (j < n) iterate(I1(), T(), F(), j++);
+      if (j < n) iterate(I2(), T(), F(), j++);
+      if (j < n) iterate(I3(), T(), F(), j++);
+      const int jm = min(j_mask, n);
+      for (; j + 3 < jm; j += 4) {
+        iterate(I0(), F(), F(), j);
+        iterate(I1(), F(), F(), j + 1);
+        iterate(I2(), F(), F(), j + 2);
+        iterate(I3(), F(), F(), j + 3);
       }
-      if (j < j_end) iterate(P1(), mask_tag, T(), T(), F(), j++);
-    };
-    steady(F(), min(j_mask, n - 1));
-    steady(T(), n - 1);
-    // j = n - 1: PV(n-2) and softmax(n-1), then drain PV(n-1) (V(n-1) was
-    // written in iteration n-2; whichever of n-2, n-1 is even ended with a
-    // barrier).
-    if (n >= 2) {
-      if ((n - 1) & 1) iterate(P1(), T(), F(), T(), F(), n - 1); else iterate(P0(), T(), F(), T(), F(), n - 1);
+      while (j < n) {
+        iterate(I0(), T(), F(), j);
+        if (++j >= n) break;
+        iterate(I1(), T(), F(), j);
+        if (++j >= n) break;
+        iterate(I2(), T(), F(), j);
+        if (++j >= n) break;
+        iterate(I3(), T(), F(), j);
+        ++j;
+      }
+      // PV of the last tile; its V landed before the last pair's barrier.
+      switch ((n - 1) & 3) {
+        case 0: pv(dma_v_slot<0>()); break;
+        case 1: pv(dma_v_slot<1>()); break;
+        case 2: pv(dma_v_slot<2>()); break;
+        default: pv(dma_v_slot<3>()); break;
+      }
+      // Loads of tiles past the end may still be in flight.
+      dma_wait_all();
     }
-    pv_tile<D, DT>(slot_v(n - 1), w.pf_prev, w.oacc, lane);
+  } else {
+    // Staging: chunk c = tid + 512 i of a (K tile, V tile) pair; whether it is
+    // a K or a V chunk is uniform over a wave.
+    int voff[NCH], lds_off[NCH], crow[NCH], ccol[NCH];
+    bool is_v[NCH];
+  #pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      is_v[i] = wave * 64 + kThreads * i >= G_::kTileChunks;
+      const int c = tid + kThreads * i - (is_v[i] ? G_::kTileChunks : 0);
+      const int r = c / G_::kChunksPerRow, cc = c % G_::kChunksPerRow;
+      voff[i] = (int)((r * kv_stride + cc * 8) * 2);
+      lds_off[i] = is_v[i] ? G_::kSlots * G_::kTileK + r * G_::kLdsV + cc * 8 : r * G_::kLdsK + cc * 8;
+      crow[i] = r;
+      ccol[i] = wi.kvh * D + cc * 8;
+    }
+    // Regular-cache item: key k of the sequence is row k mod B of local block
+    // rc_ids[rc_off + k / B], read in place.  A wave's chunk i covers 4 (D=128)
+    // or 8 (D=64) consecutive rows of a tile that start on a multiple of that
+    // count, and B >= 16 is a power of two, so those rows share one block: its
+    // index is wave-uniform and the load goes through a buffer resource over
+    // that block's layer slice.  The index of tile t + 1 is read while tile t
+    // is loaded (tiles of one chunk are loaded in order, one per call), so the
+    // data loads never wait on it.  Rows past the range read the clamped last
+    // block; they are masked.
+    const int32_t *rc_ids = kPaged ? a.rc_ids + sd.rc_off : nullptr;
+    const uint16_t *rc_layer = kPaged ? a.rc_base + a.rc_layer_elems : nullptr;
+    const int rc_mask = (1 << a.block_shift) - 1;
+    const uint32_t rc_slice_bytes = (uint32_t)(a.rc_half_elems * 4);
+    int rc_next[NCH];
+  #pragma unroll
+    for (int i = 0; i < NCH; ++i) rc_next[i] = 0;
+    // The index table is read through the constant address space: the host
+    // writes it before the launch and nothing writes it during the kernel, so
+    // the uniform index loads are scalar loads.
+    const __attribute__((address_space(4))) int32_t *rc_ids_c =
+        (const __attribute__((address_space(4))) int32_t *)rc_ids;
+    auto rc_block = [&](int t, int i) {
+      const int row0 = __builtin_amdgcn_readfirstlane(crow[i]);
+      return rc_ids_c[min(k_begin + t * KT + row0, k_end - 1) >> a.block_shift];
+    };
+    // A negative tile index (prologue only) skips that half of the pair.
+    u32x4 lr[NCH];
+    auto stage_load = [&](u32x4 (&lr)[NCH], int kj, int vj) {
+  #pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        const int t = is_v[i] ? vj : kj;
+        if (t < 0) continue;
+        if (kPaged) {
+          const int blk = __builtin_amdgcn_readfirstlane(t == 0 ? rc_block(0, i) : rc_next[i]);
+          rc_next[i] = rc_block(t + 1, i);
+          const uint16_t *base = rc_layer + (int64_t)blk * a.rc_block_elems;
+          const int row = (k_begin + t * KT + crow[i]) & rc_mask;
+          const int off = (int)((row * kv_stride + ccol[i] + (is_v[i] ? a.rc_half_elems : 0)) * 2);
+          lr[i] = __builtin_bit_cast(
+              u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                         __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(base), (short)0,
+                                                           (int)rc_slice_bytes, 0x00020000),
+                         off, 0, 0));
+        } else {
+          lr[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc(is_v[i] ? vb : kb, t),
+                                                                                   voff[i], 0, 0));
+        }
+      }
+    };
+    // kt / vt: the tiles the K and V chunks hold (ring slot = tile mod 4); a
+    // negative tile skips that half.
+    auto stage_store = [&](const u32x4 (&lr)[NCH], int kt, int vt) {
+  #pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        const int t = is_v[i] ? vt : kt;
+        if (t >= 0) {
+          const int slot_off = is_v[i] ? (t & 3) * G_::kTileV : (t & 3) * G_::kTileK;
+          *reinterpret_cast<u32x4 *>(smem + lds_off[i] + slot_off) = lr[i];
+        }
+      }
+    };
+    auto slot_k = [&](int t) { return smem + (t & 3) * G_::kTileK; };
+    auto slot_v = [&](int t) { return smem + G_::kSlots * G_::kTileK + (t & 3) * G_::kTileV; };
+
+    if (n > 0 && !timed_out) {
+      // Prologue: K(0), K(1), K(2) and V(0) into the rings (their loads in
+      // flight together), K(3) and V(1) loaded for iteration 0, then QK(0).
+      {
+        u32x4 lb[NCH], lc[NCH];
+        stage_load(lr, 0, 0);
+        stage_load(lb, 1, -1);
+        stage_load(lc, 2, -1);
+        stage_store(lr, 0, 0);
+        stage_store(lb, 1, -1);
+        stage_store(lc, 2, -1);
+        stage_load(lr, 3, 1);
+      }
+      lds_barrier();
+      qk_tile<D, DT>(slot_k(0), w.qf, w.s[0], lane);
+
+      // Iteration j (tile parity PAR): QK(j+1) and PV(j-1) on the MFMA pipe,
+      // softmax(j) on the VALU, then K(j+3), V(j+1) into the rings and K(j+4),
+      // V(j+2) from memory.  Tile j's scores live in s[PAR].  The rings hold
+      // four tiles, so a workgroup barrier is needed only after even
+      // iterations: the two iterations between barriers read K(j+1), V(j-1)
+      // written at least one barrier earlier and write the two slots read
+      // last before that barrier.
+      auto iterate = [&](auto par_tag, auto mask_tag, auto qk_tag, auto pv_tag, auto first_tag, int j) {
+        constexpr int PAR = decltype(par_tag)::value;
+        constexpr bool kMask = decltype(mask_tag)::value;
+        constexpr bool kQk = decltype(qk_tag)::value;
+        constexpr bool kPv = decltype(pv_tag)::value;
+        constexpr bool kFirst = decltype(first_tag)::value;
+        __builtin_assume(j >= 0);
+        f32x16 &sc = w.s[PAR];
+        u32x4 pf[2];
+        if (kQk) qk_tile<D, DT>(slot_k(j + 1), w.qf, w.s[PAR ^ 1], lane);
+        if (kPv) pv_tile<D, DT>(slot_v(j - 1), w.pf_prev, w.oacc, lane);
+        if (kMask) apply_mask(sc, lim_of(j));
+        if (kFirst) {
+          const float tm = tile_max(sc, sl2);
+          w.m_run = tm > -INFINITY ? tm : 0.f;
+        }
+        float rs = softmax_tile<DT>(sc, pf, sl2, w.m_run);
+        if (!kFirst && __builtin_amdgcn_ballot_w64(!(rs <= Elem<DT>::kSumLimit))) rs = settle_max<D, DT>(w, sc, pf, sl2);
+        w.l_run += rs;
+        stage_store(lr, j + 3, j + 1);
+        stage_load(lr, j + 4, j + 2);
+        if (PAR == 0) lds_barrier();
+        w.pf_prev[0] = pf[0];
+        w.pf_prev[1] = pf[1];
+      };
+      using T = std::true_type;
+      using F = std::false_type;
+      using P0 = std::integral_constant<int, 0>;
+      using P1 = std::integral_constant<int, 1>;
+      // j = 0: masked variant (exact for any tile), exact max.
+      if (n > 1) iterate(P0(), T(), T(), F(), T(), 0); else iterate(P0(), T(), F(), F(), T(), 0);
+      // Steady state j = 1 .. n - 2, unrolled by two so that tile parity is
+      // known at compile time: unmasked tiles, then masked ones.
+      int j = 1;
+      auto steady = [&](auto mask_tag, int j_end) {
+        if (j < j_end && (j & 1) == 0) iterate(P0(), mask_tag, T(), T(), F(), j++);
+        for (; j + 1 < j_end; j += 2) {
+          iterate(P1(), mask_tag, T(), T(), F(), j);
+          iterate(P0(), mask_tag, T(), T(), F(), j + 1);
+        }
+        if (j < j_end) iterate(P1(), mask_tag, T(), T(), F(), j++);
+      };
+      steady(F(), min(j_mask, n - 1));
+      steady(T(), n - 1);
+      // j = n - 1: PV(n-2) and softmax(n-1), then drain PV(n-1) (V(n-1) was
+      // written in iteration n-2; whichever of n-2, n-1 is even ended with a
+      // barrier).
+      if (n >= 2) {
+        if ((n - 1) & 1) iterate(P1(), T(), F(), T(), F(), n - 1); else iterate(P0(), T(), F(), T(), F(), n - 1);
+      }
+      pv_tile<D, DT>(slot_v(n - 1), w.pf_prev, w.oacc, lane);
+    }
+
   }
 
   // Done with K/V: every load of it has been consumed (loads past the range
@@ -619,7 +878,6 @@ __device__ __forceinline__ WorkItem implicit_item(const AttnArgs &a, int w) {
 
 template <int D, int DT>
 __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[Geo<D>::kSmem];
   const WorkItem wi = a.items != nullptr ? a.items[blockIdx.x] : implicit_item(a, blockIdx.x);
   if (wi.seq < 0) {
     // Padding slot (XCD placement): no K/V to read, but it counts as done
@@ -628,10 +886,19 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
       __hip_atomic_fetch_add(a.done_counter, (uint64_t)1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return;
   }
-  if (wi.paged)
-    attn_item<D, DT, true>(a, wi, smem);
-  else
-    attn_item<D, DT, false>(a, wi, smem);
+  if constexpr (D == 128) {
+    // K/V slots are the namespace-scope arrays above.
+    if (wi.paged)
+      attn_item<D, DT, true>(a, wi, nullptr);
+    else
+      attn_item<D, DT, false>(a, wi, nullptr);
+  } else {
+    __shared__ __attribute__((aligned(16))) uint16_t smem[Geo<D>::kSmem];
+    if (wi.paged)
+      attn_item<D, DT, true>(a, wi, smem);
+    else
+      attn_item<D, DT, false>(a, wi, smem);
+  }
 }
 
 // Split-key merge: D / 8 lanes per (token, head) row, 8 dims per lane.
@@ -763,7 +1030,18 @@ int attn_fwd_vgprs(int head_dim) {
 }
 
 size_t attn_fwd_lds_bytes(int head_dim) {
-  return head_dim == 128 ? sizeof(uint16_t) * Geo<128>::kSmem : sizeof(uint16_t) * Geo<64>::kSmem;
+  // The largest static LDS of the two element types' kernels; the full LDS
+  // of a CU if the runtime cannot tell.
+  size_t m = 0;
+  for (const void *f : {head_dim == 128 ? reinterpret_cast<const void *>(&attn_fwd_kernel<128, SC_DTYPE_BF16>)
+                                        : reinterpret_cast<const void *>(&attn_fwd_kernel<64, SC_DTYPE_BF16>),
+                        head_dim == 128 ? reinterpret_cast<const void *>(&attn_fwd_kernel<128, SC_DTYPE_F16>)
+                                        : reinterpret_cast<const void *>(&attn_fwd_kernel<64, SC_DTYPE_F16>)}) {
+    hipFuncAttributes at{};
+    if (hipFuncGetAttributes(&at, f) != hipSuccess) return (size_t)160 << 10;
+    m = at.sharedSizeBytes > m ? at.sharedSizeBytes : m;
+  }
+  return m;
 }
 
 hipError_t launch_attn_merge(const AttnArgs &a, int head_dim, hipStream_t stream) {
