@@ -195,23 +195,45 @@ struct DmaGeo {
   static constexpr int kRowBytes = 128 * 2;               // one key row of one KV head
   static constexpr int kSlotBytes = KT * kRowBytes;        // one tile, 8 KiB
 };
-__shared__ __attribute__((aligned(1024))) unsigned char dma_k0[DmaGeo::kSlotBytes];
-__shared__ __attribute__((aligned(1024))) unsigned char dma_k1[DmaGeo::kSlotBytes];
-__shared__ __attribute__((aligned(1024))) unsigned char dma_k2[DmaGeo::kSlotBytes];
-__shared__ __attribute__((aligned(1024))) unsigned char dma_k3[DmaGeo::kSlotBytes];
-__shared__ __attribute__((aligned(1024))) unsigned char dma_v0[DmaGeo::kSlotBytes];
-__shared__ __attribute__((aligned(1024))) unsigned char dma_v1[DmaGeo::kSlotBytes];
-__shared__ __attribute__((aligned(1024))) unsigned char dma_v2[DmaGeo::kSlotBytes];
-__shared__ __attribute__((aligned(1024))) unsigned char dma_v3[DmaGeo::kSlotBytes];
+// Pairs of iterations a tile load has to land in, and the ring size that
+// allows (tiles read in the A pairs after a load plus the two it loads).
+// One pair is enough: with two or three (96 or 128 KiB of LDS) the kernel
+// measured 1.5-3% slower on the 8B, 14B and long-prefix shapes.
+constexpr int kDmaAhead = 1;
+constexpr int kDmaRing = 2 * kDmaAhead + 2;
+static_assert(kDmaAhead >= 1 && kDmaRing <= 8, "ring of at most 8 slots");
+#define SC_DMA_SLOT(n)                                                          \
+  __shared__ __attribute__((aligned(1024))) unsigned char dma_k##n[DmaGeo::kSlotBytes]; \
+  __shared__ __attribute__((aligned(1024))) unsigned char dma_v##n[DmaGeo::kSlotBytes];
+SC_DMA_SLOT(0)
+SC_DMA_SLOT(1)
+SC_DMA_SLOT(2)
+SC_DMA_SLOT(3)
+SC_DMA_SLOT(4)
+SC_DMA_SLOT(5)
+SC_DMA_SLOT(6)
+SC_DMA_SLOT(7)
+#undef SC_DMA_SLOT
 template <int S>
 __device__ __forceinline__ unsigned char *dma_k_slot() {
-  static_assert(S >= 0 && S < 4, "ring slot");
-  return S == 0 ? dma_k0 : S == 1 ? dma_k1 : S == 2 ? dma_k2 : dma_k3;
+  static_assert(S >= 0 && S < kDmaRing, "ring slot");
+  return S == 0 ? dma_k0 : S == 1 ? dma_k1 : S == 2 ? dma_k2 : S == 3 ? dma_k3
+       : S == 4 ? dma_k4 : S == 5 ? dma_k5 : S == 6 ? dma_k6 : dma_k7;
 }
 template <int S>
 __device__ __forceinline__ unsigned char *dma_v_slot() {
-  static_assert(S >= 0 && S < 4, "ring slot");
-  return S == 0 ? dma_v0 : S == 1 ? dma_v1 : S == 2 ? dma_v2 : dma_v3;
+  static_assert(S >= 0 && S < kDmaRing, "ring slot");
+  return S == 0 ? dma_v0 : S == 1 ? dma_v1 : S == 2 ? dma_v2 : S == 3 ? dma_v3
+       : S == 4 ? dma_v4 : S == 5 ? dma_v5 : S == 6 ? dma_v6 : dma_v7;
+}
+
+// f(integral_constant<int, i>) for i = B .. E-1, unrolled.
+template <int B, int E, class Fn>
+__device__ __forceinline__ void static_for(Fn &&f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>());
+    static_for<B + 1, E>(f);
+  }
 }
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -538,106 +560,133 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
     if (n > 0 && !timed_out) {
       using T = std::true_type;
       using F = std::false_type;
+      constexpr int A = kDmaAhead;
+      constexpr int R = kDmaRing;
       // Regular-cache block indices of the tiles the current pair loads into
-      // K (bk0, bk1) and V (bv0, bv1), and of the next pair's K tiles.
-      int bv0 = 0, bv1 = 0, bk0 = 0, bk1 = 0, bn0 = 0, bn1 = 0;
-      // Prologue: K(0), K(1), K(2) and V(0), then QK(0).  Iteration 0 loads
-      // K(4) into the slot QK(0) reads: a second barrier.
-      {
-        const int b0 = blk_of(0), b1 = blk_of(1), b2 = blk_of(2);
-        dma(dma_k_slot<0>(), 0, F(), b0);
-        dma(dma_v_slot<0>(), 0, T(), b0);
-        dma(dma_k_slot<1>(), 1, F(), b1);
-        dma(dma_k_slot<2>(), 2, F(), b2);
-        bv0 = b1;
-        bv1 = b2;
-        bk0 = blk_of(3);
-        bk1 = blk_of(4);
-      }
+      // K (bk0, bk1) and V (bv0, bv1), and of the next pair's K tiles.  The
+      // V tiles of a pair are the K tiles of the pair before.
+      int bv0 = blk_of(2 * A - 1), bv1 = blk_of(2 * A), bk0 = blk_of(2 * A + 1), bk1 = blk_of(2 * A + 2);
+      int bn0 = 0, bn1 = 0;
+      // Prologue: K(0 .. 2A) and V(0 .. 2A-2), the operands of the first A
+      // pairs; then QK(0).  The first pair loads into the slot QK(0) reads:
+      // a second barrier.
+      static_for<0, 2 * A + 1>([&](auto t) { dma(dma_k_slot<decltype(t)::value % R>(), t, F(), blk_of(t)); });
+      static_for<0, 2 * A - 1>([&](auto t) { dma(dma_v_slot<decltype(t)::value % R>(), t, T(), blk_of(t)); });
       dma_barrier<0>();
       qk(dma_k_slot<0>(), w.s[0]);
       dma_barrier<0>();
 
-      // Iteration j (J = j mod 4 is the ring slot of tile j; tile j's scores
-      // live in s[j mod 2]).  An even iteration starts a pair of iterations:
-      // it loads K(j+3), K(j+4), V(j+1) and V(j+2) into the slots last read
-      // in the previous pair; the odd one ends the pair with a barrier after
-      // all of them have landed, so every load has two iterations to land
-      // and only every second iteration waits at a barrier.  Loads of tiles
-      // past the last one load zeros.  QK(j+1) runs in every iteration, also
-      // the last, whose product of a stale slot is never used: one body
-      // throughout keeps the MFMA accumulators in place and the MFMAs in the
-      // same basic block as the softmax they interleave with.
+      // Iteration j (J = j mod R is the ring slot of tile j; tile j's scores
+      // live in s[j mod 2]).  Pair p = iterations 2p, 2p+1 reads K(2p+1),
+      // K(2p+2), V(2p-1), V(2p).  Its even iteration loads the operands of
+      // pair p+A: K(j+1+2A), K(j+2+2A), V(j-1+2A), V(j+2A), into the slots
+      // last read in pair p-1; its odd iteration ends with a barrier once
+      // the loads issued A-1 pairs earlier have landed, so a load has A
+      // pairs of iterations to land and only every second iteration waits
+      // at a barrier.  Loads of tiles past the last one load zeros.  QK(j+1)
+      // runs in every iteration, also the last, whose product of a stale
+      // slot is never used: one body throughout keeps the MFMA accumulators
+      // in place.
       auto iterate = [&](auto j_tag, auto mask_tag, auto first_tag, int j) {
         constexpr int J = decltype(j_tag)::value;
         constexpr bool kMask = decltype(mask_tag)::value;
         constexpr bool kFirst = decltype(first_tag)::value;
         constexpr int PAR = J & 1;
-        if constexpr (PAR == 0) {
-          dma(dma_k_slot<(J + 3) % 4>(), j + 3, F(), bk0);
-          dma(dma_k_slot<J>(), j + 4, F(), bk1);
-          dma(dma_v_slot<(J + 1) % 4>(), j + 1, T(), bv0);
-          dma(dma_v_slot<(J + 2) % 4>(), j + 2, T(), bv1);
-          bn0 = blk_of(j + 5);
-          bn1 = blk_of(j + 6);
-        }
-        qk(dma_k_slot<(J + 1) % 4>(), w.s[PAR ^ 1]);
-        if constexpr (!kFirst) pv(dma_v_slot<(J + 3) % 4>());
         f32x16 &sc = w.s[PAR];
-        u32x4 pf[2];
+        f32x16 &sn = w.s[PAR ^ 1];
         if constexpr (kMask) apply_mask(sc, lim_of(j));
         if constexpr (kFirst) {
           const float tm = tile_max(sc, sl2);
           w.m_run = tm > -INFINITY ? tm : 0.f;
         }
-        float rs = softmax_tile<DT>(sc, pf, sl2, w.m_run);
+        const float mneg = -w.m_run;
+        const unsigned char *ks = dma_k_slot<(J + 1) % R>();
+        const unsigned char *vs = dma_v_slot<(J + R - 1) % R>();
+        // The 16 MFMAs of the iteration alternate between QK(j+1) (even
+        // steps, K fragment i / 2) and PV(j-1) (odd steps, V^T block
+        // c = (i / 2) mod 4 of key half t = i / 8), and each step also
+        // computes one probability of tile j: one MFMA and a sixteenth of
+        // the softmax per step, in this order (scheduling barriers keep the
+        // compiler from regrouping them).  Operands are read from LDS two
+        // steps ahead.
+        auto operand = [&](int i) -> u32x4 {
+          if ((i & 1) == 0) return *reinterpret_cast<const u32x4 *>(ks + k_rd[i >> 1]);
+          const unsigned char *p = vs + v_rd[(i >> 1) & 3] + 16 * (i >> 3) * DmaGeo::kRowBytes;
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)p);
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(p + 8 * DmaGeo::kRowBytes));
+          u32x4 vw;
+          vw[0] = __builtin_bit_cast(u32x2, lo)[0];
+          vw[1] = __builtin_bit_cast(u32x2, lo)[1];
+          vw[2] = __builtin_bit_cast(u32x2, hi)[0];
+          vw[3] = __builtin_bit_cast(u32x2, hi)[1];
+          return vw;
+        };
+        u32x4 op[16];
+        u32x4 pf[2];
+        float r2[2] = {0.f, 0.f};
+        float x_prev = 0.f;
+        op[0] = operand(0);
+        if constexpr (!kFirst) op[1] = operand(1);
+        else op[1] = u32x4{0u, 0u, 0u, 0u};
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          if (i + 2 < 16) {
+            if (!kFirst || ((i + 2) & 1) == 0) op[i + 2] = operand(i + 2);
+          }
+          if ((i & 1) == 0) {
+            sn = Elem<DT>::mfma(op[i], w.qf[i >> 1], i == 0 ? f32x16{} : sn);
+          } else if constexpr (!kFirst) {
+            w.oacc[(i >> 1) & 3] = Elem<DT>::mfma(op[i], w.pf_prev[i >> 3], w.oacc[(i >> 1) & 3]);
+          }
+          const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[i], sl2, mneg));
+          if (i & 1) {
+            const uint32_t pk = Elem<DT>::pack(x_prev, x);
+            pf[i >> 3][(i & 7) >> 1] = pk;
+            r2[i >> 3] = Elem<DT>::add_pair(pk, r2[i >> 3]);
+          }
+          x_prev = x;
+          if constexpr (PAR == 0) {
+            if (i == 1) dma(dma_k_slot<(J + 1 + 2 * A) % R>(), j + 1 + 2 * A, F(), bk0);
+            if (i == 3) dma(dma_k_slot<(J + 2 + 2 * A) % R>(), j + 2 + 2 * A, F(), bk1);
+            if (i == 5) dma(dma_v_slot<(J - 1 + 2 * A) % R>(), j - 1 + 2 * A, T(), bv0);
+            if (i == 7) dma(dma_v_slot<(J + 2 * A) % R>(), j + 2 * A, T(), bv1);
+            if (i == 9) bn0 = blk_of(j + 3 + 2 * A);
+            if (i == 11) bn1 = blk_of(j + 4 + 2 * A);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        float rs = r2[0] + r2[1];
         if (!kFirst && __builtin_amdgcn_ballot_w64(!(rs <= Elem<DT>::kSumLimit))) rs = settle_max<D, DT>(w, sc, pf, sl2);
         w.l_run += rs;
         w.pf_prev[0] = pf[0];
         w.pf_prev[1] = pf[1];
         if constexpr (PAR == 1) {
-          dma_barrier<0>();
+          dma_barrier<4 * (A - 1)>();
           bv0 = bk0;
           bv1 = bk1;
           bk0 = bn0;
           bk1 = bn1;
         }
       };
-      using I0 = std::integral_constant<int, 0>;
-      using I1 = std::integral_constant<int, 1>;
-      using I2 = std::integral_constant<int, 2>;
-      using I3 = std::integral_constant<int, 3>;
-      // j = 0..3 masked (exact for any tile; j = 0 sets the reference max),
-      // then whole groups of four unmasked tiles, then the rest masked.
-      iterate(I0(), T(), T(), 0);
-      int j = 1;
-      if (j < n) iterate(I1(), T(), F(), j++);
-      if (j < n) iterate(I2(), T(), F(), j++);
-      if (j < n) iterate(I3(), T(), F(), j++);
+      // j = 0 .. R-1 masked (exact for any tile; j = 0 sets the reference
+      // max), then whole rounds of R unmasked tiles, then the rest masked.
+      iterate(std::integral_constant<int, 0>(), T(), T(), 0);
+      static_for<1, R>([&](auto J) {
+        if (decltype(J)::value < n) iterate(J, T(), F(), decltype(J)::value);
+      });
+      int j = R;
       const int jm = min(j_mask, n);
-      for (; j + 3 < jm; j += 4) {
-        iterate(I0(), F(), F(), j);
-        iterate(I1(), F(), F(), j + 1);
-        iterate(I2(), F(), F(), j + 2);
-        iterate(I3(), F(), F(), j + 3);
-      }
-      while (j < n) {
-        iterate(I0(), T(), F(), j);
-        if (++j >= n) break;
-        iterate(I1(), T(), F(), j);
-        if (++j >= n) break;
-        iterate(I2(), T(), F(), j);
-        if (++j >= n) break;
-        iterate(I3(), T(), F(), j);
-        ++j;
-      }
+      for (; j + R - 1 < jm; j += R) static_for<0, R>([&](auto J) { iterate(J, F(), F(), j + decltype(J)::value); });
+      for (; j < n; j += R)
+        static_for<0, R>([&](auto J) {
+          if (j + decltype(J)::value < n) iterate(J, T(), F(), j + decltype(J)::value);
+        });
       // PV of the last tile; its V landed before the last pair's barrier.
-      switch ((n - 1) & 3) {
-        case 0: pv(dma_v_slot<0>()); break;
-        case 1: pv(dma_v_slot<1>()); break;
-        case 2: pv(dma_v_slot<2>()); break;
-        default: pv(dma_v_slot<3>()); break;
-      }
+      const int last = (n - 1) % R;
+      static_for<0, R>([&](auto S) {
+        if (last == decltype(S)::value) pv(dma_v_slot<decltype(S)::value>());
+      });
       // Loads of tiles past the end may still be in flight.
       dma_wait_all();
     }
