@@ -360,6 +360,37 @@ __device__ __forceinline__ float settle_max(WaveState<D> &w, const f32x16 &s, u3
   return softmax_tile<DT>(s, pf, sl2, m_new);
 }
 
+// Writes this lane's row of O (times inv, rounded to the element type) to
+// `dst`.  A lane holds 4 consecutive dims of each 8-dim block, the other 4
+// are in the same lane of the other half of the wave; one lane swap per
+// dword gives half 0 the even and half 1 the odd 8-dim blocks of each 16,
+// so every lane writes whole 16-byte chunks (the two halves of a row fill
+// 32 contiguous bytes per store).  v_permlane32_swap exchanges lanes 32-63
+// of its first operand with lanes 0-31 of its second.
+template <int D, int DT>
+__device__ __forceinline__ void store_row(const WaveState<D> &w, float inv, int half, uint16_t *dst) {
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c)
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      // A: dims 32c + 16m + 4 half + [0, 4); B: the same + 8.
+      uint32_t A[2], B[2];
+      A[0] = Elem<DT>::pack(w.oacc[c][8 * m + 0] * inv, w.oacc[c][8 * m + 1] * inv);
+      A[1] = Elem<DT>::pack(w.oacc[c][8 * m + 2] * inv, w.oacc[c][8 * m + 3] * inv);
+      B[0] = Elem<DT>::pack(w.oacc[c][8 * m + 4] * inv, w.oacc[c][8 * m + 5] * inv);
+      B[1] = Elem<DT>::pack(w.oacc[c][8 * m + 6] * inv, w.oacc[c][8 * m + 7] * inv);
+      u32x4 st;
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        // Half 0 receives the other half's A, half 1 the other half's B.
+        const auto r = __builtin_amdgcn_permlane32_swap(A[e], B[e], false, false);
+        st[e] = (uint32_t)r[0];
+        st[2 + e] = (uint32_t)r[1];
+      }
+      *reinterpret_cast<u32x4 *>(dst + 32 * c + 16 * m + 8 * half) = st;
+    }
+}
+
 // One work item.  kPaged: its keys are read in place from the regular
 // cache; the two kinds of item are separate copies of the whole body so that
 // each is register-allocated on its own.
@@ -863,17 +894,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
                         : l_tot > 0.f ? (w.m_run + __log2f(l_tot)) * 0.69314718055994530942f : -INFINITY;
   if (!valid) return;
   if (sd.n_splits == 1) {
-    uint16_t *orow = a.out + io_row * D;
-#pragma unroll
-    for (int c = 0; c < D / 32; ++c)
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int dim = 32 * c + 8 * g4 + 4 * half;
-        u32x2 pk;
-        pk[0] = Elem<DT>::pack(w.oacc[c][4 * g4 + 0] * inv, w.oacc[c][4 * g4 + 1] * inv);
-        pk[1] = Elem<DT>::pack(w.oacc[c][4 * g4 + 2] * inv, w.oacc[c][4 * g4 + 3] * inv);
-        *reinterpret_cast<u32x2 *>(orow + dim) = pk;
-      }
+    store_row<D, DT>(w, inv, half, a.out + io_row * D);
     if (a.lse != nullptr && half == 0) a.lse[(int64_t)h * a.total_q + sd.cu_q + qpos] = lse_val;
     return;
   }
@@ -883,17 +904,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
   // The partial is a convex combination of V rows, so it fits the element
   // type's range; storing it in that type halves the split traffic for one
   // extra rounding (2^-9 relative for bf16, 2^-11 for fp16).
-  uint16_t *po = a.part_o + prow * D;
-#pragma unroll
-  for (int c = 0; c < D / 32; ++c)
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const int dim = 32 * c + 8 * g4 + 4 * half;
-      u32x2 pk;
-      pk[0] = Elem<DT>::pack(w.oacc[c][4 * g4 + 0] * inv, w.oacc[c][4 * g4 + 1] * inv);
-      pk[1] = Elem<DT>::pack(w.oacc[c][4 * g4 + 2] * inv, w.oacc[c][4 * g4 + 3] * inv);
-      *reinterpret_cast<u32x2 *>(po + dim) = pk;
-    }
+  store_row<D, DT>(w, inv, half, a.part_o + prow * D);
   if (half == 0) a.part_lse[prow] = lse_val;
 }
 
