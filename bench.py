@@ -62,6 +62,34 @@ def _src_sha16(name):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
+def plain_copy_reference(torch, timed, stream, nbytes):
+    """The runtime's own device-to-device copy (torch copy_) of the fetch's
+    byte count, sources and destinations rotating over more than the
+    Infinity Cache: what a contiguous copy of the same size reaches on this
+    GPU, for comparison with the block gather of the fetch."""
+    n = max(1, nbytes // 2)
+    pairs = max(2, min(16, -(-(2 * MALL_BYTES) // max(nbytes, 1))))
+    with torch.cuda.stream(stream):
+        src = [torch.ones(n, dtype=torch.int16, device="cuda") for _ in range(pairs)]
+        dst = [torch.empty(n, dtype=torch.int16, device="cuda") for _ in range(pairs)]
+    st = {"i": 0}
+
+    def one():
+        i = st["i"]
+        with torch.cuda.stream(stream):
+            dst[i % pairs].copy_(src[(i * 7 + 3) % pairs])
+        st["i"] = i + 1
+
+    for _ in range(pairs):
+        one()
+    reps = max(4 * pairs, 32)
+    us = timed(one, reps, stream) * 1e3          # timed() returns ms per call
+    del src, dst
+    gbs = 2.0 * n * 2 / (us * 1e-6) / 1e9
+    return {"us": round(us, 2), "hbm_gbs": round(gbs, 1), "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+            "rotation": f"{pairs} source/destination pairs of {n * 2 >> 20} MiB"}
+
+
 def attention_flops(wl):
     """Algorithmic flops of one layer's attention: 4 * D * H_q per visible
     (query, key) pair; pairs per sequence = N * P + N (N + 1) / 2."""
@@ -280,6 +308,8 @@ def run_workload(args, cfg, torch, sc, W, DevicePool, with_cpu, turn=None, rc_fr
         gbs = 2.0 * payload / t_fetch / 1e9
         fetch.update({"hbm_gbs": round(gbs, 1), "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
                       "bound": "hbm"})
+        fetch["plain_copy_reference"] = plain_copy_reference(torch, timed, copy, payload)
+        fetch["vs_plain_copy"] = round(fetch["plain_copy_reference"]["us"] / (t_fetch * 1e6), 3)
     else:
         fetch.update(host_tier_detail(args, wl, dp, sc, torch, timed, rot_slots, copy, t_fetch, dev_b, host_b))
 
