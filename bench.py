@@ -53,7 +53,13 @@ ROTATE_BYTES = 512 << 20         # destination buffers the standalone fetch cycl
 # that map the same counters to a plain 256 MiB device copy), per workload,
 # with the hash of the attention source they were taken on; a stale entry
 # (the source changed since) is reported as null.
-PMC_TRAFFIC = {}
+PMC_TRAFFIC = {
+    "llama3-8b-P8192-N512": (80656766, "f96b56d72da41fde"),
+    "llama3-8b-batch16-varlen": (708219721, "f96b56d72da41fde"),
+    "qwen-14b-P32768-N1024": (362526163, "f96b56d72da41fde"),
+    "llama3-8b-P131072-N2048-hosttier": (1190410310, "f96b56d72da41fde"),
+    "llama3-8b-P8192-N512-rc0.5": (80142154, "f96b56d72da41fde"),
+}
 
 
 def _src_sha16(name):
