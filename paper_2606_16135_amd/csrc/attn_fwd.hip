@@ -908,6 +908,121 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
   if (half == 0) a.part_lse[prow] = lse_val;
 }
 
+// Split-key merge of NR (token, head) rows per lane group: D / 8 lanes per
+// row, 8 dims per lane (`sub`); rows[i] < 0 are skipped; at most SMAX
+// splits per row.  Weights
+// exp(lse_s - max) over the row's splits, weighted sum of the partials,
+// written to `out` (and the row's natural-log lse to lse_out if given).
+// Every split's lse and partial chunk of all NR rows are loaded before any
+// is used: one memory round trip, whatever the split count (merging a few
+// thousand rows is latency-bound, not bandwidth-bound).
+template <int D, int DT, int NR, int SMAX = kAttnMaxSplits>
+__device__ __forceinline__ void merge_rows(const AttnArgs &a, const int64_t (&rows_i)[NR], int sub,
+                                           const uint16_t *part_o, const float *part_lse, uint16_t *out,
+                                           float *lse_out) {
+  const int64_t rows = (int64_t)a.total_q * a.n_q_heads;
+  SeqDesc sd[NR];
+  float ls[NR][SMAX];
+  u32x4 x[NR][SMAX];
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    const int64_t row = rows_i[i] < 0 ? 0 : rows_i[i];
+    const int token = (int)(row / a.n_q_heads);
+    int lo = 0;
+    if (a.n_seqs > 1) {
+      int hi = a.n_seqs - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (a.seqs[mid].cu_q <= token) lo = mid; else hi = mid - 1;
+      }
+    }
+    sd[i] = a.seqs != nullptr ? a.seqs[lo] : a.seq0;
+    const int S = rows_i[i] < 0 ? 0 : sd[i].n_splits;
+    const uint16_t *po = part_o + row * D + sub * 8;
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s) {
+      if (s < S && S > 1) {
+        ls[i][s] = part_lse[s * rows + row];
+        x[i][s] = *reinterpret_cast<const u32x4 *>(po + (int64_t)s * rows * D);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    const int S = rows_i[i] < 0 ? 0 : sd[i].n_splits;
+    if (S <= 1) continue;
+    const int64_t row = rows_i[i];
+    const int token = (int)(row / a.n_q_heads);
+    const int h = (int)(row - (int64_t)token * a.n_q_heads);
+    const int64_t io_row = (int64_t)(sd[i].q_off + token - sd[i].cu_q) * a.n_q_heads + h;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s)
+      if (s < S) mx = fmaxf(mx, ls[i][s]);
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float wsum = 0.f;
+#pragma unroll
+    for (int s = 0; s < SMAX; ++s)
+      if (s < S) {
+        const float wgt = ls[i][s] == -INFINITY ? 0.f : __expf(ls[i][s] - mx);
+        wsum += wgt;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const f32x2 v = Elem<DT>::unpack(x[i][s][e]);
+          acc[2 * e] += wgt * v[0];
+          acc[2 * e + 1] += wgt * v[1];
+        }
+      }
+    const float winv = wsum > 0.f ? 1.f / wsum : 0.f;
+    u32x4 pk;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) pk[e] = Elem<DT>::pack(acc[2 * e] * winv, acc[2 * e + 1] * winv);
+    *reinterpret_cast<u32x4 *>(out + io_row * D + sub * 8) = pk;
+    if (lse_out != nullptr && sub == 0)
+      lse_out[(int64_t)h * a.total_q + token] = wsum > 0.f ? mx + __logf(wsum) : -INFINITY;
+  }
+}
+
+// The deferred merge of the previous layer (AttnArgs::dm_out), run by a
+// workgroup after its own item: it claims chunks of rows (one row per D / 8
+// lanes, NR rows per lane group in one memory round trip) until all are
+// claimed, so the workgroups that finish their items first do most of it.
+// With at most four splits per row (the common plans) a lane group takes
+// four rows; with more, one (the registers of the split values).  The
+// claims only divide the work; no data flows through the counter (the
+// partials were written by the previous launch on the stream).
+template <int D, int DT, int NR, int SMAX>
+__device__ __forceinline__ void deferred_merge_n(const AttnArgs &a) {
+  constexpr int LPR = D / 8;
+  constexpr int RPP = kThreads / LPR;   // rows per pass and row slot
+  constexpr int64_t kChunk = (int64_t)NR * RPP;
+  __shared__ uint32_t s_claim;
+  const int64_t rows = (int64_t)a.total_q * a.n_q_heads;
+  const int64_t n_chunks = (rows + kChunk - 1) / kChunk;
+  const int sub = threadIdx.x % LPR;
+  for (;;) {
+    __syncthreads();                      // every lane has read the last claim
+    if (threadIdx.x == 0)
+      s_claim = __hip_atomic_fetch_add(a.dm_counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    const int64_t c = (int64_t)s_claim;
+    if (c >= n_chunks) break;
+    const int64_t base = c * kChunk + threadIdx.x / LPR;
+    int64_t rr[NR];
+#pragma unroll
+    for (int i = 0; i < NR; ++i) rr[i] = base + i * RPP < rows ? base + i * RPP : -1;
+    merge_rows<D, DT, NR, SMAX>(a, rr, sub, a.dm_part_o, a.dm_part_lse, a.dm_out, nullptr);
+  }
+}
+
+template <int D, int DT>
+__device__ __forceinline__ void deferred_merge(const AttnArgs &a) {
+  if (a.dm_max_splits <= 4)
+    deferred_merge_n<D, DT, 4, 4>(a);
+  else
+    deferred_merge_n<D, DT, 1, kAttnMaxSplits>(a);
+}
+
 // Item of workgroup w in an implicit work list (see AttnArgs::seq0).
 __device__ __forceinline__ WorkItem implicit_item(const AttnArgs &a, int w) {
   WorkItem wi{-1, 0, 0, 0, 0, 0, 0, 0};
@@ -937,7 +1052,7 @@ __device__ __forceinline__ WorkItem implicit_item(const AttnArgs &a, int w) {
 }
 
 template <int D, int DT>
-__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
+__device__ __forceinline__ void attn_fwd_body(const AttnArgs &a) {
   const WorkItem wi = a.items != nullptr ? a.items[blockIdx.x] : implicit_item(a, blockIdx.x);
   if (wi.seq < 0) {
     // Padding slot (XCD placement): no K/V to read, but it counts as done
@@ -961,68 +1076,23 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
   }
 }
 
-// Split-key merge: D / 8 lanes per (token, head) row, 8 dims per lane.
-// Weights exp(lse_s - max) over the splits, weighted sum of the partials.
+// One work item per workgroup, then (in a layer stack with deferred
+// merges) its share of the previous layer's merge.
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(AttnArgs a) {
+  attn_fwd_body<D, DT>(a);
+  if (a.dm_out != nullptr) deferred_merge<D, DT>(a);
+}
+
 template <int D, int DT>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
   constexpr int LPR = D / 8;
   constexpr int RPB = 256 / LPR;
   const int64_t rows = (int64_t)a.total_q * a.n_q_heads;
   const int64_t row = (int64_t)blockIdx.x * RPB + threadIdx.x / LPR;
-  const int sub = threadIdx.x % LPR;
   if (row >= rows) return;
-  const int token = (int)(row / a.n_q_heads);
-  const int h = (int)(row - (int64_t)token * a.n_q_heads);
-  int lo = 0;
-  if (a.n_seqs > 1) {
-    int hi = a.n_seqs - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (a.seqs[mid].cu_q <= token) lo = mid; else hi = mid - 1;
-    }
-  }
-  const SeqDesc sd = a.seqs != nullptr ? a.seqs[lo] : a.seq0;
-  const int S = sd.n_splits;
-  if (S <= 1) return;
-  const int64_t io_row = (int64_t)(sd.q_off + token - sd.cu_q) * a.n_q_heads + h;
-  // Every split's lse and partial row are loaded before any is used: one
-  // memory round trip per row, whatever the split count (a merge of a few
-  // thousand rows is latency-bound, not bandwidth-bound).
-  const uint16_t *po = a.part_o + row * D + sub * 8;
-  float ls[kAttnMaxSplits];
-  u32x4 x[kAttnMaxSplits];
-#pragma unroll
-  for (int s = 0; s < kAttnMaxSplits; ++s) {
-    if (s < S) {
-      ls[s] = a.part_lse[s * rows + row];
-      x[s] = *reinterpret_cast<const u32x4 *>(po + (int64_t)s * rows * D);
-    }
-  }
-  float mx = -INFINITY;
-#pragma unroll
-  for (int s = 0; s < kAttnMaxSplits; ++s)
-    if (s < S) mx = fmaxf(mx, ls[s]);
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  float wsum = 0.f;
-#pragma unroll
-  for (int s = 0; s < kAttnMaxSplits; ++s)
-    if (s < S) {
-      const float wgt = ls[s] == -INFINITY ? 0.f : __expf(ls[s] - mx);
-      wsum += wgt;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const f32x2 v = Elem<DT>::unpack(x[s][e]);
-        acc[2 * e] += wgt * v[0];
-        acc[2 * e + 1] += wgt * v[1];
-      }
-    }
-  const float winv = wsum > 0.f ? 1.f / wsum : 0.f;
-  u32x4 pk;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) pk[e] = Elem<DT>::pack(acc[2 * e] * winv, acc[2 * e + 1] * winv);
-  *reinterpret_cast<u32x4 *>(a.out + io_row * D + sub * 8) = pk;
-  if (a.lse != nullptr && sub == 0)
-    a.lse[(int64_t)h * a.total_q + token] = wsum > 0.f ? mx + __logf(wsum) : -INFINITY;
+  const int64_t rr[1] = {row};
+  merge_rows<D, DT, 1>(a, rr, threadIdx.x % LPR, a.part_o, a.part_lse, a.out, a.lse);
 }
 
 // Split-key partials of the allocation-free entry point: one array per

@@ -464,11 +464,31 @@ struct RcView {
   const int32_t *ids = nullptr;
 };
 
+// Split-key partials of a layer stack whose merges are deferred: the
+// layer's own partial buffer (ws) and the previous layer's (prev_ws, merged
+// into prev_out by the forward kernel's workgroups before their own items),
+// both laid out as a plan-sized workspace (partials, then lse).
+struct StackMerge {
+  void *ws = nullptr;
+  const void *prev_ws = nullptr;
+  void *prev_out = nullptr;
+  uint32_t *prev_counter = nullptr;   // zero before the launch
+};
+
+
+// Bytes of a plan's split-key workspace and the lse array's offset in it.
+size_t plan_ws_bytes(const AttnPlan &plan, int hq, int head_dim, size_t *lse_off = nullptr) {
+  const size_t rows = (size_t)plan.max_splits * plan.total_q * hq;
+  if (lse_off) *lse_off = rows * (size_t)head_dim * sizeof(uint16_t);
+  return rows * ((size_t)head_dim * sizeof(uint16_t) + sizeof(float));
+}
+
 sc_status run_attention(int device, const AttnPlan &plan, const void *q, const void *k, const void *v,
                         void *out, float *lse, int hq, int hkv, int head_dim, int dtype, float scale,
                         hipStream_t stream, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
                         hipEvent_t after_fwd = nullptr, const RcView &rc = RcView(),
-                        int spin_limit = kAttnReadySpinLimit, uint64_t *done_counter = nullptr) {
+                        int spin_limit = kAttnReadySpinLimit, uint64_t *done_counter = nullptr,
+                        const StackMerge *sm = nullptr) {
   if (plan.n_items == 0) return SC_OK;
   // The kernel addresses one sequence's rows of one KV head with 32-bit
   // byte offsets.
@@ -496,13 +516,22 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
   // Held until the forward and merge kernels are enqueued (see get_workspace).
   std::unique_lock<std::mutex> ws_hold;
   if (plan.max_splits > 1) {
-    const size_t rows = (size_t)plan.max_splits * plan.total_q * hq;
-    void *ws = nullptr;
-    sc_status st = get_workspace(device, stream, rows * ((size_t)head_dim * sizeof(uint16_t) + sizeof(float)), &ws,
-                                 &ws_hold);
-    if (st != SC_OK) return st;
+    size_t lse_off = 0;
+    const size_t bytes = plan_ws_bytes(plan, hq, head_dim, &lse_off);
+    void *ws = sm ? sm->ws : nullptr;
+    if (!ws) {
+      sc_status st = get_workspace(device, stream, bytes, &ws, &ws_hold);
+      if (st != SC_OK) return st;
+    }
     a.part_o = static_cast<uint16_t *>(ws);
-    a.part_lse = reinterpret_cast<float *>(a.part_o + rows * head_dim);
+    a.part_lse = reinterpret_cast<float *>(static_cast<char *>(ws) + lse_off);
+    if (sm && sm->prev_ws) {
+      a.dm_part_o = static_cast<const uint16_t *>(sm->prev_ws);
+      a.dm_part_lse = reinterpret_cast<const float *>(static_cast<const char *>(sm->prev_ws) + lse_off);
+      a.dm_out = static_cast<uint16_t *>(sm->prev_out);
+      a.dm_counter = sm->prev_counter;
+      a.dm_max_splits = plan.max_splits;
+    }
   }
   if (plan.paged) {
     if (!rc.pool || !rc.ids || !rc.pool->rc_base)
@@ -527,11 +556,34 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
   hipError_t e = launch_attn_fwd(a, head_dim, plan.n_items, stream);
   if (e != hipSuccess) return fail_hip(e, "attn_fwd launch");
   if (after_fwd) SC_HIP(hipEventRecord(after_fwd, stream));
-  if (plan.max_splits > 1) {
+  if (plan.max_splits > 1 && !sm) {
     e = launch_attn_merge(a, head_dim, stream);
     if (e != hipSuccess) return fail_hip(e, "attn_merge launch");
   }
   return SC_OK;
+}
+
+// The merge kernel alone over a plan-sized workspace (the last layer of a
+// stack whose merges are deferred).
+sc_status run_merge(const AttnPlan &plan, const void *ws, void *out, int hq, int hkv, int head_dim, int dtype,
+                    hipStream_t stream) {
+  if (plan.n_items == 0 || plan.max_splits <= 1) return SC_OK;
+  size_t lse_off = 0;
+  plan_ws_bytes(plan, hq, head_dim, &lse_off);
+  AttnArgs a{};
+  a.out = static_cast<uint16_t *>(out);
+  a.seqs = plan.d_seqs;
+  a.n_seqs = (int32_t)plan.seqs.size();
+  a.total_q = (int32_t)plan.total_q;
+  a.n_q_heads = hq;
+  a.n_kv_heads = hkv;
+  a.group = plan.group;
+  a.rows_q = plan.rows_q;
+  a.dtype = dtype;
+  a.part_o = static_cast<uint16_t *>(const_cast<void *>(ws));
+  a.part_lse = reinterpret_cast<float *>(static_cast<char *>(const_cast<void *>(ws)) + lse_off);
+  hipError_t e = launch_attn_merge(a, head_dim, stream);
+  return e == hipSuccess ? SC_OK : fail_hip(e, "attn_merge launch");
 }
 
 sc_status check_heads(int hq, int hkv, int head_dim) {
@@ -1618,6 +1670,46 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   hipStream_t caller_cs = (hipStream_t)compute_stream;
   hipStream_t cs = ss ? ss->attn : caller_cs;
   hipStream_t xs = ss ? ss->copy : (hipStream_t)copy_stream;
+  // Split-key merges are deferred when every layer runs one plan with key
+  // splits: the forward kernel of layer l merges layer l-1's partials
+  // (spread over its workgroups, before their own items; in the overlapped
+  // stack while they wait for their slot), and one merge kernel follows the
+  // last layer.  That saves a merge launch per layer and its ~6 us on the
+  // 8B shape.  Partials alternate between two halves of one workspace,
+  // held for the whole enqueue.
+  const bool defer_merge = n_chunks == 1 && plans[0]->max_splits > 1;
+  std::unique_lock<std::mutex> dws_hold;
+  char *dws = nullptr;
+  size_t dws_half = 0;
+  uint32_t *claims = nullptr;             // one claim counter per layer
+  if (defer_merge) {
+    dws_half = (plan_ws_bytes(*plans[0], n_q_heads, d.head_dim) + 255) & ~(size_t)255;
+    const size_t claim_bytes = ((size_t)n_layers * sizeof(uint32_t) + 255) & ~(size_t)255;
+    void *w = nullptr;
+    st = get_workspace(d.device, cs, 2 * dws_half + claim_bytes, &w, &dws_hold);
+    if (st != SC_OK) return st;
+    dws = static_cast<char *>(w);
+    claims = reinterpret_cast<uint32_t *>(dws + 2 * dws_half);
+    // Zeroed by a fill kernel on the attention stream, before any forward
+    // kernel of this stack.
+    hipError_t e = launch_kv_fill(claims, claim_bytes, 0, cs);
+    if (e != hipSuccess) return fail_hip(e, "claim counter reset");
+  }
+  auto stack_merge = [&](int l) {
+    StackMerge m;
+    m.ws = dws + (size_t)(l & 1) * dws_half;
+    if (l > 0) {
+      m.prev_ws = dws + (size_t)((l - 1) & 1) * dws_half;
+      m.prev_out = out_per_layer[l - 1];
+      m.prev_counter = claims + (l - 1);
+    }
+    return m;
+  };
+  auto last_merge = [&]() -> sc_status {
+    if (!defer_merge) return SC_OK;
+    return run_merge(*plans[0], dws + (size_t)((n_layers - 1) & 1) * dws_half, out_per_layer[n_layers - 1],
+                     n_q_heads, d.n_kv_heads, d.head_dim, d.dtype, cs);
+  };
   // The first chunk waits for the slot; the slot-free event follows the
   // last chunk's forward kernel.
   // A forced time-out (tests of the failure path) waits for a count the
@@ -1627,11 +1719,13 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   auto attn = [&](int l, const sc_active &slot, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
                   hipEvent_t after_fwd = nullptr, uint64_t *done_counter = nullptr) {
     RcView rc{pool, l, table->d_rc_ids};
+    const StackMerge sm = defer_merge ? stack_merge(l) : StackMerge();
     for (int c = 0; c < n_chunks; ++c) {
       sc_status r = run_attention(d.device, *plans[c], q_per_layer[l], slot.k, slot.v, out_per_layer[l], nullptr,
                                   n_q_heads, d.n_kv_heads, d.head_dim, d.dtype, scale, cs,
                                   c == 0 ? ready_flag : nullptr, ready_value + (ready_flag ? never : 0),
-                                  c == n_chunks - 1 ? after_fwd : nullptr, rc, spin_limit, done_counter);
+                                  c == n_chunks - 1 ? after_fwd : nullptr, rc, spin_limit, done_counter,
+                                  defer_merge ? &sm : nullptr);
       if (r != SC_OK) return r;
     }
     return SC_OK;
@@ -1642,7 +1736,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
       st = attn(l, slots[l & 1]);
       if (st != SC_OK) return st;
     }
-    return SC_OK;
+    return last_merge();
   }
   // Debug poisoning: NaN patterns over a slot's K and V before it is refilled.
   auto poison_slot = [&](const sc_active &slot, hipStream_t s) -> sc_status {
@@ -1660,7 +1754,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
       if ((st = attn(l, slots[0])) != SC_OK) return st;
       if (do_st && (st = do_store(pool, table, l, knew_per_layer[l], vnew_per_layer[l], cs)) != SC_OK) return st;
     }
-    return SC_OK;
+    return last_merge();
   }
 
   // Overlapped.  Attention of layer l waits on the device for the copy
@@ -1737,6 +1831,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   const uint64_t never_f = never_free ? (uint64_t)1 << 40 : 0;
   const int gate_spin = never_free ? kAttnTestSpinLimit : kAttnReadySpinLimit;
   auto body = [&]() -> sc_status {
+    sc_status r0;
     if (device_wait && tw->last_overlap_recorded) SC_HIP(hipStreamWaitEvent(caller_cs, tw->last_overlap, 0));
     // The done count starts from zero for this stack; the copy stream
     // starts after this write (event below).
@@ -1781,6 +1876,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
       SC_HIP(hipStreamWaitEvent(cs, ready[s], 0));
       if ((r = attn(l, slots[s], nullptr, 0, free_[s])) != SC_OK) return r;
     }
+    if ((r0 = last_merge()) != SC_OK) return r0;
     // The caller's compute stream ends after the last attention and store.
     SC_HIP(hipEventRecord(start, xs));
     SC_HIP(hipStreamWaitEvent(caller_cs, start, 0));

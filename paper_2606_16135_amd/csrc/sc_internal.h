@@ -170,6 +170,18 @@ struct AttnArgs {
   int32_t imp_tiles;      // query tiles per KV head
   int32_t imp_splits;     // key splits per query tile (S)
   int32_t imp_per_xcd;    // items per XCD (grid = 8 * imp_per_xcd)
+  // Optional deferred merge (layer stack, same plan for every layer): once
+  // its own item is done, a workgroup claims chunks of rows of the previous
+  // layer's split partials (dm_part_o, dm_part_lse, laid out like part_o /
+  // part_lse; at most dm_max_splits splits per row) from *dm_counter (zero
+  // before the launch) and merges them into dm_out exactly as
+  // attn_merge_kernel would, until every chunk is claimed; workgroups that
+  // finish early take more.  dm_out == nullptr: none.
+  const uint16_t *dm_part_o;
+  const float *dm_part_lse;
+  uint16_t *dm_out;
+  uint32_t *dm_counter;
+  int32_t dm_max_splits;
 };
 
 // Tile geometry the planner and the kernel agree on.
