@@ -13,9 +13,13 @@
 // workgroups (split-key): each writes a normalised partial output (in the
 // element type; it is a convex combination of V rows) and
 // its log-sum-exp, and attn_merge_kernel combines them exactly
-// (o = sum_s exp(lse_s - lse) o_s).  The merge is a separate launch: merging
-// in the last-arriving workgroup would need device-scope fences, whose L2
-// write-back / invalidate stalls the other workgroups streaming K/V.
+// (o = sum_s exp(lse_s - lse) o_s).  The merge is not done by the
+// last-arriving split's workgroup: that would need device-scope fences,
+// whose L2 write-back / invalidate stalls the other workgroups streaming
+// K/V.  A single call launches the merge kernel after the forward kernel;
+// in a layer stack the forward kernel of the next layer does it, each
+// workgroup claiming chunks of rows once its own item is done (the launch
+// boundary orders the partials' writes before those reads).
 //
 // q, K, V and out are bf16 or IEEE fp16 (Elem<DT> below); everything else
 // is the same for both types.
