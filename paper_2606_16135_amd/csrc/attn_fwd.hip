@@ -88,6 +88,21 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
+// A record of 32-bit fields read through the constant address space: the
+// host writes work items and sequence records before the launch and nothing
+// writes them during it, so a uniform index gives scalar loads.
+template <class T>
+__device__ __forceinline__ T load_const(const T *p) {
+  static_assert(sizeof(T) % 4 == 0, "32-bit fields");
+  const __attribute__((address_space(4))) int32_t *q = (const __attribute__((address_space(4))) int32_t *)p;
+  int32_t v[sizeof(T) / 4];
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 4); ++i) v[i] = q[i];
+  T r;
+  __builtin_memcpy(&r, v, sizeof(T));
+  return r;
+}
+
 constexpr int kThreads = 512;            // 8 waves, 2 per SIMD
 constexpr int KT = kAttnKeyTile;
 static_assert(kAttnRows == 8 * 32, "eight waves of 32 rows");
@@ -342,7 +357,8 @@ struct WaveState {
   u32x4 qf[D / 16];   // raw 16-bit patterns
   f32x16 oacc[D / 32];
   f32x16 s[2];        // raw scores of the even / odd tiles
-  u32x4 pf_prev[2];   // P(j-1) for the PV product
+  u32x4 pf_prev[2];   // P(j-1) for the PV product (head_dim 64 loop)
+  u32x4 pfb[2][2];    // P of the even / odd tiles (head_dim 128 loop: no copy per tile)
   float m_run;        // reference max of sl2 * s, log2 units (0 until a key is visible)
   float l_run;        // this lane's share of the denominator
 };
@@ -402,7 +418,9 @@ template <int D, int DT, bool kPaged>
 __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi, uint16_t *smem) {
   using G_ = Geo<D>;
   constexpr int NCH = G_::kChunksPerThread;
-  const SeqDesc sd = a.seqs != nullptr ? a.seqs[wi.seq] : a.seq0;
+  // Scalar loads (see load_const), so the key-range and address arithmetic
+  // built from the record stays in scalar registers.
+  const SeqDesc sd = a.seqs != nullptr ? load_const(a.seqs + wi.seq) : a.seq0;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -558,9 +576,12 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
                                               (int64_t)wi.kvh * D);
         range = rows > 0 ? ((rows - 1) * row_bytes + 2 * D) : 0;
       } else {
-        const uint32_t off = (uint32_t)t * tile_bytes + (uint32_t)(my_row * row_bytes);
+        // 64-bit signed arithmetic with a max (scalar instructions); a
+        // saturating 32-bit subtract would be a vector instruction.
+        const int64_t off = (int64_t)t * tile_bytes + (int64_t)my_row * row_bytes;
         base = reinterpret_cast<const char *>(kV ? vb : kb) + off;
-        range = (int)(range_bytes > off ? range_bytes - off : 0u);
+        const int64_t left = (int64_t)range_bytes - off;
+        range = (int)(left > 0 ? left : 0);
       }
       const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<char *>(base), (short)0, __builtin_amdgcn_readfirstlane(range), 0x00020000);
@@ -575,7 +596,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
         s = Elem<DT>::mfma(*reinterpret_cast<const u32x4 *>(slot + k_rd[k]), w.qf[k], s);
     };
     // O^T += V^T . P^T, operands as in pv_tile.
-    auto pv = [&](const unsigned char *slot) {
+    auto pv = [&](const unsigned char *slot, const u32x4 (&pfp)[2]) {
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -588,7 +609,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
           vw[1] = __builtin_bit_cast(u32x2, lo)[1];
           vw[2] = __builtin_bit_cast(u32x2, hi)[0];
           vw[3] = __builtin_bit_cast(u32x2, hi)[1];
-          w.oacc[c] = Elem<DT>::mfma(vw, w.pf_prev[t], w.oacc[c]);
+          w.oacc[c] = Elem<DT>::mfma(vw, pfp[t], w.oacc[c]);
         }
     };
 
@@ -657,8 +678,10 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
           return vw;
         };
         u32x4 op[16];
-        u32x4 pf[2];
-        float r2[2] = {0.f, 0.f};
+        // Probabilities of tile j go to pfb[j mod 2]; PV(j-1) reads the other.
+        u32x4 (&pf)[2] = w.pfb[PAR];
+        const u32x4 (&pfp)[2] = w.pfb[PAR ^ 1];
+        float rsum = 0.f;                 // one pair-sum chain over the tile
         float x_prev = 0.f;
         op[0] = operand(0);
         if constexpr (!kFirst) op[1] = operand(1);
@@ -672,13 +695,13 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
           if ((i & 1) == 0) {
             sn = Elem<DT>::mfma(op[i], w.qf[i >> 1], i == 0 ? f32x16{} : sn);
           } else if constexpr (!kFirst) {
-            w.oacc[(i >> 1) & 3] = Elem<DT>::mfma(op[i], w.pf_prev[i >> 3], w.oacc[(i >> 1) & 3]);
+            w.oacc[(i >> 1) & 3] = Elem<DT>::mfma(op[i], pfp[i >> 3], w.oacc[(i >> 1) & 3]);
           }
           const float x = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[i], sl2, mneg));
           if (i & 1) {
             const uint32_t pk = Elem<DT>::pack(x_prev, x);
             pf[i >> 3][(i & 7) >> 1] = pk;
-            r2[i >> 3] = Elem<DT>::add_pair(pk, r2[i >> 3]);
+            rsum = Elem<DT>::add_pair(pk, rsum);
           }
           x_prev = x;
           if constexpr (PAR == 0) {
@@ -691,11 +714,9 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
           }
           __builtin_amdgcn_sched_barrier(0);
         }
-        float rs = r2[0] + r2[1];
+        float rs = rsum;
         if (!kFirst && __builtin_amdgcn_ballot_w64(!(rs <= Elem<DT>::kSumLimit))) rs = settle_max<D, DT>(w, sc, pf, sl2);
         w.l_run += rs;
-        w.pf_prev[0] = pf[0];
-        w.pf_prev[1] = pf[1];
         if constexpr (PAR == 1) {
           dma_barrier<4 * (A - 1)>();
           bv0 = bk0;
@@ -720,7 +741,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
       // PV of the last tile; its V landed before the last pair's barrier.
       const int last = (n - 1) % R;
       static_for<0, R>([&](auto S) {
-        if (last == decltype(S)::value) pv(dma_v_slot<decltype(S)::value>());
+        constexpr int kS = decltype(S)::value;
+        if (last == kS) pv(dma_v_slot<kS>(), w.pfb[kS & 1]);   // R is even: kS has the parity of n-1
       });
       // Loads of tiles past the end may still be in flight.
       dma_wait_all();
@@ -1057,7 +1079,7 @@ __device__ __forceinline__ WorkItem implicit_item(const AttnArgs &a, int w) {
 
 template <int D, int DT>
 __device__ __forceinline__ void attn_fwd_body(const AttnArgs &a) {
-  const WorkItem wi = a.items != nullptr ? a.items[blockIdx.x] : implicit_item(a, blockIdx.x);
+  const WorkItem wi = a.items != nullptr ? load_const(a.items + blockIdx.x) : implicit_item(a, blockIdx.x);
   if (wi.seq < 0) {
     // Padding slot (XCD placement): no K/V to read, but it counts as done
     // like every other workgroup of the launch.
