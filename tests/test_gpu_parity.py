@@ -248,6 +248,55 @@ def test_layer_stack_matches_oracle(name, mode):
         dp.close()
 
 
+# Stacks whose plans split keys: each layer's split partials are merged by
+# the next layer's forward kernel (claimed in chunks by the workgroups that
+# finish first), the last layer's by a merge kernel.  (P, N, Hq, Hkv, D,
+# layers, which merge path: at most four splits per row -> four rows per
+# lane group, more -> one.)
+DEFERRED = {
+    "nr4_multi_seq": ([2500, 800, 3000], [200, 100, 250], 32, 8, 128, 3, "le4"),
+    "nr1_multi_seq": ([3000, 5000, 1200], [40, 25, 60], 32, 8, 128, 2, "gt4"),
+    "one_layer": ([1500], [500], 32, 8, 128, 1, "le4"),
+    "d64_nr4": ([2000, 1500], [300, 200], 32, 8, 64, 2, "le4"),
+    "d64_nr1": ([3000, 1000], [300, 150], 16, 4, 64, 2, "gt4"),
+}
+
+
+@pytest.mark.parametrize("mode", ["overlap", "serial"])
+@pytest.mark.parametrize("name", list(DEFERRED))
+def test_stack_deferred_merge_matches_oracle(name, mode):
+    """Every layer of a stack with key splits against the oracle: the
+    deferred merges (one, several and no sequences split per plan, at most
+    and more than four splits per row, head_dim 64 and 128, a single
+    layer)."""
+    sc = require_gpu()
+    import torch
+    P, N, hq, hkv, D, L, path = DEFERRED[name]
+    _, splits = sc.sc_attn_plan_query(P, N, hq, hkv)
+    assert (max(splits) <= 4) == (path == "le4") and max(splits) > 1, splits
+    wl = W.small_workload(250 + list(DEFERRED).index(name), P, N, L, hq, hkv, D)
+    pool_u16 = W.pool_numpy(wl)
+    dp = DevicePool(sc, wl, pool_u16)
+    try:
+        ins = [W.layer_inputs_numpy(wl, l) for l in range(L)]
+        dev = [[from_u16(x, "cuda", wl.dtype) for x in t] for t in ins]
+        outs = [torch.full((wl.total_q, hq, D), float("nan"), dtype=W.torch_dtype(wl), device="cuda")
+                for _ in range(L)]
+        slots = [new_active(sc, wl) for _ in range(2)]
+        copy = torch.cuda.Stream()
+        flags = sc.SC_STACK_OVERLAP if mode == "overlap" else sc.SC_STACK_SERIAL
+        sc.sc_prefill_stack(dp.handle, dp.table, [d[0].data_ptr() for d in dev], [d[1].data_ptr() for d in dev],
+                            [d[2].data_ptr() for d in dev], [o.data_ptr() for o in outs], [s[2] for s in slots], hq,
+                            flags, 0.0, torch.cuda.current_stream().cuda_stream, copy.cuda_stream)
+        torch.cuda.synchronize()
+        for l in range(L):
+            q, kn, vn = ins[l]
+            *_, o_ref, _ = _oracle_layer(wl, pool_u16, l, q, kn, vn)
+            compare_attention(to_u16(outs[l]), o_ref, f"{name} {mode} layer {l}", wl.dtype)
+    finally:
+        dp.close()
+
+
 def test_overlapped_stacks_on_one_table_from_two_streams():
     """Two overlapped stacks on the same table, enqueued back to back on two
     different caller streams with their own slots and outputs: they share
