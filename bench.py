@@ -48,17 +48,18 @@ MFMA_PEAK_TFLOPS = 2500.0        # dense bf16 (and fp16) MFMA, MI355X
 MALL_BYTES = 256 << 20
 ROTATE_BYTES = 512 << 20         # destination buffers the standalone fetch cycles through
 
-# HBM bytes of one attention call (forward + merge kernels) from two
+# HBM bytes of one layer's attention (forward kernel, plus the merge kernels
+# spread over the layers when a stack defers its merges) from two
 # rocprofv3 --pmc passes (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0: the factors
 # that map the same counters to a plain 256 MiB device copy), per workload,
 # with the hash of the attention source they were taken on; a stale entry
 # (the source changed since) is reported as null.
 PMC_TRAFFIC = {
-    "llama3-8b-P8192-N512": (80656766, "f96b56d72da41fde"),
-    "llama3-8b-batch16-varlen": (708219721, "f96b56d72da41fde"),
-    "qwen-14b-P32768-N1024": (362526163, "f96b56d72da41fde"),
-    "llama3-8b-P131072-N2048-hosttier": (1190410310, "f96b56d72da41fde"),
-    "llama3-8b-P8192-N512-rc0.5": (80142154, "f96b56d72da41fde"),
+    "llama3-8b-P8192-N512": (80550764, "8f0e9368f4fe3f67"),
+    "llama3-8b-batch16-varlen": (707568354, "8f0e9368f4fe3f67"),
+    "qwen-14b-P32768-N1024": (364441825, "8f0e9368f4fe3f67"),
+    "llama3-8b-P131072-N2048-hosttier": (1191218842, "8f0e9368f4fe3f67"),
+    "llama3-8b-P8192-N512-rc0.5": (80027354, "8f0e9368f4fe3f67"),
 }
 
 
@@ -260,7 +261,11 @@ def run_workload(args, cfg, torch, sc, W, DevicePool, with_cpu, turn=None, rc_fr
     rot_slots = slots + [s[2] for s in rot]
 
     if args.only is not None:
-        return profile_only(args, wl, dp, sc, torch, stack, rot_slots, compute, L)
+        def fill_other_slot():
+            l = max(0, L - 2)
+            sc.sc_fetch_layer_kv(dp.handle, dp.table, l, slots[1], compute.cuda_stream)
+            sc.sc_append_new_kv(dp.handle, dp.table, kp[l], vp[l], slots[1], compute.cuda_stream)
+        return profile_only(args, wl, dp, sc, torch, stack, rot_slots, compute, L, fill_other_slot)
 
     # ---- headline: the overlapped stack, wall clock -------------------------
     print(f"bench.py: {wl.name}: timing", file=sys.stderr, flush=True)
@@ -445,7 +450,7 @@ def host_tier_detail(args, wl, dp, sc, torch, timed, rot_slots, copy, t_fetch, d
     return out
 
 
-def profile_only(args, wl, dp, sc, torch, stack, rot_slots, compute, L):
+def profile_only(args, wl, dp, sc, torch, stack, rot_slots, compute, L, fill_other_slot):
     """Profiling aid: one op of the path over every layer, warmup then timed
     steps; prints its per-layer time."""
     copy_src = copy_dst = None
@@ -465,10 +470,14 @@ def profile_only(args, wl, dp, sc, torch, stack, rot_slots, compute, L):
         else:
             for _ in range(L):
                 copy_dst.copy_(copy_src)
-    # Fill both slots in serial mode: a profiler that serialises dispatches
-    # would otherwise hold the overlapped stack's attention, which waits on
-    # the device for the copy stream, until its wait gives up.
+    # Fill both slots without the overlapped stack: a profiler that
+    # serialises dispatches would otherwise hold the overlapped stack's
+    # attention, which waits on the device for the copy stream, until its
+    # wait gives up.  The serial stack leaves layer L-1 in slot 0; slot 1 gets
+    # layer L-2 (or 0), so every attention-only layer reads a real layer's
+    # K/V rather than whatever the slot's memory held.
     stack(sc.SC_STACK_SERIAL)
+    fill_other_slot()
     for _ in range(args.warmup):
         run_op()
     torch.cuda.synchronize()
