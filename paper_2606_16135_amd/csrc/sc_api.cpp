@@ -644,7 +644,9 @@ sc_status table_plan(sc_table *t, int hq, AttnPlan **out, int slots = 0, int chu
 // stream restricted to kHostFetchCus CUs and an attention stream restricted
 // to the others.  CU mask bit i selects logical CU i; logical CUs are
 // interleaved across the XCDs, so the low bits take the same number of CUs
-// from every XCD.
+// from every XCD (on MI355X the low 16 bits are two CUs of each of the 8
+// XCDs, as the hardware's XCC_ID and HW_ID registers read by workgroups of
+// such a stream show).  The streams live as long as the process.
 // ---------------------------------------------------------------------------
 constexpr int kHostFetchCus = 16;
 
