@@ -327,6 +327,13 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
  * stacks on one table share its slot counter, so the library runs them one
  * after another on the device even when they are enqueued from different
  * threads or caller streams (each starts after the previous one ended).
+ * When the attention plan splits key ranges, layer l's split partials are
+ * merged by the forward kernel of layer l+1 (its workgroups take chunks of
+ * rows once their own work items are done) and the last layer's by one
+ * merge kernel; out_per_layer[l] is therefore complete only when the whole
+ * stack is, which is when the compute stream reaches the end of the stack.
+ * The partials use the library's split-key workspace of the attention
+ * stream (two layers' worth while the stack is enqueued).
  * Arrays of per-layer device pointers (host arrays of length n_layers):
  *   q_per_layer, knew_per_layer, vnew_per_layer, out_per_layer.
  * flags: SC_STACK_OVERLAP (two streams, two slots), SC_STACK_SERIAL
