@@ -492,9 +492,11 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
   // workgroup: an acquire here would invalidate the XCD's L2 under the
   // other workgroups' K/V).  No stale K/V lines can be cached: this kernel's
   // dispatch invalidated the caches after the last reader of the slot (two
-  // layers back, same stream) had finished, nothing reads the slot until the
-  // flag is set, and the copy kernels' completion wrote their data back
-  // before the flag was written.
+  // layers back, same stream) had finished, the only kernel that touches the
+  // slot after that is the copy kernel, whose completion wrote its data back
+  // before the flag was written, and nothing reads the slot until the flag
+  // is set.  A stack that also writes the slot from another kernel after
+  // this dispatch (debug poisoning) asks for the acquire (ready_acquire).
   bool timed_out = false;
   if (a.ready_flag != nullptr) {
     __shared__ int s_timeout;
@@ -508,6 +510,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
         }
         __builtin_amdgcn_s_sleep(8);
       }
+      if (a.ready_acquire && !late) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       s_timeout = late;
     }
     __syncthreads();

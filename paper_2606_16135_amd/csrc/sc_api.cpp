@@ -488,7 +488,7 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
                         hipStream_t stream, const uint64_t *ready_flag = nullptr, uint64_t ready_value = 0,
                         hipEvent_t after_fwd = nullptr, const RcView &rc = RcView(),
                         int spin_limit = kAttnReadySpinLimit, uint64_t *done_counter = nullptr,
-                        const StackMerge *sm = nullptr) {
+                        const StackMerge *sm = nullptr, bool ready_acquire = false) {
   if (plan.n_items == 0) return SC_OK;
   // The kernel addresses one sequence's rows of one KV head with 32-bit
   // byte offsets.
@@ -551,6 +551,7 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
     a.ready_value = ready_value;
     a.ready_timeout = reinterpret_cast<uint32_t *>(const_cast<uint64_t *>(ready_flag + 1));
     a.ready_spin_limit = spin_limit;
+    a.ready_acquire = ready_acquire ? 1 : 0;
   }
   a.done_counter = done_counter;
   hipError_t e = launch_attn_fwd(a, head_dim, plan.n_items, stream);
@@ -1727,7 +1728,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
                                   n_q_heads, d.n_kv_heads, d.head_dim, d.dtype, scale, cs,
                                   c == 0 ? ready_flag : nullptr, ready_value + (ready_flag ? never : 0),
                                   c == n_chunks - 1 ? after_fwd : nullptr, rc, spin_limit, done_counter,
-                                  defer_merge ? &sm : nullptr);
+                                  defer_merge ? &sm : nullptr, poison);
       if (r != SC_OK) return r;
     }
     return SC_OK;

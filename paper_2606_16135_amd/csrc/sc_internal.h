@@ -145,6 +145,12 @@ struct AttnArgs {
   uint64_t ready_value;
   uint32_t *ready_timeout;
   int32_t ready_spin_limit;
+  // Nonzero: once the flag is seen, an agent-scope acquire (invalidates
+  // this XCD's L2) before any K/V read.  For stacks in which another kernel
+  // writes the slot after this kernel's dispatch (the debug poisoning):
+  // that kernel's lines may stay valid in this XCD's L2 while the copy
+  // kernel's newer data was written from another XCD.
+  int32_t ready_acquire;
   // Optional: every workgroup adds 1 to *done_counter once it has finished
   // reading K/V (after its last key tile; timed-out and empty workgroups
   // too), so that the next refill of the slot can wait on the device.
