@@ -36,9 +36,12 @@
 // rounded to bf16, for a fixed permutation of the 16 keys of each MFMA step.
 // V^T operands come from the row-major V tile through LDS transpose reads
 // (ds_read_b64_tr_b16: in each 16-lane group, lanes 4r..4r+3 read 4 dims
-// each of key r and lane j gets dim j of the 4 keys).  Row sums use
-// v_dot2c_f32_bf16 on the packed bf16 probabilities, i.e. the same rounded
-// values the PV product consumes.
+// each of key r and lane j gets dim j of the 4 keys).  With head_dim 128
+// the row sum adds the fp32 probabilities before rounding, in two chains
+// (two v_add_f32 per pair measured 1-2% faster than one v_dot2c_f32_bf16
+// on the packed pair); the head_dim 64 loop and the rare re-reference path
+// sum the packed bf16 values with v_dot2c_f32_bf16.  Either sum differs
+// from the other by the rounding of P, far below the tolerance.
 //
 // Software pipeline.  A single wave issues MFMAs at half the SIMD's matrix
 // rate and VALU ops at half its vector rate, so each wave interleaves both:
@@ -666,8 +669,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
         // c = (i / 2) mod 4 of key half t = i / 8), and each step also
         // computes one probability of tile j: one MFMA and a sixteenth of
         // the softmax per step, in this order (scheduling barriers keep the
-        // compiler from regrouping them).  Operands are read from LDS two
-        // steps ahead.
+        // compiler from regrouping them).  Operands are read from LDS three
+        // steps ahead (two measured ~0.5% slower, four no better).
         auto operand = [&](int i) -> u32x4 {
           if ((i & 1) == 0) return *reinterpret_cast<const u32x4 *>(ks + k_rd[i >> 1]);
           const unsigned char *p = vs + v_rd[(i >> 1) & 3] + 16 * (i >> 3) * DmaGeo::kRowBytes;
@@ -684,16 +687,19 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
         // Probabilities of tile j go to pfb[j mod 2]; PV(j-1) reads the other.
         u32x4 (&pf)[2] = w.pfb[PAR];
         const u32x4 (&pfp)[2] = w.pfb[PAR ^ 1];
-        float rsum = 0.f;                 // one pair-sum chain over the tile
+        float rsum0 = 0.f, rsum1 = 0.f;   // row sum: even and odd keys of the tile
         float x_prev = 0.f;
-        op[0] = operand(0);
-        if constexpr (!kFirst) op[1] = operand(1);
-        else op[1] = u32x4{0u, 0u, 0u, 0u};
+        constexpr int kAhead = 3;         // LDS operand reads, steps ahead of their MFMA
+#pragma unroll
+        for (int i = 0; i < kAhead; ++i) {
+          if (!kFirst || (i & 1) == 0) op[i] = operand(i);
+          else op[i] = u32x4{0u, 0u, 0u, 0u};
+        }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          if (i + 2 < 16) {
-            if (!kFirst || ((i + 2) & 1) == 0) op[i + 2] = operand(i + 2);
+          if (i + kAhead < 16) {
+            if (!kFirst || ((i + kAhead) & 1) == 0) op[i + kAhead] = operand(i + kAhead);
           }
           if ((i & 1) == 0) {
             sn = Elem<DT>::mfma(op[i], w.qf[i >> 1], i == 0 ? f32x16{} : sn);
@@ -704,7 +710,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
           if (i & 1) {
             const uint32_t pk = Elem<DT>::pack(x_prev, x);
             pf[i >> 3][(i & 7) >> 1] = pk;
-            rsum = Elem<DT>::add_pair(pk, rsum);
+            rsum0 += x_prev;
+            rsum1 += x;
           }
           x_prev = x;
           if constexpr (PAR == 0) {
@@ -717,7 +724,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
           }
           __builtin_amdgcn_sched_barrier(0);
         }
-        float rs = rsum;
+        float rs = rsum0 + rsum1;
         if (!kFirst && __builtin_amdgcn_ballot_w64(!(rs <= Elem<DT>::kSumLimit))) rs = settle_max<D, DT>(w, sc, pf, sl2);
         w.l_run += rs;
         if constexpr (PAR == 1) {
