@@ -473,7 +473,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
   const int64_t first_row = ((int64_t)sd.cu_k + k_begin) * kv_stride + (int64_t)wi.kvh * D;
   const uint16_t *const kb = a.k + first_row;
   const uint16_t *const vb = a.v + first_row;
-  // Byte counts fit in 31 bits (checked on the host).
+  // Byte counts, also of the tiles loaded past the end, fit in 31 bits
+  // (checked on the host).
   const uint32_t range_bytes = (uint32_t)((((int64_t)(k_end - k_begin) - 1) * kv_stride + D) * 2);
   const uint32_t tile_bytes = (uint32_t)(KT * kv_stride * 2);
   auto rsrc = [&](const uint16_t *base, int t) {
@@ -582,12 +583,14 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
                                               (int64_t)wi.kvh * D);
         range = rows > 0 ? ((rows - 1) * row_bytes + 2 * D) : 0;
       } else {
-        // 64-bit signed arithmetic with a max (scalar instructions); a
-        // saturating 32-bit subtract would be a vector instruction.
-        const int64_t off = (int64_t)t * tile_bytes + (int64_t)my_row * row_bytes;
+        // Signed 32-bit offsets (the host keeps a sequence's keys, plus the
+        // tiles loaded past its end, under 2^31 bytes): a subtract and a max
+        // on the scalar unit.  A 64-bit compare would be a vector
+        // instruction whose result the scalar select then waits for (~2%
+        // of the loop), as would a saturating unsigned subtract.
+        const int off = t * (int)tile_bytes + my_row * row_bytes;
         base = reinterpret_cast<const char *>(kV ? vb : kb) + off;
-        const int64_t left = (int64_t)range_bytes - off;
-        range = (int)(left > 0 ? left : 0);
+        range = max((int)range_bytes - off, 0);
       }
       const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<char *>(base), (short)0, __builtin_amdgcn_readfirstlane(range), 0x00020000);

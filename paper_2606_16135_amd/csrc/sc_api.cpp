@@ -493,9 +493,10 @@ sc_status run_attention(int device, const AttnPlan &plan, const void *q, const v
   // The kernel addresses one sequence's rows of one KV head with 32-bit
   // byte offsets.
   for (const SeqDesc &s : plan.seqs)
-    if (((int64_t)s.prefix + s.n_new) * hkv * head_dim * 2 >= ((int64_t)1 << 31))
-      return fail(SC_ERR_UNSUPPORTED, "sequence of %lld tokens x %d KV heads x head_dim %d exceeds 2 GiB of keys",
-                  (long long)s.prefix + s.n_new, hkv, head_dim);
+    if (!keys_fit_offsets((int64_t)s.prefix + s.n_new, hkv, head_dim))
+      return fail(SC_ERR_UNSUPPORTED,
+                  "sequence of %lld tokens x %d KV heads x head_dim %d exceeds 2 GiB of keys less %d tokens",
+                  (long long)s.prefix + s.n_new, hkv, head_dim, kKeyOffsetMarginTokens);
   AttnArgs a{};
   a.q = static_cast<const uint16_t *>(q);
   a.k = static_cast<const uint16_t *>(k);
@@ -1506,9 +1507,10 @@ sc_status sc_prefill_attn_noalloc(const void *q, const void *k_active, const voi
   if (!aligned16(q) || !aligned16(k_active) || !aligned16(v_active) || !aligned16(out))
     return fail(SC_ERR_INVALID, "q, k_active, v_active and out must be 16-byte aligned");
   if ((reinterpret_cast<uintptr_t>(lse) & 3) != 0) return fail(SC_ERR_INVALID, "lse must be 4-byte aligned");
-  if (((int64_t)prefix_len + new_len) * n_kv_heads * head_dim * 2 >= ((int64_t)1 << 31))
-    return fail(SC_ERR_UNSUPPORTED, "sequence of %lld tokens x %d KV heads x head_dim %d exceeds 2 GiB of keys",
-                (long long)prefix_len + new_len, n_kv_heads, head_dim);
+  if (!keys_fit_offsets((int64_t)prefix_len + new_len, n_kv_heads, head_dim))
+    return fail(SC_ERR_UNSUPPORTED,
+                "sequence of %lld tokens x %d KV heads x head_dim %d exceeds 2 GiB of keys less %d tokens",
+                (long long)prefix_len + new_len, n_kv_heads, head_dim, kKeyOffsetMarginTokens);
   int device = 0;
   SC_HIP(hipGetDevice(&device));
   int cus = 0;

@@ -193,6 +193,14 @@ struct AttnArgs {
 // Tile geometry the planner and the kernel agree on.
 constexpr int kAttnRows = 256;   // (query, head) rows per workgroup
 constexpr int kAttnKeyTile = 32; // keys per LDS tile
+// The attention kernel addresses one sequence's key rows (all KV heads)
+// with signed 32-bit byte offsets, including the loads of up to a few tiles
+// past the last one (which the buffer range turns into zeros): a sequence
+// must fit in 2 GiB of keys less this many tokens.
+constexpr int kKeyOffsetMarginTokens = 8 * kAttnKeyTile;
+inline bool keys_fit_offsets(int64_t tokens, int n_kv_heads, int head_dim) {
+  return (tokens + kKeyOffsetMarginTokens) * n_kv_heads * head_dim * 2 < ((int64_t)1 << 31);
+}
 constexpr int kAttnMaxSplits = 16; // key splits per sequence (merge kernel bound)
 // Polls of the ready flag before an attention workgroup gives up (about a
 // second), and the limit a forced time-out uses.

@@ -438,6 +438,12 @@ def test_noalloc_argument_validation(sc):
         sc.sc_prefill_attn_noalloc(1, 1, 1, -1, 4, 8, 8, 128, 1)
     assert e.value.status == sc.SC_ERR_INVALID
     sc.sc_prefill_attn_noalloc(0, 0, 0, 5, 0, 8, 8, 128, 0)          # new_len == 0 is a no-op
+    # Key rows are addressed with signed 32-bit byte offsets, loads past the
+    # last tile included: 8 KV heads x 128 dims x 2 bytes = 2 KiB per token,
+    # so 2^20 tokens are 2 GiB, and the last 256 below that are refused too.
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn_noalloc(FAKE_BASE, FAKE_BASE, FAKE_BASE, (1 << 20) - 256 - 64, 64, 32, 8, 128, FAKE_BASE)
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED and "2 GiB" in str(e.value)
     with pytest.raises(sc.SwiftCacheError) as e:
         sc.sc_attn_noalloc_splits(4, 70000, 32, 8)                   # beyond the fixed buffers
     assert e.value.status == sc.SC_ERR_RANGE
