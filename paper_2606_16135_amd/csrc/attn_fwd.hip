@@ -477,11 +477,12 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
   // (checked on the host).
   const uint32_t range_bytes = (uint32_t)((((int64_t)(k_end - k_begin) - 1) * kv_stride + D) * 2);
   const uint32_t tile_bytes = (uint32_t)(KT * kv_stride * 2);
+  // Signed 32-bit offset arithmetic stays on the scalar unit (an unsigned
+  // saturating subtract would be a vector instruction plus a readfirstlane).
   auto rsrc = [&](const uint16_t *base, int t) {
-    const uint32_t off = (uint32_t)t * tile_bytes;
-    return __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<char *>(reinterpret_cast<const char *>(base) + off), (short)0,
-        __builtin_amdgcn_readfirstlane((int)(range_bytes > off ? range_bytes - off : 0u)), 0x00020000);
+    const int off = t * (int)tile_bytes;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(reinterpret_cast<const char *>(base) + off),
+                                             (short)0, max((int)range_bytes - off, 0), 0x00020000);
   };
 
   // First tile that needs the mask, the same for the whole workgroup: it
