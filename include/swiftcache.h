@@ -237,7 +237,11 @@ sc_status sc_append_new_kv(sc_pool *pool, const sc_table *table, const void *k_n
  * to nearest even.  The library may use a device workspace of its own for
  * split-key partials (one per device and stream, grown on demand).
  * Errors: SC_ERR_INVALID (null, negative length, n_q_heads not a multiple
- * of n_kv_heads), SC_ERR_UNSUPPORTED (head_dim not 64/128, group > 16).
+ * of n_kv_heads), SC_ERR_UNSUPPORTED (head_dim not 64/128, group > 16, or
+ * (prefix_len + new_len + 256) x n_kv_heads x head_dim x 2 bytes of keys
+ * reaching 2 GiB: key rows are addressed with signed 32-bit offsets, the
+ * loads of a few tiles past the last one included; the same bound applies
+ * to every sequence of the varlen, layer and stack calls).
  * new_len == 0 is a no-op.
  */
 sc_status sc_prefill_attn(const void *q, const void *k_active, const void *v_active,
