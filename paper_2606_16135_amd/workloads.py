@@ -366,3 +366,24 @@ def layer_inputs_torch(wl, layer, device, q_scale=1.0):
     v = torch.randn((t, wl.n_kv_heads, wl.head_dim), generator=g, device=device)
     td = torch_dtype(wl)
     return q.to(td), k.to(td), v.to(td)
+
+
+def long_sequence_torch(seed, prefix_len, new_len, n_q_heads, n_kv_heads, head_dim, device):
+    """One sequence's q[new_len][H_q][D] and active K, V[prefix_len +
+    new_len][H_kv][D] as bf16 device tensors of N(0,1) draws, for lengths
+    too large to draw on the host (the longest sequence the attention
+    accepts)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    t = prefix_len + new_len
+    q = torch.randn((new_len, n_q_heads, head_dim), generator=g, device=device).to(torch.bfloat16)
+    k = torch.empty((t, n_kv_heads, head_dim), dtype=torch.bfloat16, device=device)
+    v = torch.empty_like(k)
+    step = 1 << 16
+    for dst in (k, v):
+        for i in range(0, t, step):
+            n = min(step, t - i)
+            dst[i:i + n] = torch.randn((n, n_kv_heads, head_dim), generator=g, device=device).to(torch.bfloat16)
+    return q, k, v
+

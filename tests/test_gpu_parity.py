@@ -434,6 +434,51 @@ def test_sequence_beyond_32_bit_key_offsets_is_rejected():
     assert e.value.status == sc.SC_ERR_UNSUPPORTED
 
 
+def test_longest_accepted_sequence_matches_oracle():
+    """The longest sequence the kernel's signed 32-bit key offsets admit at
+    8 KV heads x 128 dims: 2 GiB of keys less 256 tokens (2^20 - 257
+    tokens), whose last tiles and the loads past them sit just below 2^31
+    bytes.  With 4096 new tokens the plan does not split keys, so each work
+    item addresses the whole key range from one base.  Sampled rows (first,
+    middle and last new token of a head in the first and the last KV group)
+    against the oracle, lse included; one more token is refused before any
+    launch."""
+    sc = require_gpu()
+    import torch
+    hq, hkv, d, n = 32, 8, 128, 4096
+    tokens = (1 << 31) // (hkv * d * 2) - 256 - 1
+    p = tokens - n
+    items, splits = sc.sc_attn_plan_query([p], [n], hq, hkv)
+    assert splits[0] == 1 and all(it[4] == 0 for it in items) and any(it[5] == tokens for it in items)
+    q, k, v = W.long_sequence_torch(301, p, n, hq, hkv, d, "cuda")
+    out = torch.full((n, hq, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lse = torch.full((hq, n), float("nan"), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    print(f"[longest] P={p} N={n} heads {hq}/{hkv} D={d}", flush=True)
+    sc.sc_prefill_attn(q.data_ptr(), k.data_ptr(), v.data_ptr(), p, n, hq, hkv, d, out.data_ptr(),
+                       lse=lse.data_ptr(), stream=stream)
+    torch.cuda.synchronize()
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_prefill_attn(q.data_ptr(), k.data_ptr(), v.data_ptr(), p + 1, n, hq, hkv, d, out.data_ptr(),
+                           stream=stream)
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED
+    o_bits = to_u16(out)
+    lse_h = lse.cpu().numpy()
+    group = hq // hkv
+    for h in (0, hq - 1):
+        g = h // group
+        # One KV head's keys and values, as a one-head problem for the oracle.
+        kg = bits_to_f64(to_u16(k[:, g:g + 1]))
+        vg = bits_to_f64(to_u16(v[:, g:g + 1]))
+        qh = bits_to_f64(to_u16(q[:, h:h + 1]))
+        rows = [(0, i, 0) for i in (0, n // 2, n - 1)]
+        o_ref, l_ref = oa.attention_rows(qh, kg, vg, [p], [n], rows)
+        for r, (_, i, _) in enumerate(rows):
+            compare_attention(o_bits[i, h][None, :], o_ref[r][None, :], f"longest row {i} head {h}")
+            assert abs(lse_h[h, i] - l_ref[r]) <= 2.0 ** -8 + 1e-4 * abs(l_ref[r]), (h, i, lse_h[h, i], l_ref[r])
+        del kg, vg
+
+
 def test_capacity_and_layer_errors():
     sc = require_gpu()
     wl = W.config(1)
