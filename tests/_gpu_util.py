@@ -51,7 +51,7 @@ def compare_attention(gpu_bits, ref, what="", dtype="bf16"):
 
 def oracle_workers():
     """Threads for the dense oracle at benchmark shapes: the host's cores in
-    this process's affinity, at most 16 (one GPU's share of a GPU machine)."""
+    this process's affinity, at most 16 (one GPU's share of a host with eight)."""
     import os
     return max(1, min(16, len(os.sched_getaffinity(0))))
 
