@@ -199,7 +199,8 @@ constexpr int kAttnKeyTile = 32; // keys per LDS tile
 // must fit in 2 GiB of keys less this many tokens.
 constexpr int kKeyOffsetMarginTokens = 8 * kAttnKeyTile;
 inline bool keys_fit_offsets(int64_t tokens, int n_kv_heads, int head_dim) {
-  return (tokens + kKeyOffsetMarginTokens) * n_kv_heads * head_dim * 2 < ((int64_t)1 << 31);
+  const int64_t row_bytes = (int64_t)n_kv_heads * head_dim * 2;   // head_dim is 64 or 128
+  return row_bytes > 0 && tokens >= 0 && tokens + kKeyOffsetMarginTokens <= (((int64_t)1 << 31) - 1) / row_bytes;
 }
 constexpr int kAttnMaxSplits = 16; // key splits per sequence (merge kernel bound)
 // Polls of the ready flag before an attention workgroup gives up (about a
