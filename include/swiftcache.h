@@ -323,8 +323,9 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
  * counter the copy stream advances (no stream-level wait in front of every
  * attention), and "wait until released" by a one-wave kernel on the copy
  * stream polling a count of finished attention workgroups, whenever a copy
- * workgroup can always run beside an attention workgroup; otherwise both are
- * stream event waits.  The device waits are bounded (about a second); an
+ * workgroup can always run beside an attention workgroup (and kernel
+ * dispatches are not serialised, see SC_STACK_EVENT_WAIT); otherwise both
+ * are stream event waits.  The device waits are bounded (about a second); an
  * attention workgroup that gives up writes NaN rows, and a copy whose wait
  * gave up writes NaN into the slot instead of K/V, so a lost dependency is
  * visible in the output, never silent.  Overlapped
@@ -362,6 +363,12 @@ sc_status sc_store_layer_kv(sc_pool *pool, const sc_table *table, int32_t layer,
  * up after a few hundred polls; those layers' slots are filled with NaN, so
  * their rows come out NaN (layers whose slot was refilled while they read it
  * may too), and sc_table_stack_status reports the time-out.
+ * SC_STACK_EVENT_WAIT (with SC_STACK_OVERLAP): both directions wait on
+ * stream events instead of on the device.  The library also chooses this
+ * by itself when the environment serialises kernel dispatches (the ROCm
+ * profiler collecting counters, AMD_SERIALIZE_KERNEL or HIP_LAUNCH_BLOCKING
+ * set): a device-side wait needs the copy kernel to run while the attention
+ * kernel holds the GPU.
  */
 enum {
   SC_STACK_OVERLAP = 0,
@@ -371,7 +378,8 @@ enum {
   SC_STACK_NO_STORE = 4,
   SC_STACK_TEST_NEVER_READY = 8,
   SC_STACK_DEBUG_POISON = 16,
-  SC_STACK_TEST_NEVER_FREE = 32
+  SC_STACK_TEST_NEVER_FREE = 32,
+  SC_STACK_EVENT_WAIT = 64
 };
 sc_status sc_prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers,
                            const void *const *q_per_layer, const void *const *knew_per_layer,
@@ -526,6 +534,15 @@ sc_status sc_scale_down(int64_t worker_blocks, int32_t worker_block_size, int64_
  * stack reports 0.
  */
 sc_status sc_table_stack_status(const sc_table *table, int32_t *timed_out, int32_t clear);
+
+/*
+ * Host-side introspection (no device work): *device_wait = 1 when
+ * sc_prefill_stack(table, ..., flags, ...) would order its copy and compute
+ * streams with the device-side slot waits, 0 when with stream events (see
+ * SC_STACK_EVENT_WAIT; serial and attention-only stacks have no such
+ * waits and report 0).  Errors: SC_ERR_INVALID (null).
+ */
+sc_status sc_stack_wait_kind(const sc_table *table, uint32_t flags, int32_t *device_wait);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char *sc_last_error(void);

@@ -697,6 +697,23 @@ constexpr int kCopyBesideAttn = 2;
 std::mutex g_reserve_mu;
 std::map<std::pair<int, int>, size_t> g_reserve;
 
+// Settings under which kernels of different streams do not run at the same
+// time: counter collection by the ROCm profiler serialises dispatches, and
+// the two runtime switches make every launch wait for the previous kernel.
+// The device-side slot waits need a copy kernel to run while an attention
+// kernel holds the GPU, so under these the stack waits on stream events.
+bool dispatch_is_serialised() {
+  static const bool serialised = [] {
+    auto on = [](const char *name) {
+      const char *e = std::getenv(name);
+      return e != nullptr && *e != '\0' && std::strcmp(e, "0") != 0 && std::strcmp(e, "false") != 0 &&
+             std::strcmp(e, "False") != 0;
+    };
+    return on("ROCPROF_COUNTER_COLLECTION") || on("AMD_SERIALIZE_KERNEL") || on("HIP_LAUNCH_BLOCKING");
+  }();
+  return serialised;
+}
+
 // Whether a copy workgroup can always start on a CU that holds an attention
 // workgroup (one wave per SIMD beside the attention's two; 512 VGPRs per
 // SIMD lane, allocated in steps of 8).  Only then may attention wait for the
@@ -706,6 +723,17 @@ bool copy_fits_beside_attention(int head_dim) {
   if (av <= 0 || cv <= 0) return false;
   auto alloc = [](int v) { return (v + 7) / 8 * 8; };
   return 2 * alloc(av) + alloc(cv) <= 512;
+}
+
+// Whether an sc_prefill_stack call with these flags orders its two streams
+// with device-side waits (else stream events): overlapped stacks only, not
+// when asked for events or when dispatches are serialised, and only when a
+// copy workgroup always fits beside attention or the copies run on CUs of
+// their own (a fetch that reaches into the host tier).
+bool stack_device_wait(const sc_table *t, uint32_t flags) {
+  if ((flags & SC_STACK_MODE_MASK) != SC_STACK_OVERLAP) return false;
+  if ((flags & SC_STACK_EVENT_WAIT) != 0 || dispatch_is_serialised()) return false;
+  return t->n_fetch_host > 0 || copy_fits_beside_attention(t->pool->desc.head_dim);
 }
 
 size_t copy_lds_reserve(int device, int head_dim) {
@@ -1367,6 +1395,14 @@ sc_status sc_table_totals(const sc_table *table, int64_t *total_q, int64_t *tota
   return SC_OK;
 }
 
+sc_status sc_stack_wait_kind(const sc_table *table, uint32_t flags, int32_t *device_wait) {
+  clear_error();
+  if (!table || !device_wait) return fail(SC_ERR_INVALID, "null argument");
+  sc::DeviceGuard guard(table->pool->desc.device);
+  *device_wait = sc::stack_device_wait(table, flags) ? 1 : 0;
+  return SC_OK;
+}
+
 sc_status sc_table_stack_status(const sc_table *table, int32_t *timed_out, int32_t clear) {
   clear_error();
   if (!table || !timed_out) return fail(SC_ERR_INVALID, "null argument");
@@ -1621,7 +1657,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   if (n_layers <= 0 || n_layers > pool->desc.n_layers)
     return fail(SC_ERR_RANGE, "n_layers %d outside [1, %d]", n_layers, pool->desc.n_layers);
   if (flags & ~(uint32_t)(SC_STACK_MODE_MASK | SC_STACK_NO_STORE | SC_STACK_TEST_NEVER_READY |
-                          SC_STACK_DEBUG_POISON | SC_STACK_TEST_NEVER_FREE))
+                          SC_STACK_DEBUG_POISON | SC_STACK_TEST_NEVER_FREE | SC_STACK_EVENT_WAIT))
     return fail(SC_ERR_INVALID, "unknown flags");
   const uint32_t mode = flags & SC_STACK_MODE_MASK;
   if (mode > SC_STACK_ATTN_ONLY) return fail(SC_ERR_INVALID, "unknown stack mode");
@@ -1634,6 +1670,8 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   const bool never_free = (flags & SC_STACK_TEST_NEVER_FREE) != 0;
   if (never_free && mode != SC_STACK_OVERLAP)
     return fail(SC_ERR_INVALID, "SC_STACK_TEST_NEVER_FREE needs SC_STACK_OVERLAP");
+  if ((flags & SC_STACK_EVENT_WAIT) && mode != SC_STACK_OVERLAP)
+    return fail(SC_ERR_INVALID, "SC_STACK_EVENT_WAIT needs SC_STACK_OVERLAP");
   const bool do_st = !(flags & SC_STACK_NO_STORE);
   const int n_slots = mode == SC_STACK_SERIAL ? 1 : 2;
   for (int s = 0; s < n_slots; ++s) {
@@ -1776,7 +1814,7 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   // which bounded short turns.  Without the device wait (a copy workgroup
   // could be kept off a CU by attention) the streams wait on events.
   // Disjoint CU sets (host tier) never block each other.
-  const bool device_wait = ss != nullptr || copy_fits_beside_attention(d.head_dim);
+  const bool device_wait = stack_device_wait(table, flags);
   if ((never_ready || never_free) && !device_wait)
     return fail(SC_ERR_UNSUPPORTED, "this stack waits on stream events; there is no device wait to time out");
   // One overlapped stack with a device-side wait at a time per table (they

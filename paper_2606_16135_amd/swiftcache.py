@@ -37,11 +37,12 @@ SC_STACK_NO_STORE = 4
 SC_STACK_TEST_NEVER_READY = 8
 SC_STACK_DEBUG_POISON = 16
 SC_STACK_TEST_NEVER_FREE = 32
+SC_STACK_EVENT_WAIT = 64
 
 EXPORTED = [
     "sc_pool_create", "sc_pool_destroy", "sc_pool_layout_get", "sc_table_create",
-    "sc_table_destroy", "sc_table_totals", "sc_table_stack_status", "sc_fetch_layer_kv", "sc_fetch_layer_kv_dma",
-    "sc_append_new_kv",
+    "sc_table_destroy", "sc_table_totals", "sc_table_stack_status", "sc_stack_wait_kind", "sc_fetch_layer_kv",
+    "sc_fetch_layer_kv_dma", "sc_append_new_kv",
     "sc_prefill_attn", "sc_prefill_attn_f16", "sc_prefill_attn_noalloc", "sc_attn_noalloc_splits",
     "sc_prefill_attn_varlen", "sc_store_layer_kv",
     "sc_prefill_stack", "sc_prefill_stack_chunked", "sc_attn_plan_query", "sc_pool_resize", "sc_plan_capacity", "sc_elastic_unit", "sc_scale_up",
@@ -112,6 +113,7 @@ def load():
         "sc_table_destroy": (None, [P]),
         "sc_table_totals": (I32, [P, ctypes.POINTER(I64), ctypes.POINTER(I64)]),
         "sc_table_stack_status": (I32, [P, ctypes.POINTER(I32), I32]),
+        "sc_stack_wait_kind": (I32, [P, ctypes.c_uint32, ctypes.POINTER(I32)]),
         "sc_fetch_layer_kv": (I32, [P, P, I32, ctypes.POINTER(sc_active), VP]),
         "sc_fetch_layer_kv_dma": (I32, [P, P, I32, ctypes.POINTER(sc_active), I32, VP]),
         "sc_append_new_kv": (I32, [P, P, VP, VP, ctypes.POINTER(sc_active), VP]),
@@ -197,6 +199,14 @@ def sc_table_totals(table):
     tq, tk = ctypes.c_int64(), ctypes.c_int64()
     _check(load().sc_table_totals(table, ctypes.byref(tq), ctypes.byref(tk)))
     return tq.value, tk.value
+
+
+def sc_stack_wait_kind(table, flags):
+    """True when an sc_prefill_stack call with these flags would use the
+    device-side slot waits, False when stream events."""
+    t = ctypes.c_int32()
+    _check(load().sc_stack_wait_kind(table, flags, ctypes.byref(t)))
+    return bool(t.value)
 
 
 def sc_table_stack_status(table, clear=False):

@@ -203,13 +203,15 @@ def test_single_visible_key_returns_its_value_row_exactly(dtype):
             assert np.array_equal(o[0, h], v[0, h // g]), (hq, hkv, d, h)
 
 
-@pytest.mark.parametrize("mode", ["overlap", "serial", "overlap-poison"])
+@pytest.mark.parametrize("mode", ["overlap", "serial", "overlap-poison", "overlap-event", "overlap-event-poison"])
 @pytest.mark.parametrize("name", ["stack_g4", "stack_varlen_host", "stack_rc", "stack_f16_rc"])
 def test_layer_stack_matches_oracle(name, mode):
     """The whole layer stack against the oracle, layer by layer, and the pool
     after every store.  "overlap-poison" overwrites each slot with NaN
     patterns before it is refilled, so an attention that ran ahead of its
-    slot's fetch and append would leave NaN rows."""
+    slot's fetch and append would leave NaN rows.  The "event" modes order
+    the two streams with stream events instead of device-side waits (the
+    path taken when dispatches are serialised)."""
     sc = require_gpu()
     import torch
     if name == "stack_g4":
@@ -231,7 +233,10 @@ def test_layer_stack_matches_oracle(name, mode):
         slots = [new_active(sc, wl) for _ in range(2)]
         copy = torch.cuda.Stream()
         flags = {"overlap": sc.SC_STACK_OVERLAP, "serial": sc.SC_STACK_SERIAL,
-                 "overlap-poison": sc.SC_STACK_OVERLAP | sc.SC_STACK_DEBUG_POISON}[mode]
+                 "overlap-poison": sc.SC_STACK_OVERLAP | sc.SC_STACK_DEBUG_POISON,
+                 "overlap-event": sc.SC_STACK_OVERLAP | sc.SC_STACK_EVENT_WAIT,
+                 "overlap-event-poison": sc.SC_STACK_OVERLAP | sc.SC_STACK_EVENT_WAIT | sc.SC_STACK_DEBUG_POISON,
+                 }[mode]
         sc.sc_prefill_stack(dp.handle, dp.table, [d[0].data_ptr() for d in dev],
                             [d[1].data_ptr() for d in dev], [d[2].data_ptr() for d in dev],
                             [o.data_ptr() for o in outs], [s[2] for s in slots], wl.n_q_heads, flags,
@@ -380,6 +385,45 @@ def test_forced_slot_wait_timeout_is_reported_and_recoverable(which):
             compare_attention(to_u16(outs[l]), o_ref, f"after recovery, layer {l}", wl.dtype)
         with pytest.raises(sc.SwiftCacheError):
             run(sc.SC_STACK_SERIAL | flag)
+        with pytest.raises(sc.SwiftCacheError) as e:       # event waits have no device wait to time out
+            run(sc.SC_STACK_OVERLAP | sc.SC_STACK_EVENT_WAIT | flag)
+        assert e.value.status == sc.SC_ERR_UNSUPPORTED
+    finally:
+        dp.close()
+
+
+def test_stack_under_serialised_dispatch_uses_event_waits():
+    """With AMD_SERIALIZE_KERNEL set (each kernel waits for the previous
+    one, as under counter collection), a device-side slot wait could only
+    time out; the library then orders the streams with events.  A child
+    process runs an overlapped stack in that environment and compares every
+    layer with the oracle; it must report no time-out."""
+    require_gpu()
+    import json
+    import os
+    import subprocess
+    import sys
+    env = dict(os.environ, AMD_SERIALIZE_KERNEL="3")
+    child = os.path.join(os.path.dirname(__file__), "_stack_child.py")
+    print("[serialised] child stack with AMD_SERIALIZE_KERNEL=3", flush=True)
+    r = subprocess.run([sys.executable, "-u", child], env=env, capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, r.stdout[-2000:] + r.stderr[-2000:]
+    res = json.loads(r.stdout.strip().splitlines()[-1])
+    assert res["device_wait"] is False, res
+    assert res["timed_out"] is False and res["layers_ok"] == res["layers"], res
+
+
+def test_stack_wait_kind():
+    """Without a serialising environment an overlapped stack at head_dim 128
+    waits on the device; SC_STACK_EVENT_WAIT and the other modes do not."""
+    sc = require_gpu()
+    wl = W.small_workload(207, [100], [20], 1, 32, 8, 128)
+    dp = DevicePool(sc, wl, W.pool_numpy(wl))
+    try:
+        assert sc.sc_stack_wait_kind(dp.table, sc.SC_STACK_OVERLAP)
+        assert not sc.sc_stack_wait_kind(dp.table, sc.SC_STACK_OVERLAP | sc.SC_STACK_EVENT_WAIT)
+        assert not sc.sc_stack_wait_kind(dp.table, sc.SC_STACK_SERIAL)
+        assert not sc.sc_stack_wait_kind(dp.table, sc.SC_STACK_ATTN_ONLY)
     finally:
         dp.close()
 
