@@ -124,11 +124,11 @@ def test_layer_path_matches_oracle(name, q_scale):
             torch.cuda.synchronize()
             compare_attention(to_u16(out), o_ref, f"{name} layer {layer} varlen", wl.dtype)
             lse_g = lse.cpu().numpy().astype(np.float64)[:, :wl.total_q]
-            # The kernel's denominator sums the probabilities rounded to the
-            # element type (the same weights that multiply V), each within
-            # 2^-9 (bf16) or 2^-11 (fp16) relative of its exact value, so
-            # ln l is off by at most about 2^-9 plus fp32 accumulation:
-            # 2^-8 bounds it.
+            # The kernel's denominator sums the probabilities in fp32
+            # (head_dim 128) or rounded to the element type (head_dim 64:
+            # the weights that multiply V, each within 2^-9 (bf16) or 2^-11
+            # (fp16) relative of its exact value), so ln l is off by at most
+            # about 2^-9 plus fp32 accumulation: 2^-8 bounds it.
             np.testing.assert_allclose(lse_g, lse_ref, atol=2.0 ** -8, rtol=1e-4)
             if wl.batch == 1 and not wl.n_rc_blocks:
                 out1 = torch.empty_like(out)
@@ -464,6 +464,42 @@ def test_chunked_stack_matches_oracle(name, chunk, mode):
             compare_attention(to_u16(outs[l]), o_ref, f"{name} chunk {chunk} layer {l}", wl.dtype)
             expect = ok.store_layer(expect, wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, l, kn, vn)
         assert np.array_equal(dp.full_u16(), expect)
+    finally:
+        dp.close()
+
+
+@pytest.mark.parametrize("name", ["host_tier", "rc_host", "f16_host"])
+def test_dma_fetch_matches_oracle(name):
+    """The KV Load with the host tier moved by the DMA engines (one
+    host-to-device copy per block half and layer): the same bytes as the
+    fetch kernel, prefix rows outside the regular cache bit-exact and every
+    other row untouched; the batched-copy variant either gives the same
+    bytes or reports that the runtime lacks it.  The table's totals match
+    the workload."""
+    sc = require_gpu()
+    import torch
+    wl = _case(name)
+    pool_u16 = W.pool_numpy(wl)
+    dp = DevicePool(sc, wl, pool_u16)
+    stream = torch.cuda.current_stream().cuda_stream
+    try:
+        assert sc.sc_table_totals(dp.table) == (wl.total_q, wl.total_kv)
+        pre = _prefix_rows(wl) & ~_rc_rows(wl)
+        for layer in range(wl.n_layers):
+            k_act, v_act = ok.gather_layer(pool_u16, wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, layer)
+            for per_copy in (True, False):
+                k, v, act = new_active(sc, wl, fill_bits=0xFFFF)
+                try:
+                    sc.sc_fetch_layer_kv_dma(dp.handle, dp.table, layer, act, per_copy_calls=per_copy, stream=stream)
+                except sc.SwiftCacheError as e:
+                    assert not per_copy and e.status == sc.SC_ERR_UNSUPPORTED, e
+                    continue
+                torch.cuda.synchronize()
+                kg, vg = to_u16(k), to_u16(v)
+                what = f"{name} layer {layer} per_copy={per_copy}"
+                assert np.array_equal(kg[pre], k_act[pre]), f"{what}: K"
+                assert np.array_equal(vg[pre], v_act[pre]), f"{what}: V"
+                assert np.all(kg[~pre] == 0xFFFF) and np.all(vg[~pre] == 0xFFFF), what
     finally:
         dp.close()
 
