@@ -55,11 +55,11 @@ ROTATE_BYTES = 512 << 20         # destination buffers the standalone fetch cycl
 # with the hash of the attention source they were taken on; a stale entry
 # (the source changed since) is reported as null.
 PMC_TRAFFIC = {
-    "llama3-8b-P8192-N512": (80482318, "7e4f7fe1afabdf87"),
-    "llama3-8b-batch16-varlen": (708725889, "7e4f7fe1afabdf87"),
-    "qwen-14b-P32768-N1024": (363890106, "7e4f7fe1afabdf87"),
-    "llama3-8b-P131072-N2048-hosttier": (1190534633, "7e4f7fe1afabdf87"),
-    "llama3-8b-P8192-N512-rc0.5": (79912278, "7e4f7fe1afabdf87"),
+    "llama3-8b-P8192-N512": (80457170, "545c5444e79913ba"),
+    "llama3-8b-batch16-varlen": (703592740, "545c5444e79913ba"),
+    "qwen-14b-P32768-N1024": (363977370, "545c5444e79913ba"),
+    "llama3-8b-P131072-N2048-hosttier": (1190857483, "545c5444e79913ba"),
+    "llama3-8b-P8192-N512-rc0.5": (79857606, "545c5444e79913ba"),
 }
 
 

@@ -36,12 +36,12 @@
 // rounded to bf16, for a fixed permutation of the 16 keys of each MFMA step.
 // V^T operands come from the row-major V tile through LDS transpose reads
 // (ds_read_b64_tr_b16: in each 16-lane group, lanes 4r..4r+3 read 4 dims
-// each of key r and lane j gets dim j of the 4 keys).  With head_dim 128
-// the row sum adds the fp32 probabilities before rounding, in two chains
-// (two v_add_f32 per pair measured 1-2% faster than one v_dot2c_f32_bf16
-// on the packed pair); the head_dim 64 loop and the rare re-reference path
-// sum the packed bf16 values with v_dot2c_f32_bf16.  Either sum differs
-// from the other by the rounding of P, far below the tolerance.
+// each of key r and lane j gets dim j of the 4 keys).  The row sum adds the
+// fp32 probabilities before rounding, in two chains (two v_add_f32 per pair
+// measured 1-2% faster at head_dim 128 and 2-4% at 64 than one
+// v_dot2c_f32_bf16 on the packed pair); it differs from the sum of the
+// rounded weights the PV product uses by the rounding of P, far below the
+// tolerance.
 //
 // Software pipeline.  A single wave issues MFMAs at half the SIMD's matrix
 // rate and VALU ops at half its vector rate, so each wave interleaves both:
@@ -135,7 +135,7 @@ struct Geo {
 // Element type of q, K, V, the probabilities of the PV product and the
 // output: bf16 or IEEE fp16 (the paper's serving precision, §5).  Operands
 // travel as raw 16-bit patterns; only the MFMA, the packing of fp32 values
-// (round to nearest even) and the pair sum depend on the type.
+// (round to nearest even) and the unpacking depend on the type.
 template <int DT>
 struct Elem;
 
@@ -153,11 +153,6 @@ struct Elem<SC_DTYPE_BF16> {
   static __device__ __forceinline__ uint32_t pack(float a, float b) {
     const bf16x2 p = {(__bf16)a, (__bf16)b};
     return __builtin_bit_cast(uint32_t, p);
-  }
-  // Sum of the two halves of `p` added to `acc` (v_dot2c_f32_bf16 with 1, 1).
-  static __device__ __forceinline__ float add_pair(uint32_t p, float acc) {
-    const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p), one, acc, false);
   }
   // Packed pair back to floats (exact).
   static __device__ __forceinline__ f32x2 unpack(uint32_t p) {
@@ -181,10 +176,6 @@ struct Elem<SC_DTYPE_F16> {
   static __device__ __forceinline__ uint32_t pack(float a, float b) {
     const f16x2 p = {(_Float16)a, (_Float16)b};
     return __builtin_bit_cast(uint32_t, p);
-  }
-  static __device__ __forceinline__ float add_pair(uint32_t p, float acc) {
-    const f16x2 one = {(_Float16)1.0f, (_Float16)1.0f};
-    return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, p), one, acc, false);
   }
   static __device__ __forceinline__ f32x2 unpack(uint32_t p) {
     const f16x2 h = __builtin_bit_cast(f16x2, p);
@@ -338,8 +329,8 @@ __device__ __forceinline__ float tile_max(const f32x16 &s, float sl2) {
   return max_with_other_half(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]))) * sl2;
 }
 
-// p = exp2(sl2 * s - m) for this lane's 16 keys, packed to bf16, and the sum
-// of the packed values (the weights the PV product uses).
+// p = exp2(sl2 * s - m) for this lane's 16 keys, packed to the element type,
+// and their fp32 sum (two chains).
 template <int DT>
 __device__ __forceinline__ float softmax_tile(const f32x16 &s, u32x4 (&pf)[2], float sl2, float m) {
   float r2[2] = {0.f, 0.f};
@@ -347,10 +338,11 @@ __device__ __forceinline__ float softmax_tile(const f32x16 &s, u32x4 (&pf)[2], f
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int e = 0; e < 8; e += 2) {
-      const uint32_t w = Elem<DT>::pack(__builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * t + e], sl2, -m)),
-                                   __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * t + e + 1], sl2, -m)));
-      pf[t][e >> 1] = w;
-      r2[t] = Elem<DT>::add_pair(w, r2[t]);
+      const float x0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * t + e], sl2, -m));
+      const float x1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * t + e + 1], sl2, -m));
+      pf[t][e >> 1] = Elem<DT>::pack(x0, x1);
+      r2[0] += x0;
+      r2[1] += x1;
     }
   return r2[0] + r2[1];
 }
