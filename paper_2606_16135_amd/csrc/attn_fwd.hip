@@ -46,15 +46,15 @@
 // Software pipeline.  A single wave issues MFMAs at half the SIMD's matrix
 // rate and VALU ops at half its vector rate, so each wave interleaves both:
 // iteration j issues QK(j+1) and PV(j-1) (16 MFMAs) in the same basic block
-// as the softmax of tile j, and both waves of a SIMD do so.  With head_dim
-// 128 one exponential per score already costs as much SIMD time as the two
-// MFMA products, so the softmax is cut to its minimum: p = exp2(c s - m),
-// the bf16 packing and the row sum.  The reference max m is the exact max
-// of the first tile and moves only when a lane's tile sum exceeds
-// kSumLimit: softmax is invariant to the reference, and fp32/bf16 keep their
-// relative precision at any scale, so a stale reference changes nothing but
-// the exponent range, which the limit bounds.  No per-tile row max is
-// computed on the common path.
+// as the softmax of tile j, and both waves of a SIMD do so.  The MFMAs do
+// not hide the vector work completely (measured: each vector instruction
+// per score costs 2-3% of the loop), so the softmax is cut to its minimum:
+// p = exp2(c s - m), the bf16 packing and the row sum.  The reference max m
+// is the exact max of the first tile and moves only when a lane's tile sum
+// exceeds kSumLimit: softmax is invariant to the reference, and fp32/bf16
+// keep their relative precision at any scale, so a stale reference changes
+// nothing but the exponent range, which the limit bounds.  No per-tile row
+// max is computed on the common path.
 //
 // K and V tiles each live in a 4-entry LDS ring (slot = tile mod 4), and
 // iteration j reads K(j+1) and V(j-1).  With head_dim 128 the tiles go from

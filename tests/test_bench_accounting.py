@@ -36,3 +36,15 @@ def test_fetch_payload(bench):
     assert bench.fetch_payload_bytes(W.config(2, rc_fraction=0.5)) == 16 << 20
     wl = W.config(3)
     assert bench.fetch_payload_bytes(wl) == int(wl.prefix_len.sum()) * 4096
+
+
+def test_traffic_counters_match_the_attention_code(bench):
+    """Every benchmark workload has HBM byte counters, taken on the attention
+    code as it stands (the hash ignores comments): the bench line's
+    roofline.traffic is never stale or missing for them."""
+    code = bench._src_sha16("attn_fwd.hip")
+    for name in ("llama3-8b-P8192-N512", "llama3-8b-batch16-varlen", "qwen-14b-P32768-N1024",
+                 "llama3-8b-P131072-N2048-hosttier"):
+        nbytes, key = bench.PMC_TRAFFIC[name]
+        assert key == code, f"{name}: counters taken on code {key}, the source is now {code}"
+        assert nbytes > 0
