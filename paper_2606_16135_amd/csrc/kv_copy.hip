@@ -38,15 +38,34 @@ constexpr int kStorePolicy = 2;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// A record of 32-bit fields read through the constant address space: the
+// host writes the copy items before the launch and nothing writes them
+// during it, so a uniform index gives one scalar load, the item stays in
+// scalar registers and the buffer resources built from it need no
+// per-lane loop.  (Read as ordinary global memory, the fields came back
+// one dependent vector load at a time and every buffer access was wrapped
+// in a loop over the distinct resources of the wave.)
+typedef int32_t i32x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ CopyItem load_item(const CopyItem *p) {
+  static_assert(sizeof(CopyItem) == sizeof(i32x8), "one 32-byte record");
+  const i32x8 v = *(const __attribute__((address_space(4))) i32x8 *)p;
+  CopyItem r;
+  __builtin_memcpy(&r, &v, sizeof(r));
+  return r;
+}
+
 // poison: write nan2 over the destination instead of copying (fetch and
-// append into a slot whose gate timed out).
-template <int MODE>
+// append into a slot whose gate timed out).  kSerialStores: one store in
+// flight per wave (see launch_kv_copy).
+template <int MODE, bool kSerialStores>
 __device__ __forceinline__ void copy_rows(const CopyArgs &a, int g, bool poison = false, uint32_t nan2 = 0) {
   const int item_idx = g >> 1;
   const int is_v = g & 1;
-  const CopyItem it = a.items[item_idx];
+  const CopyItem it = load_item(a.items + item_idx);
   if (MODE != COPY_APPEND && !((a.tier_mask >> it.tier) & 1)) return;
-  const int64_t nchunks = ((int64_t)it.nrows * a.row_bytes) >> 4;
+  // One item is at most 256 rows of one KV layer (under 4 MiB), so 32-bit
+  // chunk indices and byte offsets cover it.
+  const int nchunks = (int)(((int64_t)it.nrows * a.row_bytes) >> 4);
   const int64_t half_off = is_v ? a.v_half_off : 0;
   const char *src;
   char *dst;
@@ -60,26 +79,28 @@ __device__ __forceinline__ void copy_rows(const CopyArgs &a, int g, bool poison 
     src = (is_v ? a.new_v : a.new_k) + it.src_row * a.row_bytes;
     dst = a.tier_base[it.tier] + it.pool_off + a.layer_off + half_off;
   }
-  // One item is at most 256 rows of one KV layer (under 4 MiB), so 32-bit
-  // byte offsets cover it.
-  const int bytes = (int)(nchunks * 16);
+  const int bytes = nchunks * 16;
+  // Lanes past the item's last chunk are not masked off: the buffer
+  // resources end at the item's last byte, so their loads return zeros and
+  // their stores are dropped by the hardware's range check.
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(src), (short)0, bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(dst, (short)0, bytes, 0x00020000);
-  for (int64_t base = 0; base < nchunks; base += (int64_t)kThreads * kUnroll) {
+  for (int base = 0; base < nchunks; base += kThreads * kUnroll) {
     u32x4 r[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int64_t idx = base + u * kThreads + threadIdx.x;
+      const int idx = base + u * kThreads + (int)threadIdx.x;
       if (poison)
         r[u] = u32x4{nan2, nan2, nan2, nan2};
-      else if (idx < nchunks)
-        r[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(idx * 16), 0, kLoadPolicy));
+      else
+        r[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, idx * 16, 0, kLoadPolicy));
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int64_t idx = base + u * kThreads + threadIdx.x;
-      if (idx < nchunks) __builtin_amdgcn_raw_buffer_store_b128(r[u], rd, (int)(idx * 16), 0, kStorePolicy);
+      const int idx = base + u * kThreads + (int)threadIdx.x;
+      if constexpr (kSerialStores) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __builtin_amdgcn_raw_buffer_store_b128(r[u], rd, idx * 16, 0, kStorePolicy);
     }
   }
 }
@@ -89,7 +110,10 @@ __device__ __forceinline__ void copy_rows(const CopyArgs &a, int g, bool poison 
 // 2 * n_items walks the halves with a stride of the grid size.
 template <int MODE>
 __device__ __forceinline__ void copy_all(const CopyArgs &a) {
-  for (int g = blockIdx.x; g < 2 * a.n_items; g += gridDim.x) copy_rows<MODE>(a, g);
+  if (a.serial_stores)
+    for (int g = blockIdx.x; g < 2 * a.n_items; g += gridDim.x) copy_rows<MODE, true>(a, g);
+  else
+    for (int g = blockIdx.x; g < 2 * a.n_items; g += gridDim.x) copy_rows<MODE, false>(a, g);
 }
 __global__ __launch_bounds__(kThreads) void kv_fetch_kernel(CopyArgs a) { copy_all<COPY_FETCH>(a); }
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(CopyArgs a) { copy_all<COPY_APPEND>(a); }
@@ -105,11 +129,11 @@ __global__ __launch_bounds__(kThreads) void kv_layer_copy_kernel(LayerCopyArgs a
   const int n2 = n1 + 2 * a.part[2].n_items;
   for (int g = blockIdx.x; g < n2; g += gridDim.x) {
     if (g < n0)
-      copy_rows<COPY_FETCH>(a.part[0], g, poison, a.nan2);
+      copy_rows<COPY_FETCH, true>(a.part[0], g, poison, a.nan2);
     else if (g < n1)
-      copy_rows<COPY_APPEND>(a.part[1], g - n0, poison, a.nan2);
+      copy_rows<COPY_APPEND, true>(a.part[1], g - n0, poison, a.nan2);
     else
-      copy_rows<COPY_STORE>(a.part[2], g - n1);
+      copy_rows<COPY_STORE, true>(a.part[2], g - n1);
   }
 }
 
@@ -161,9 +185,30 @@ int kv_copy_vgprs() {
   return m;
 }
 
-hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_reserve, int max_groups) {
-  if (a.n_items <= 0) return hipSuccess;
-  const int groups = max_groups > 0 && max_groups < 2 * a.n_items ? max_groups : 2 * a.n_items;
+// Workgroups of a copy kernel that the device runs at once (all CUs).
+int copy_resident_groups(const void *kernel, size_t lds_reserve) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, lds_reserve) != hipSuccess)
+    return 0;
+  return cus * per_cu;
+}
+
+hipError_t launch_kv_copy(const CopyArgs &args, hipStream_t stream, size_t lds_reserve, int max_groups) {
+  if (args.n_items <= 0) return hipSuccess;
+  const int groups = max_groups > 0 && max_groups < 2 * args.n_items ? max_groups : 2 * args.n_items;
+  const void *kernel = args.mode == COPY_FETCH    ? reinterpret_cast<const void *>(&kv_fetch_kernel)
+                       : args.mode == COPY_APPEND ? reinterpret_cast<const void *>(&kv_append_kernel)
+                                                  : reinterpret_cast<const void *>(&kv_store_kernel);
+  // Store policy, by measurement: when the whole grid is resident at once
+  // (one round of workgroups, e.g. the 8B shape's 32 MiB layer in 1024
+  // workgroups) or runs capped beside attention, one store in flight per
+  // wave (eight in flight: 11% slower there, and burstier writes slow the
+  // attention beside them); with several rounds of workgroups (128-330 MiB
+  // layers) eight in flight, 4-6% faster.
+  CopyArgs a = args;
+  a.serial_stores = (max_groups > 0 || groups <= copy_resident_groups(kernel, lds_reserve)) ? 1 : 0;
   const dim3 grid(groups), block(kThreads);
   if (a.mode == COPY_FETCH)
     hipLaunchKernelGGL(kv_fetch_kernel, grid, block, lds_reserve, stream, a);
@@ -174,9 +219,12 @@ hipError_t launch_kv_copy(const CopyArgs &a, hipStream_t stream, size_t lds_rese
   return hipGetLastError();
 }
 
-hipError_t launch_kv_layer_copy(const LayerCopyArgs &a, hipStream_t stream, size_t lds_reserve, int max_groups) {
-  const int halves = 2 * (a.part[0].n_items + a.part[1].n_items + a.part[2].n_items);
+hipError_t launch_kv_layer_copy(const LayerCopyArgs &args, hipStream_t stream, size_t lds_reserve, int max_groups) {
+  const int halves = 2 * (args.part[0].n_items + args.part[1].n_items + args.part[2].n_items);
   if (halves <= 0) return hipSuccess;
+  // Beside attention: one store in flight per wave (see launch_kv_copy;
+  // the kernel always stores that way).
+  const LayerCopyArgs &a = args;
   const int groups = max_groups > 0 && max_groups < halves ? max_groups : halves;
   hipLaunchKernelGGL(kv_layer_copy_kernel, dim3(groups), dim3(kThreads), lds_reserve, stream, a);
   return hipGetLastError();

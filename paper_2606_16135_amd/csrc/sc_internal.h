@@ -61,6 +61,7 @@ struct CopyArgs {
   char *act_v;
   const char *new_k;
   const char *new_v;
+  int32_t serial_stores;  // set by the launch: one store in flight per wave
 };
 
 // lds_reserve: bytes of LDS each copy workgroup reserves without using them
