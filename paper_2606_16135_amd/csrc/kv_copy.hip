@@ -5,23 +5,25 @@
 // All three move whole token rows (n_kv_heads * head_dim bf16 = row_bytes)
 // between a block of the block-major pool (§3.4) and a packed buffer, so one
 // body serves them: workgroup 2*i copies item i's K rows, workgroup 2*i+1
-// its V rows (a grid capped below 2 * n_items, as the overlapped layer stack
-// launches it beside attention, strides over the item halves).  A block slice of one layer is contiguous in the pool (K half
-// then V half, Eq. 1), and consecutive rows of a sequence are contiguous in
-// the active buffer, so each item is one contiguous range on both sides.
+// its V rows (a grid capped below 2 * n_items, as the overlapped layer
+// stack launches it beside attention, strides over the item halves).  A
+// block slice of one layer is contiguous in the pool (K half then V half,
+// Eq. 1), and consecutive rows of a sequence are contiguous in the active
+// buffer, so each item is one contiguous range on both sides.
 //
 // The overlapped layer stack launches all three of a layer in one grid
 // (kv_layer_copy_kernel) after a one-wave gate kernel that waits on the
 // device for the attention that last read the slot.
 //
 // HBM-bound: every lane moves 16-byte chunks with kUnroll loads in flight
-// before the matching stores, through buffer resources over the item's two
-// ranges.  Both sides are streamed once per call: the loads are
+// before the matching stores (one store or all of them in flight, see
+// launch_kv_copy), through buffer resources over the item's two ranges.
+// Both sides are streamed once per call: the loads are
 // system-coherent and non-temporal (sc0 sc1 nt: no cache keeps the source),
 // the stores non-temporal (nt), so neither evicts the attention's K/V
-// working set from L2.  Measured on MI355X against non-temporal loads, the
-// fetch of the 8B shape runs about 7% faster (11.9 vs 12.8 us per layer);
-// against cached stores, non-temporal stores about 6% faster.  The data a
+// working set from L2.  Measured on MI355X, every other combination of
+// cached and non-temporal loads and stores is slower (up to a third with
+// both cached).  The data a
 // copy reads was written by earlier kernels, whose completion wrote it back
 // beyond the caches.  Host-tier blocks are read or written through their
 // device-visible pinned mapping, over the host link.
