@@ -29,6 +29,10 @@
 // device-visible pinned mapping, over the host link.
 #include "sc_internal.h"
 
+#include <map>
+#include <mutex>
+#include <tuple>
+
 namespace sc {
 namespace {
 
@@ -187,14 +191,22 @@ int kv_copy_vgprs() {
   return m;
 }
 
-// Workgroups of a copy kernel that the device runs at once (all CUs).
+// Workgroups of a copy kernel that the device runs at once (all CUs),
+// computed once per (device, kernel, LDS reservation).
 int copy_resident_groups(const void *kernel, size_t lds_reserve) {
-  int dev = 0, cus = 0, per_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+  static std::mutex mu;
+  static std::map<std::tuple<int, const void *, size_t>, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  const auto key = std::make_tuple(dev, kernel, lds_reserve);
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, lds_reserve) != hipSuccess)
     return 0;
-  return cus * per_cu;
+  return cache[key] = cus * per_cu;
 }
 
 hipError_t launch_kv_copy(const CopyArgs &args, hipStream_t stream, size_t lds_reserve, int max_groups) {
