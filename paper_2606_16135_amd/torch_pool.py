@@ -75,6 +75,28 @@ class DevicePool:
             parts.append(r)
         return np.concatenate(parts).view(np.uint16)[:, None]
 
+    def ref_layer_u16(self, layer, ids):
+        """Layer `layer` of the pool blocks `ids` (table order), as a 6-D
+        uint16 array [len(ids)][1][2][B][H_kv][D]; only those blocks cross
+        to the host."""
+        wl = self.wl
+        shp = (2, wl.block_size, wl.n_kv_heads, wl.head_dim)
+        ids = np.asarray(ids, dtype=np.int64)
+        out = np.zeros((len(ids), 1) + shp, dtype=np.int16)
+        tiers = [(self.dev, 0, wl.n_device_blocks), (self.host, wl.n_device_blocks, wl.n_host_blocks),
+                 (self.rc, wl.rc_first_id, wl.n_rc_blocks)]
+        for t, first, n in tiers:
+            sel = np.nonzero((ids >= first) & (ids < first + n))[0]
+            if t is None or n == 0 or len(sel) == 0:
+                continue
+            v = t.view(torch.int16)[: n * wl.block_elems].view(n, wl.n_layers, *shp)[:, layer]
+            local = torch.from_numpy(ids[sel] - first)
+            if t.is_cuda:
+                out[sel, 0] = v.index_select(0, local.to(t.device)).cpu().numpy()
+            else:
+                out[sel, 0] = v[local].numpy()
+        return out.view(np.uint16)
+
     def full_u16(self):
         wl = self.wl
         parts = []

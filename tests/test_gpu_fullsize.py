@@ -9,8 +9,11 @@ overwritten with NaN patterns before it is refilled, so an attention that
 ran ahead of its slot's fetch and append would leave NaN rows.
 
 Checked layers: every layer of the 8B shape's plain run, layers {0, L/2,
-L-2, L-1} otherwise.  On each, against the oracle (which works from a host
-snapshot of the layer taken before the stack ran):
+L-2, L-1} otherwise, and the fetch alone on every other layer (fetched
+again after the stack and compared byte for byte with the oracle's gather
+of the pool, whose prefix rows the store never writes).  On each checked
+layer, against the oracle (which works from a host snapshot of the layer
+taken before the stack ran):
 
 * fetch + append: every byte of the active layer (all tokens, all KV heads)
   outside the regular-cache rows, which are never copied.  The two slots
@@ -132,5 +135,26 @@ def test_benchmark_shape_stack_matches_oracle(case):
             assert np.array_equal(after, expect), f"{case} layer {l}: store"
             print(f"[fullsize] {case} layer {l}: fetch/append ({src}) and store exact, attention on all "
                   f"{o_ref.shape[0] * o_ref.shape[1]} rows {stats} ({time.perf_counter() - t0:.1f} s)", flush=True)
+
+        # fetch of every other layer, byte for byte: the store never writes
+        # prefix rows, so the pool after the stack still defines them
+        _, cu_k = ok.seq_offsets(wl.prefix_len, wl.new_len)
+        pre = np.zeros(wl.total_kv, dtype=bool)
+        for b, p in enumerate(wl.prefix_len):
+            pre[cu_k[b]:cu_k[b] + p] = True
+        pre &= f
+        rest = [l for l in range(L) if l not in check_layers]
+        t0 = time.perf_counter()
+        for l in rest:
+            sub = dp.ref_layer_u16(l, ids)
+            k_act, v_act = ok.gather_layer(sub, local_ids, wl.cu_blocks, wl.prefix_len, wl.new_len, 0)
+            sc.sc_fetch_layer_kv(dp.handle, dp.table, l, slots[2], compute.cuda_stream)
+            torch.cuda.synchronize()
+            kg, vg = to_u16(slot_t[2][0]), to_u16(slot_t[2][1])
+            assert np.array_equal(kg[pre], k_act[pre]), f"{case} layer {l}: K fetch"
+            assert np.array_equal(vg[pre], v_act[pre]), f"{case} layer {l}: V fetch"
+        if rest:
+            print(f"[fullsize] {case}: fetch exact on the other {len(rest)} layers "
+                  f"({time.perf_counter() - t0:.1f} s)", flush=True)
     finally:
         dp.close()
