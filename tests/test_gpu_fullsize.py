@@ -8,8 +8,8 @@ runs (8B and varlen shapes) add SC_STACK_DEBUG_POISON: every slot is
 overwritten with NaN patterns before it is refilled, so an attention that
 ran ahead of its slot's fetch and append would leave NaN rows.
 
-Checked layers: every layer of the 8B shape's plain run, layers {0, L/2,
-L-2, L-1} otherwise, and the fetch alone on every other layer (fetched
+Checked layers: every layer of the 8B and varlen shapes' plain runs,
+layers {0, L/2, L-2, L-1} otherwise, and the fetch alone on every other layer (fetched
 again after the stack and compared byte for byte with the oracle's gather
 of the pool, whose prefix rows the store never writes).  On each checked
 layer, against the oracle (which works from a host snapshot of the layer
@@ -43,13 +43,13 @@ pytestmark = pytest.mark.gpu
 
 def _sub_pool(dp, layer, ids):
     """Layer `layer` of the referenced blocks only, in table order."""
-    return dp.layer_slice_u16(layer)[ids]
+    return dp.ref_layer_u16(layer, ids)
 
 
 # cfg, regular-cache fraction, element type, debug poison, q scale, layers checked
 CASES = {
     "2": (2, 0.0, "bf16", False, 1.0, "all"),
-    "3": (3, 0.0, "bf16", False, 1.0, "ends"),
+    "3": (3, 0.0, "bf16", False, 1.0, "all"),
     "4": (4, 0.0, "bf16", False, 1.0, "ends"),
     "5": (5, 0.0, "bf16", False, 1.0, "ends"),
     "2-peaky": (2, 0.0, "bf16", False, 8.0, "ends"),
