@@ -1140,7 +1140,16 @@ sc_status sc_pool_resize(sc_pool *pool, int64_t n_device_blocks) {
       // Work already queued (e.g. by tables since destroyed) may still read
       // the chunks about to go.
       SC_HIP(hipDeviceSynchronize());
-      while ((int64_t)pool->vmm_handles.size() > need) SC_HIP(vmm_release_last_chunk(pool));
+      while ((int64_t)pool->vmm_handles.size() > need) {
+        const hipError_t e = vmm_release_last_chunk(pool);
+        if (e != hipSuccess) {
+          // The chunk's handle is gone either way: keep every usable id
+          // mapped, so no later table can name a block of a lost chunk.
+          pool->dev_lent = std::min<int64_t>(pool->dev_lent,
+                                             (int64_t)pool->vmm_handles.size() * pool->vmm_chunk_blocks);
+          return fail_hip(e, "releasing HBM blocks");
+        }
+      }
     }
     while ((int64_t)pool->vmm_handles.size() < need) {
       hipError_t e = vmm_append_chunk(pool);
@@ -1329,7 +1338,9 @@ sc_status sc_table_create(sc_pool *pool, int32_t batch, const int32_t *block_ids
     std::lock_guard<std::mutex> lk(pool->mu);
     if (max_dev_id >= pool->dev_lent) {
       if (t->d_items) (void)hipFree(t->d_items);
+      if (t->d_rc_ids) (void)hipFree(t->d_rc_ids);
       t->d_items = nullptr;
+      t->d_rc_ids = nullptr;
       return fail(SC_ERR_RANGE, "the pool shrank below block %lld while the table was being created",
                   (long long)max_dev_id);
     }
