@@ -436,10 +436,18 @@ sc_status single_plan(int device, int P, int N, int hq, int hkv, int head_dim, A
     return SC_OK;
   }
   if (g_single_plans.size() >= 256) {
-    // Plans may still be referenced by queued kernels: drain before freeing.
+    // Plans may still be referenced by queued kernels: drain this device
+    // before freeing its plans (the caller made it current); other
+    // devices' plans stay.
     SC_HIP(hipDeviceSynchronize());
-    for (auto &kv : g_single_plans) free_plan(kv.second.get());
-    g_single_plans.clear();
+    for (auto i = g_single_plans.begin(); i != g_single_plans.end();) {
+      if (std::get<0>(i->first) == device) {
+        free_plan(i->second.get());
+        i = g_single_plans.erase(i);
+      } else {
+        ++i;
+      }
+    }
   }
   auto plan = std::make_unique<AttnPlan>();
   plan_attention({P}, {N}, hq, hkv, attn_slots(device), plan.get());
@@ -1726,9 +1734,8 @@ sc_status prefill_stack(sc_pool *pool, const sc_table *table, int32_t n_layers, 
   hipStream_t xs = ss ? ss->copy : (hipStream_t)copy_stream;
   // Split-key merges are deferred when every layer runs one plan with key
   // splits: the forward kernel of layer l merges layer l-1's partials
-  // (spread over its workgroups, before their own items; in the overlapped
-  // stack while they wait for their slot), and one merge kernel follows the
-  // last layer.  That saves a merge launch per layer and its ~6 us on the
+  // (chunks of rows claimed by its workgroups once their own items are
+  // done), and one merge kernel follows the last layer.  That saves a merge launch per layer and its ~6 us on the
   // 8B shape.  Partials alternate between two halves of one workspace,
   // held for the whole enqueue.
   const bool defer_merge = n_chunks == 1 && plans[0]->max_splits > 1;
