@@ -1,6 +1,6 @@
 """GPU parity of every C-ABI call against the oracle, element by element, on
 seeded inputs small enough for the dense oracle: several key tiles and query
-tiles with ragged tails, head groups 1/4/5/8, head_dim 64/128, bf16 and fp16 values, empty prefix,
+tiles with ragged tails, head groups 1/3/4/5/6/7/8/16, head_dim 64/128, bf16 and fp16 values, empty prefix,
 a batch with an empty new turn, split-key work, a half host-pinned pool, and
 tables whose leading blocks sit in the regular-cache tier (read in place by
 attention; their active-buffer rows hold NaN patterns the kernel must not
@@ -52,13 +52,20 @@ def _case(name):
         "bs1": lambda: sw(132, [50, 3], [9, 20], 1, 8, 8, 64, block_size=1),
         "many_seqs": lambda: sw(133, list(range(0, 400, 10)), [1 + (7 * i) % 40 for i in range(40)], 1, 16, 4, 64),
         "g16_d64": lambda: sw(134, [129], [100], 1, 32, 2, 64),
+        # groups that do not divide the 256-row workgroup (its last rows
+        # idle), as in 28/4 and 12/2 head layouts, and the largest group at
+        # head_dim 128
+        "g7_d128_split": lambda: sw(135, [3000], [45], 1, 28, 4, 128),
+        "g6_d64_varlen": lambda: sw(136, [500, 90], [37, 70], 2, 12, 2, 64),
+        "g3_d128_rc": lambda: sw(137, [800, 41], [60, 9], 1, 24, 8, 128, rc_fraction=0.5),
+        "g16_d128": lambda: sw(138, [300], [40], 1, 32, 2, 128),
     }[name]()
 
 
 CASES = ["cfg1", "g4_d128_ragged", "g5_d128", "g1_d64_P0", "g4_split_long", "varlen_batch",
          "varlen_empty_turn", "host_tier", "g8_d64", "rc_varlen", "rc_split_d128", "rc_whole_prefix",
          "rc_host", "f16_g4_d128_ragged", "f16_varlen", "f16_g5_split_rc", "f16_host", "bs256_rc", "bs1",
-         "many_seqs", "g16_d64"]
+         "many_seqs", "g16_d64", "g7_d128_split", "g6_d64_varlen", "g3_d128_rc", "g16_d128"]
 
 
 def _oracle_layer(wl, pool_u16, layer, q, kn, vn):
