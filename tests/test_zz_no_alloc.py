@@ -5,8 +5,10 @@ file-scope device array and derives each workgroup's work from its index;
 sc_prefill_attn allocates a workspace and uploads a work list.  Both run the
 same kernels over the same key splits, so their outputs (and log-sum-exps)
 must agree bit for bit; the outputs are also checked against the oracle.
-Two calls in a row, the second smaller, show that the shared array's
-leftover contents from the first call do not leak into the second.
+Calls in a row, each smaller than the one before, show that the shared
+array's leftover contents from an earlier call do not leak into a later
+one; the last also has a GQA group (7) that leaves rows of the 256-row
+workgroup idle, at head_dim 64.
 """
 
 import numpy as np
@@ -19,8 +21,8 @@ from _gpu_util import compare_attention, require_gpu, to_u16
 pytestmark = pytest.mark.gpu
 
 # (prefix, new turn, q heads, KV heads, head_dim): the 8B benchmark shape's
-# layer (4 key splits) first, then a smaller call.
-CALLS = [(8192, 512, 32, 8, 128), (3000, 200, 32, 8, 128)]
+# layer (4 key splits) first, then smaller calls.
+CALLS = [(8192, 512, 32, 8, 128), (3000, 200, 32, 8, 128), (1500, 90, 28, 4, 64)]
 
 
 def _inputs(torch, P, N, hq, hkv, d, seed):
@@ -33,7 +35,7 @@ def _inputs(torch, P, N, hq, hkv, d, seed):
 
 
 @pytest.mark.timeout(300)
-def test_noalloc_matches_allocating_entry_point_twice():
+def test_noalloc_matches_allocating_entry_point_on_successive_calls():
     sc = require_gpu()
     import torch
 
@@ -59,8 +61,8 @@ def test_noalloc_matches_allocating_entry_point_twice():
         stats = compare_attention(to_u16(out_n), o_ref, f"noalloc call {idx}")
         assert np.abs(lse_n.cpu().numpy() - lse_ref).max() <= 2.0 ** -8
         print(f"[noalloc] call {idx}: {splits} key splits, bit-identical to sc_prefill_attn, {stats}", flush=True)
-    if idx == 0:
-        pytest.fail("expected two calls")
+    if idx < 1:
+        pytest.fail("expected at least two calls")
 
 
 def test_noalloc_rejects_partials_beyond_its_array():
