@@ -686,7 +686,11 @@ sc_status split_streams(int device, SplitStreams **out) {
   }
   SplitStreams ss;
   SC_HIP(hipExtStreamCreateWithCUMask(&ss.attn, (uint32_t)words, attn_mask.data()));
-  SC_HIP(hipExtStreamCreateWithCUMask(&ss.copy, (uint32_t)words, copy_mask.data()));
+  const hipError_t e = hipExtStreamCreateWithCUMask(&ss.copy, (uint32_t)words, copy_mask.data());
+  if (e != hipSuccess) {
+    (void)hipStreamDestroy(ss.attn);
+    return fail_hip(e, "copy stream with a CU mask");
+  }
   ss.attn_cus = cus - kHostFetchCus;
   *out = &(g_split[device] = ss);
   return SC_OK;
