@@ -1,8 +1,10 @@
-"""A seeded random sweep of small workloads through the whole overlapped
-layer stack, against the oracle: batch 1-5, prefixes 0-2000 tokens (empty
-ones included, lengths not multiples of the block), new turns 0-200 tokens,
-head_dim 64 and 128, GQA groups 1-8, block sizes 8-64, half host-pinned
-pools, regular-cache tables, bf16 and fp16, 1-3 layers.  Each case checks
+"""A seeded random sweep of small workloads through the whole layer stack,
+against the oracle: batch 1-5, prefixes 0-3000 tokens (empty ones
+included, lengths not multiples of the block), new turns 0-300 tokens,
+head_dim 64 and 128, GQA groups 1-8 and 16, block sizes 8-128, half
+host-pinned pools, regular-cache tables, bf16 and fp16, 1-3 layers;
+overlapped stacks with device-side or event waits and serial stacks, whole
+or chunked new turns.  Each case checks
 every attention output element of every layer, the last layer's active slot
 byte for byte, and the pool after every store, so together they cover the
 combinations the hand-picked parity cases do not."""
@@ -16,28 +18,30 @@ from paper_2606_16135_amd import workloads as W
 
 from _gpu_util import DevicePool, compare_attention, from_u16, new_active, require_gpu, to_u16
 
-N_CASES = 40
+N_CASES = 60
 
 
 def random_case(i):
     """Workload parameters of sweep case i (pure function of i)."""
-    rng = np.random.default_rng(2606_16135_900 + i)
+    rng = np.random.default_rng(77_000 + i)
     batch = int(rng.integers(1, 6))
     head_dim = int(rng.choice([64, 128]))
-    n_kv = int(rng.choice([1, 2, 4, 8]))
-    group = int(rng.choice([1, 2, 4, 5, 8]))
-    block = int(rng.choice([8, 16, 32, 64]))
-    prefix = [int(rng.integers(0, 2001)) if rng.random() > 0.15 else 0 for _ in range(batch)]
-    new = [int(rng.integers(1, 201)) if rng.random() > 0.1 else 0 for _ in range(batch)]
+    group = int(rng.choice([1, 2, 3, 4, 5, 6, 7, 8, 16]))
+    n_kv = int(rng.choice([1, 2, 4, 8])) if group <= 8 else int(rng.choice([1, 2]))
+    block = int(rng.choice([8, 16, 32, 64, 128]))
+    prefix = [int(rng.integers(0, 3001)) if rng.random() > 0.15 else 0 for _ in range(batch)]
+    new = [int(rng.integers(1, 301)) if rng.random() > 0.1 else 0 for _ in range(batch)]
     if sum(new) == 0:
-        new[0] = int(rng.integers(1, 201))
+        new[0] = int(rng.integers(1, 301))
     host = float(rng.choice([0.0, 0.0, 0.4]))
     rc = float(rng.choice([0.0, 0.0, 0.5])) if block >= 16 else 0.0
     dtype = str(rng.choice(["bf16", "f16"]))
     layers = int(rng.integers(1, 4))
-    return dict(seed=2606_16135_900 + i, prefix_len=prefix, new_len=new, n_layers=layers,
+    mode = str(rng.choice(["overlap", "overlap", "serial", "event"]))
+    chunk = int(rng.choice([0, 0, 0, 32, 100]))
+    return dict(seed=77_000 + i, prefix_len=prefix, new_len=new, n_layers=layers,
                 n_q_heads=n_kv * group, n_kv_heads=n_kv, head_dim=head_dim, block_size=block,
-                host_fraction=host, rc_fraction=rc, dtype=dtype)
+                host_fraction=host, rc_fraction=rc, dtype=dtype, mode=mode, chunk=chunk)
 
 
 @pytest.mark.gpu
@@ -59,11 +63,16 @@ def test_random_stack_matches_oracle(i):
                            dtype=W.torch_dtype(wl), device="cuda") for _ in range(wl.n_layers)]
         slots = [new_active(sc, wl) for _ in range(2)]
         copy = torch.cuda.Stream()
-        sc.sc_prefill_stack(dp.handle, dp.table, [d[0].data_ptr() for d in dev],
-                            [d[1].data_ptr() for d in dev], [d[2].data_ptr() for d in dev],
-                            [o.data_ptr() for o in outs], [s[2] for s in slots], wl.n_q_heads,
-                            sc.SC_STACK_OVERLAP, 0.0, torch.cuda.current_stream().cuda_stream,
-                            copy.cuda_stream)
+        flags = {"overlap": sc.SC_STACK_OVERLAP, "serial": sc.SC_STACK_SERIAL,
+                 "event": sc.SC_STACK_OVERLAP | sc.SC_STACK_EVENT_WAIT}[p["mode"]]
+        args = (dp.handle, dp.table, [d[0].data_ptr() for d in dev], [d[1].data_ptr() for d in dev],
+                [d[2].data_ptr() for d in dev], [o.data_ptr() for o in outs], [s[2] for s in slots],
+                wl.n_q_heads)
+        cs = torch.cuda.current_stream().cuda_stream
+        if p["chunk"]:
+            sc.sc_prefill_stack_chunked(*args, p["chunk"], flags, 0.0, cs, copy.cuda_stream)
+        else:
+            sc.sc_prefill_stack(*args, flags, 0.0, cs, copy.cuda_stream)
         torch.cuda.synchronize()
         rc_rows = ok.regular_cache_rows(wl.block_ids, wl.cu_blocks, wl.prefix_len, wl.new_len,
                                         wl.block_size, wl.rc_first_id)
@@ -78,7 +87,7 @@ def test_random_stack_matches_oracle(i):
                                         oa.bits_to_f64(v_full, wl.dtype), wl.prefix_len, wl.new_len)
                 compare_attention(to_u16(outs[l])[:wl.total_q], o_ref, f"sweep {i} layer {l}", wl.dtype)
             if l == wl.n_layers - 1:
-                k_slot, v_slot, _ = slots[l & 1]
+                k_slot, v_slot, _ = slots[0] if p["mode"] == "serial" else slots[l & 1]
                 keep = ~rc_rows
                 assert np.array_equal(to_u16(k_slot)[keep], k_full[keep]), f"sweep {i}: K slot"
                 assert np.array_equal(to_u16(v_slot)[keep], v_full[keep]), f"sweep {i}: V slot"
@@ -95,8 +104,11 @@ def test_sweep_covers_the_stated_combinations():
     assert random_case(7) == random_case(7)
     assert {c["head_dim"] for c in cases} == {64, 128}
     assert {c["dtype"] for c in cases} == {"bf16", "f16"}
-    assert {c["n_q_heads"] // c["n_kv_heads"] for c in cases} >= {1, 2, 4, 5, 8}
-    assert {c["block_size"] for c in cases} == {8, 16, 32, 64}
+    assert {c["n_q_heads"] // c["n_kv_heads"] for c in cases} == {1, 2, 3, 4, 5, 6, 7, 8, 16}
+    assert {c["block_size"] for c in cases} == {8, 16, 32, 64, 128}
+    assert {c["mode"] for c in cases} == {"overlap", "serial", "event"}
+    assert any(c["chunk"] for c in cases) and any(not c["chunk"] for c in cases)
+    assert all(any(c["chunk"] and c["mode"] == m for c in cases) for m in ("overlap", "serial", "event"))
     assert any(c["host_fraction"] > 0 for c in cases) and any(c["rc_fraction"] > 0 for c in cases)
     assert any(c["host_fraction"] > 0 and c["rc_fraction"] > 0 for c in cases)
     assert any(0 in c["prefix_len"] for c in cases) and any(0 in c["new_len"] for c in cases)
