@@ -322,8 +322,8 @@ def run_workload(args, cfg, torch, sc, W, DevicePool, with_cpu, turn=None, rc_fr
                              "slices of the pool"}
     if host_b == 0:
         gbs = 2.0 * payload / t_fetch / 1e9
-        fetch.update({"hbm_gbs": round(gbs, 1), "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
-                      "bound": "hbm"})
+        fetch.update({"hbm_gbs": round(gbs, 1), "payload_gbs": round(gbs / 2.0, 1),
+                      "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4), "bound": "hbm"})
         fetch["plain_copy_reference"] = plain_copy_reference(torch, timed, copy, payload)
         fetch["vs_plain_copy"] = round(fetch["plain_copy_reference"]["us"] / (t_fetch * 1e6), 3)
     else:
@@ -332,6 +332,8 @@ def run_workload(args, cfg, torch, sc, W, DevicePool, with_cpu, turn=None, rc_fr
     entry = {
         "workload": wl.name, "description": wl.description,
         "value": round(value, 1), "unit": "tokens/s", "ms_per_step": round(ms_step, 3),
+        # every token the step's attention covers (prefix + new turn), per second
+        "context_tokens_per_s": round(float(np.sum(wl.prefix_len) + wl.total_q) * args.steps / elapsed, 1),
         "steps": args.steps, "warmup": args.warmup,
         "shape": {"layers": L, "q_heads": wl.n_q_heads, "kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
                   "batch": wl.batch, "prefix_len_total": int(np.sum(wl.prefix_len)),
