@@ -55,11 +55,11 @@ ROTATE_BYTES = 512 << 20         # destination buffers the standalone fetch cycl
 # with the hash of the attention source's code (comments left out) they were
 # taken on; a stale entry (the code changed since) is reported as null.
 PMC_TRAFFIC = {
-    "llama3-8b-P8192-N512": (80457170, "65c624ed31e7ca8d"),
-    "llama3-8b-batch16-varlen": (703592740, "65c624ed31e7ca8d"),
-    "qwen-14b-P32768-N1024": (363977370, "65c624ed31e7ca8d"),
-    "llama3-8b-P131072-N2048-hosttier": (1190857483, "65c624ed31e7ca8d"),
-    "llama3-8b-P8192-N512-rc0.5": (79857606, "65c624ed31e7ca8d"),
+    "llama3-8b-P8192-N512": (80481765, "4ba710f1265470eb"),
+    "llama3-8b-batch16-varlen": (705816836, "4ba710f1265470eb"),
+    "qwen-14b-P32768-N1024": (364153977, "4ba710f1265470eb"),
+    "llama3-8b-P131072-N2048-hosttier": (1191660843, "4ba710f1265470eb"),
+    "llama3-8b-P8192-N512-rc0.5": (79959614, "4ba710f1265470eb"),
 }
 
 

@@ -88,7 +88,8 @@ typedef struct sc_table sc_table;   /* opaque, library-owned */
  * [n_device_blocks + n_host_blocks, ... + n_rc_blocks) address the regular
  * cache (§3.2 "Regular Cache"): full-layer blocks in the master's own HBM,
  * which attention reads in place through the block table instead of
- * fetching them (needs a power-of-two block_size of at least 16).
+ * fetching them (needs a power-of-two block_size of at least 16 and blocks
+ * under 4 GiB over all layers; SC_ERR_UNSUPPORTED otherwise).
  *
  * device_base / host_base: when non-NULL the pool indexes caller-owned
  * memory of at least n_device_blocks * block_bytes (device memory on

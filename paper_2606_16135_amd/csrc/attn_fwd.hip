@@ -550,7 +550,13 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
     // pair of iterations before the tile's data load.
     const __attribute__((address_space(4))) int32_t *rc_ids_c =
         kPaged ? (const __attribute__((address_space(4))) int32_t *)(a.rc_ids + sd.rc_off) : nullptr;
-    const uint16_t *rc_layer = kPaged ? a.rc_base + a.rc_layer_elems : nullptr;
+    // This KV head's K and V rows in block 0 of the layer; block b is
+    // b * rc_block_bytes further (under 4 GiB, checked on the host), so the
+    // per-tile address is a 32 x 32 -> 64-bit product and two adds.
+    const char *rc_kbase =
+        kPaged ? reinterpret_cast<const char *>(a.rc_base + a.rc_layer_elems + (int64_t)wi.kvh * D) : nullptr;
+    const char *rc_vbase = kPaged ? rc_kbase + a.rc_half_elems * 2 : nullptr;
+    const uint32_t rc_block_bytes = kPaged ? (uint32_t)(a.rc_block_elems * 2) : 0u;
     const int rc_mask = (1 << a.block_shift) - 1;
     auto blk_of = [&](int t) -> int {
       if constexpr (!kPaged) {
@@ -571,9 +577,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs &a, const WorkItem &wi,
       if constexpr (kPaged) {
         const int rib = min(key, k_end - 1) & rc_mask;   // first row within the block
         const int rows = min(rc_mask + 1 - rib, k_end - key);
-        base = reinterpret_cast<const char *>(rc_layer + (int64_t)blk * a.rc_block_elems +
-                                              (kV ? a.rc_half_elems : 0) + (int64_t)rib * kv_stride +
-                                              (int64_t)wi.kvh * D);
+        base = (kV ? rc_vbase : rc_kbase) + (uint64_t)(uint32_t)blk * rc_block_bytes + (uint32_t)(rib * row_bytes);
         range = rows > 0 ? ((rows - 1) * row_bytes + 2 * D) : 0;
       } else {
         // Signed 32-bit offsets (the host keeps a sequence's keys, plus the

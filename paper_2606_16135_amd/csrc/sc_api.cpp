@@ -1042,6 +1042,11 @@ sc_status sc_pool_create(const sc_pool_desc *desc, sc_pool **out) {
   if (d.n_rc_blocks > 0 && (d.block_size < 16 || (d.block_size & (d.block_size - 1)) != 0))
     return fail(SC_ERR_UNSUPPORTED, "a regular cache needs a power-of-two block size >= 16 (got %d)",
                 d.block_size);
+  // Attention addresses a regular-cache block as block index x block bytes
+  // in 32 x 32-bit arithmetic.
+  if (d.n_rc_blocks > 0 &&
+      (int64_t)d.n_layers * 2 * d.block_size * d.n_kv_heads * d.head_dim * 2 >= ((int64_t)1 << 32))
+    return fail(SC_ERR_UNSUPPORTED, "a regular cache needs blocks under 4 GiB (all layers, K and V)");
   if (!aligned16(d.device_base) || !aligned16(d.host_base) || !aligned16(d.rc_base))
     return fail(SC_ERR_INVALID, "caller-owned pool tiers must be 16-byte aligned");
   // Pools over caller-owned HBM without a host tier make no HIP call here.
