@@ -117,6 +117,13 @@ def test_regular_cache_pool_validation(sc):
     with pytest.raises(sc.SwiftCacheError) as e:
         sc.sc_pool_create(2, 2, 64, 16, 8, 0, 0, FAKE_BASE, 0, -1, FAKE_BASE)
     assert e.value.status == sc.SC_ERR_INVALID
+    # attention addresses a regular-cache block in 32-bit products: blocks
+    # (all layers, K and V) must stay under 4 GiB; 512 layers x 2 x 256 rows
+    # x 64 heads x 128 x 2 bytes is exactly 4 GiB, 511 layers is under
+    with pytest.raises(sc.SwiftCacheError) as e:
+        sc.sc_pool_create(512, 64, 128, 256, 0, 0, 0, 0, 0, 1, FAKE_BASE)
+    assert e.value.status == sc.SC_ERR_UNSUPPORTED and "4 GiB" in str(e.value)
+    sc.sc_pool_destroy(sc.sc_pool_create(511, 64, 128, 256, 0, 0, 0, 0, 0, 1, FAKE_BASE))
     p = sc.sc_pool_create(2, 2, 64, 16, 0, 0, 0, 0, 0, 4, FAKE_BASE)   # a regular cache alone
     try:
         lay = sc.sc_pool_layout_get(p)
